@@ -1,0 +1,146 @@
+/*
+ * gs.h -- C ABI of the gs-SGD gradient-compression hot path on one AMD Instinct MI355X.
+ *
+ * Method: Dai, Diao, Li, Xu, "A Distributed SGD Algorithm with Global Sketching for Deep
+ * Learning Training Acceleration" (arXiv 2108.06004). Per training iteration every worker
+ * accumulates momentum and error feedback into its flat gradient, compresses the result
+ * into a Count Sketch, the P sketches are summed along a binomial tree (Alg. 1), the top-k
+ * coordinates are recovered from the summed sketch, and their exact values are fetched
+ * and removed from the error accumulators (HEAVYMIX, Alg. 2).
+ *
+ * One GPU holds all P workers: per-worker arrays are stacked row-major as [P][d].
+ *
+ * Conventions shared by every call
+ *   - Array arguments are DEVICE pointers to memory owned by the caller (for example
+ *     torch tensors on the GPU). The library never frees or retains them beyond the call.
+ *     fp32 arrays are IEEE binary32; index arrays are int32. Arrays are dense, row-major,
+ *     and must not overlap unless a call says it works in place.
+ *   - `stream` is a hipStream_t passed as void* (NULL is the default stream). Every call
+ *     validates its arguments on the host, enqueues its kernels on `stream` and returns
+ *     without waiting; outputs are valid once the stream has been synchronized.
+ *   - The return value is the only error channel. GS_ERR_INVALID_ARG is returned before
+ *     anything is enqueued; GS_ERR_DEVICE reports a launch or runtime failure (details in
+ *     gs_last_error). No call aborts the process or throws across the ABI.
+ *   - Calls on one context must not overlap on different streams: the context's scratch
+ *     memory (histograms, candidate lists, bitmaps, internal tables) is shared by them.
+ *     Different contexts are independent.
+ *   - Inputs must be finite; results for NaN or infinite inputs are unspecified.
+ */
+#ifndef GS_H
+#define GS_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gs_status {
+  GS_OK = 0,
+  GS_ERR_INVALID_ARG = 1,   /* argument check failed; nothing was enqueued            */
+  GS_ERR_OUT_OF_MEMORY = 2, /* gs_create could not allocate its device scratch        */
+  GS_ERR_DEVICE = 3,        /* a HIP launch or runtime call failed                    */
+  GS_ERR_UNSUPPORTED = 4    /* shape outside what this build implements               */
+} gs_status;
+
+#define GS_MAX_WORKERS 64
+#define GS_MAX_ROWS 16
+#define GS_MERSENNE_P 2147483647u /* 2^31 - 1 */
+
+/*
+ * Problem description (Alg. 1 inputs: k, P; the Count Sketch of Sec. III-A).
+ *   d        coordinates per worker, 1 <= d <= p - 1 (so every index is a valid hash input)
+ *   P        workers, 1 <= P <= GS_MAX_WORKERS
+ *   r, c     sketch rows and columns, 1 <= r <= GS_MAX_ROWS, 1 <= c <= p - 1
+ *   k_max    the largest k any call on this context may request, 1 <= k_max <= d
+ *   rho      momentum factor of the accumulation u <- rho*u + g (finite)
+ *   reset_momentum  1: the reset after selection zeroes u as well as v; 0: only v
+ *   hash_a, hash_b  HOST arrays [r]: bucket hash h_j(i) = ((a_j*i + b_j) mod p) mod c
+ *   sign_a, sign_b  HOST arrays [r]: sign s_j(i) = +1 if ((a_j*i + b_j) mod p) is odd, else -1
+ *                   with 1 <= a < p and 0 <= b < p for all four; copied by gs_create.
+ */
+typedef struct gs_config {
+  int64_t d;
+  int32_t P;
+  int32_t r;
+  int64_t c;
+  int64_t k_max;
+  float rho;
+  int32_t reset_momentum;
+  const uint32_t* hash_a;
+  const uint32_t* hash_b;
+  const uint32_t* sign_a;
+  const uint32_t* sign_b;
+} gs_config;
+
+typedef struct gs_ctx gs_ctx; /* opaque: a copy of the config plus device scratch */
+
+/* Validate `cfg`, copy it, and allocate the device scratch on the current HIP device.
+ * This is the only call that allocates. On success *out receives the context. */
+gs_status gs_create(const gs_config* cfg, gs_ctx** out);
+
+/* Free the context's scratch (after synchronizing the device). NULL is accepted. */
+gs_status gs_destroy(gs_ctx* ctx);
+
+/* Momentum and error-feedback accumulation (Sec. II, sketching paragraph: momentum and
+ * error accumulation carried along with the sketch; Alg. 1 starts from a zero state).
+ * For every worker q and coordinate i, in IEEE fp32 with each operation rounded:
+ *     u[q][i] = rho * u[q][i] + g[q][i];   v[q][i] = v[q][i] + u[q][i].
+ * g: [P][d] input. u, v: [P][d], updated in place. */
+gs_status gs_accumulate(gs_ctx* ctx, void* stream, const float* g, float* u, float* v);
+
+/* Count Sketch of every worker's accumulator (Sec. III-A; Alg. 1 sketch step):
+ *     tables[q][j][col] = sum over i with h_j(i) == col of s_j(i) * v[q][i].
+ * v: [P][d] input. tables: [P][r][c] output (overwritten; fp32 cell sums whose rounding
+ * depends on the summation order). */
+gs_status gs_sketch(gs_ctx* ctx, void* stream, const float* v, float* tables);
+
+/* Sum of the P worker sketches in the binomial-tree order of Alg. 1 (in each round the
+ * even local rank adds the next rank's sketch; an unpaired highest rank passes through).
+ * tables: [P][r][c] input. merged: [r][c] output. Deterministic. */
+gs_status gs_merge(gs_ctx* ctx, void* stream, const float* tables, float* merged);
+
+/* HEAVYMIX estimate and selection (Alg. 2). For every coordinate i the estimate is the
+ * median over rows of s_j(i) * merged[j][h_j(i)] (even r: mean of the two middle values,
+ * fl(fl(m1 + m2) * 0.5)). idx receives the k coordinates with the largest |estimate|,
+ * ties broken toward the lower index, in ascending order.
+ * merged: [r][c] input. est: [d] output, or NULL when not wanted. idx: [k] output.
+ * 1 <= k <= k_max. */
+gs_status gs_unsketch_topk(gs_ctx* ctx, void* stream, const float* merged, int64_t k, float* est, int32_t* idx);
+
+/* Exact values of the selected coordinates (Alg. 2, second round) and their reset.
+ * For t < k, with i = idx[t]: values[t] = tree-order sum over q of v[q][i] (the merge
+ * order above); then v[q][i] = 0 for every q, and u[q][i] = 0 too when reset_momentum.
+ * idx: [k] distinct coordinates in [0, d) (e.g. the output of gs_unsketch_topk).
+ * u, v: [P][d], updated in place. values: [k] output. 1 <= k <= k_max. */
+gs_status gs_gather_reset(gs_ctx* ctx, void* stream, const int32_t* idx, int64_t k, float* u, float* v,
+                          float* values);
+
+/* One whole step: accumulate, sketch, merge, estimate + top-k, exact values + reset, with
+ * the per-worker tables kept in context scratch. Equivalent to the five calls above.
+ * g: [P][d] input. u, v: [P][d] in place. merged: [r][c] output. idx, values: [k] outputs. */
+gs_status gs_step(gs_ctx* ctx, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
+                  int32_t* idx, float* values);
+
+/* Stage timing for benchmarks and profiling. Runs exactly the kernels of gs_step, records a
+ * HIP event on `stream` before the first stage and after each stage, synchronizes the stream
+ * and writes the stage durations in milliseconds to the HOST array stage_ms[GS_NUM_STAGES]:
+ *   [0] accumulate   [1] sketch (0 when fused into [0])   [2] merge
+ *   [3] estimate + top-k selection                        [4] gather + reset
+ * Unlike gs_step this call blocks until the step has finished. */
+#define GS_NUM_STAGES 5
+gs_status gs_step_profiled(gs_ctx* ctx, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
+                           int32_t* idx, float* values, float* stage_ms);
+
+/* Static description of a status code. */
+const char* gs_status_string(gs_status status);
+
+/* Message describing the last failing call on `ctx` ("" if none); valid until the next
+ * call on the context. With ctx == NULL: the last gs_create failure on this thread. */
+const char* gs_last_error(const gs_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GS_H */

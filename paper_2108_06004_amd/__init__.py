@@ -1,0 +1,250 @@
+"""Python binding of the gs-SGD compression hot path (C ABI in include/gs.h).
+
+Argument marshalling only: every computation runs in the HIP kernels of ``libgs.so``.
+Tensors are torch CUDA (ROCm) tensors owned by the caller; the stream is torch's current
+stream unless one is given. There is no CPU fallback: if ``libgs.so`` has not been built,
+loading raises ``GsLibraryMissing``.
+
+Names follow the C ABI: ``gs_create``, ``gs_accumulate``, ``gs_sketch``, ``gs_merge``,
+``gs_unsketch_topk``, ``gs_gather_reset``, ``gs_step``, ``gs_destroy``. ``GsContext``
+bundles them with shape checks.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgs.so")
+
+GS_OK, GS_ERR_INVALID_ARG, GS_ERR_OUT_OF_MEMORY, GS_ERR_DEVICE, GS_ERR_UNSUPPORTED = range(5)
+GS_MAX_WORKERS = 64
+GS_MAX_ROWS = 16
+EXPORTED = ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
+            "gs_gather_reset", "gs_step", "gs_step_profiled", "gs_status_string", "gs_last_error")
+GS_NUM_STAGES = 5
+STAGES = ("accumulate", "sketch", "merge", "select", "gather_reset")
+
+
+class GsLibraryMissing(RuntimeError):
+    pass
+
+
+class GsError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+class gs_config(ctypes.Structure):
+    _fields_ = [
+        ("d", ctypes.c_int64),
+        ("P", ctypes.c_int32),
+        ("r", ctypes.c_int32),
+        ("c", ctypes.c_int64),
+        ("k_max", ctypes.c_int64),
+        ("rho", ctypes.c_float),
+        ("reset_momentum", ctypes.c_int32),
+        ("hash_a", ctypes.POINTER(ctypes.c_uint32)),
+        ("hash_b", ctypes.POINTER(ctypes.c_uint32)),
+        ("sign_a", ctypes.POINTER(ctypes.c_uint32)),
+        ("sign_b", ctypes.POINTER(ctypes.c_uint32)),
+    ]
+
+
+_lib = None
+
+
+def load_library():
+    """Load libgs.so (built in-tree by ``__graft_entry__.build()``)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise GsLibraryMissing(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i64, st = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    lib.gs_create.argtypes = [ctypes.POINTER(gs_config), ctypes.POINTER(vp)]
+    lib.gs_destroy.argtypes = [vp]
+    lib.gs_accumulate.argtypes = [vp, vp, vp, vp, vp]
+    lib.gs_sketch.argtypes = [vp, vp, vp, vp]
+    lib.gs_merge.argtypes = [vp, vp, vp, vp]
+    lib.gs_unsketch_topk.argtypes = [vp, vp, vp, i64, vp, vp]
+    lib.gs_gather_reset.argtypes = [vp, vp, vp, i64, vp, vp, vp]
+    lib.gs_step.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp]
+    lib.gs_step_profiled.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp, vp]
+    for name in ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
+                 "gs_gather_reset", "gs_step", "gs_step_profiled"):
+        getattr(lib, name).restype = st
+    lib.gs_status_string.argtypes = [st]
+    lib.gs_status_string.restype = ctypes.c_char_p
+    lib.gs_last_error.argtypes = [vp]
+    lib.gs_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(status: int, ctx=None, what: str = ""):
+    if status != GS_OK:
+        lib = load_library()
+        detail = lib.gs_last_error(ctx).decode() if lib.gs_last_error(ctx) is not None else ""
+        raise GsError(status, f"{what}: {lib.gs_status_string(status).decode()}: {detail}")
+
+
+def _ptr(t, dtype=None, numel=None, name="tensor"):
+    """Device pointer of a contiguous CUDA tensor after shape/dtype checks (None -> NULL)."""
+    if t is None:
+        return None
+    import torch
+
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} must have {numel} elements, got {t.numel()}")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    import torch
+
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def gs_create(d: int, P: int, r: int, c: int, k_max: int, hash_a, hash_b, sign_a, sign_b, rho: float = 0.9,
+              reset_momentum: bool = True) -> int:
+    """Create a context on the current device; returns the opaque handle (an int)."""
+    lib = load_library()
+    arrs = [np.ascontiguousarray(a, dtype=np.uint32) for a in (hash_a, hash_b, sign_a, sign_b)]
+    if any(a.size != r for a in arrs):
+        raise ValueError("hash parameter arrays must have r entries")
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    cfg = gs_config(d, P, r, c, k_max, rho, int(bool(reset_momentum)), *(a.ctypes.data_as(u32p) for a in arrs))
+    out = ctypes.c_void_p()
+    _check(lib.gs_create(ctypes.byref(cfg), ctypes.byref(out)), None, "gs_create")
+    return out.value
+
+
+def gs_destroy(ctx: int) -> None:
+    _check(load_library().gs_destroy(ctx), None, "gs_destroy")
+
+
+def gs_accumulate(ctx: int, g, u, v, stream=None) -> None:
+    _check(load_library().gs_accumulate(ctx, _stream(stream), _ptr(g, name="g"), _ptr(u, name="u"),
+                                        _ptr(v, name="v")), ctx, "gs_accumulate")
+
+
+def gs_sketch(ctx: int, v, tables, stream=None) -> None:
+    _check(load_library().gs_sketch(ctx, _stream(stream), _ptr(v, name="v"), _ptr(tables, name="tables")), ctx,
+           "gs_sketch")
+
+
+def gs_merge(ctx: int, tables, merged, stream=None) -> None:
+    _check(load_library().gs_merge(ctx, _stream(stream), _ptr(tables, name="tables"), _ptr(merged, name="merged")),
+           ctx, "gs_merge")
+
+
+def gs_unsketch_topk(ctx: int, merged, k: int, est, idx, stream=None) -> None:
+    _check(load_library().gs_unsketch_topk(ctx, _stream(stream), _ptr(merged, name="merged"), k,
+                                           _ptr(est, name="est"), _ptr(idx, name="idx")), ctx, "gs_unsketch_topk")
+
+
+def gs_gather_reset(ctx: int, idx, k: int, u, v, values, stream=None) -> None:
+    _check(load_library().gs_gather_reset(ctx, _stream(stream), _ptr(idx, name="idx"), k, _ptr(u, name="u"),
+                                          _ptr(v, name="v"), _ptr(values, name="values")), ctx, "gs_gather_reset")
+
+
+def gs_step(ctx: int, g, u, v, k: int, merged, idx, values, stream=None) -> None:
+    _check(load_library().gs_step(ctx, _stream(stream), _ptr(g, name="g"), _ptr(u, name="u"), _ptr(v, name="v"), k,
+                                  _ptr(merged, name="merged"), _ptr(idx, name="idx"), _ptr(values, name="values")),
+           ctx, "gs_step")
+
+
+def gs_step_profiled(ctx: int, g, u, v, k: int, merged, idx, values, stream=None) -> dict:
+    """gs_step with per-stage HIP-event timing (blocks until done); returns stage -> ms."""
+    ms = (ctypes.c_float * GS_NUM_STAGES)()
+    _check(load_library().gs_step_profiled(ctx, _stream(stream), _ptr(g, name="g"), _ptr(u, name="u"),
+                                           _ptr(v, name="v"), k, _ptr(merged, name="merged"), _ptr(idx, name="idx"),
+                                           _ptr(values, name="values"), ms), ctx, "gs_step_profiled")
+    return dict(zip(STAGES, [float(x) for x in ms]))
+
+
+class GsContext:
+    """A context plus shape/dtype checks on every call."""
+
+    def __init__(self, d: int, P: int, r: int, c: int, k_max: int, hash_params: dict, rho: float = 0.9,
+                 reset_momentum: bool = True):
+        self.d, self.P, self.r, self.c, self.k_max = d, P, r, c, k_max
+        self.handle = gs_create(d, P, r, c, k_max, hash_params["a"], hash_params["b"], hash_params["a2"],
+                                hash_params["b2"], rho, reset_momentum)
+
+    def close(self):
+        if self.handle:
+            gs_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _f32(self, t, n, name):
+        import torch
+
+        _ptr(t, torch.float32, n, name)
+        return t
+
+    def accumulate(self, g, u, v, stream=None):
+        n = self.P * self.d
+        gs_accumulate(self.handle, self._f32(g, n, "g"), self._f32(u, n, "u"), self._f32(v, n, "v"), stream)
+
+    def sketch(self, v, tables, stream=None):
+        gs_sketch(self.handle, self._f32(v, self.P * self.d, "v"), self._f32(tables, self.P * self.r * self.c,
+                                                                             "tables"), stream)
+
+    def merge(self, tables, merged, stream=None):
+        gs_merge(self.handle, self._f32(tables, self.P * self.r * self.c, "tables"),
+                 self._f32(merged, self.r * self.c, "merged"), stream)
+
+    def unsketch_topk(self, merged, k, idx, est=None, stream=None):
+        import torch
+
+        _ptr(idx, torch.int32, k, "idx")
+        if est is not None:
+            self._f32(est, self.d, "est")
+        gs_unsketch_topk(self.handle, self._f32(merged, self.r * self.c, "merged"), k, est, idx, stream)
+
+    def gather_reset(self, idx, k, u, v, values, stream=None):
+        import torch
+
+        _ptr(idx, torch.int32, k, "idx")
+        n = self.P * self.d
+        gs_gather_reset(self.handle, idx, k, self._f32(u, n, "u"), self._f32(v, n, "v"),
+                        self._f32(values, k, "values"), stream)
+
+    def step(self, g, u, v, k, merged, idx, values, stream=None):
+        import torch
+
+        n = self.P * self.d
+        _ptr(idx, torch.int32, k, "idx")
+        gs_step(self.handle, self._f32(g, n, "g"), self._f32(u, n, "u"), self._f32(v, n, "v"), k,
+                self._f32(merged, self.r * self.c, "merged"), idx, self._f32(values, k, "values"), stream)
+
+    def step_profiled(self, g, u, v, k, merged, idx, values, stream=None) -> dict:
+        import torch
+
+        n = self.P * self.d
+        _ptr(idx, torch.int32, k, "idx")
+        return gs_step_profiled(self.handle, self._f32(g, n, "g"), self._f32(u, n, "u"), self._f32(v, n, "v"), k,
+                                self._f32(merged, self.r * self.c, "merged"), idx, self._f32(values, k, "values"),
+                                stream)

@@ -1,0 +1,260 @@
+// gs_api.hip -- the C ABI declared in include/gs.h: argument validation, the context and
+// its device scratch, and the kernel sequence of each call.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "../../include/gs.h"
+#include "gs_internal.hpp"
+
+namespace {
+
+thread_local std::string g_create_error;
+
+constexpr int64_t kP = GS_MERSENNE_P;
+
+gs_status fail(gs_ctx* x, gs_status st, const std::string& msg) {
+  if (x) x->last_error = msg;
+  return st;
+}
+
+gs_status device_status(gs_ctx* x, hipError_t e, const char* where) {
+  if (e == hipSuccess) return GS_OK;
+  return fail(x, GS_ERR_DEVICE, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+// Granlund-Montgomery reciprocal for 31-bit dividends: l = ceil(log2 c), m = ceil(2^(31+l)/c).
+void set_divisor(gs::HashSet& hs, uint32_t c) {
+  hs.c = c;
+  hs.magic = 0;
+  hs.shift = 0;
+  if (c < 2) return;
+  uint32_t l = 0;
+  while ((1ull << l) < c) ++l;
+  const uint64_t num = 1ull << (31 + l);
+  hs.magic = (uint32_t)((num + c - 1) / c);
+  hs.shift = l - 1;
+}
+
+template <typename T>
+hipError_t alloc(T** p, int64_t count) {
+  *p = nullptr;
+  if (count <= 0) count = 1;
+  return hipMalloc(reinterpret_cast<void**>(p), (size_t)count * sizeof(T));
+}
+
+void free_scratch(gs_ctx* x) {
+  void* ptrs[] = {x->keys, x->hist, x->ctl, x->cand_key, x->cand_idx, x->bitmap, x->blockcnt, x->acc64};
+  for (void* p : ptrs)
+    if (p) (void)hipFree(p);
+  x->keys = nullptr;
+  x->hist = nullptr;
+  x->ctl = nullptr;
+  x->cand_key = nullptr;
+  x->cand_idx = nullptr;
+  x->bitmap = nullptr;
+  x->blockcnt = nullptr;
+  x->acc64 = nullptr;
+}
+
+bool valid_ab(const uint32_t* a, const uint32_t* b, int r) {
+  for (int j = 0; j < r; ++j)
+    if (a[j] < 1 || (int64_t)a[j] >= kP || (int64_t)b[j] >= kP) return false;
+  return true;
+}
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+const char* gs_status_string(gs_status st) {
+  switch (st) {
+    case GS_OK: return "ok";
+    case GS_ERR_INVALID_ARG: return "invalid argument";
+    case GS_ERR_OUT_OF_MEMORY: return "out of device memory";
+    case GS_ERR_DEVICE: return "device error";
+    case GS_ERR_UNSUPPORTED: return "unsupported";
+  }
+  return "unknown status";
+}
+
+const char* gs_last_error(const gs_ctx* x) { return x ? x->last_error.c_str() : g_create_error.c_str(); }
+
+gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
+  g_create_error.clear();
+  auto bad = [](const char* m) {
+    g_create_error = m;
+    return GS_ERR_INVALID_ARG;
+  };
+  if (!out) return bad("out is NULL");
+  *out = nullptr;
+  if (!cfg) return bad("cfg is NULL");
+  if (cfg->d < 1 || cfg->d > kP - 1) return bad("d must satisfy 1 <= d <= 2^31 - 2");
+  if (cfg->P < 1 || cfg->P > GS_MAX_WORKERS) return bad("P must satisfy 1 <= P <= GS_MAX_WORKERS");
+  if (cfg->r < 1 || cfg->r > GS_MAX_ROWS) return bad("r must satisfy 1 <= r <= GS_MAX_ROWS");
+  if (cfg->c < 1 || cfg->c > kP - 1) return bad("c must satisfy 1 <= c <= 2^31 - 2");
+  if (cfg->k_max < 1 || cfg->k_max > cfg->d) return bad("k_max must satisfy 1 <= k_max <= d");
+  if (!std::isfinite(cfg->rho)) return bad("rho must be finite");
+  if (!cfg->hash_a || !cfg->hash_b || !cfg->sign_a || !cfg->sign_b) return bad("hash parameter array is NULL");
+  if (!valid_ab(cfg->hash_a, cfg->hash_b, cfg->r) || !valid_ab(cfg->sign_a, cfg->sign_b, cfg->r))
+    return bad("hash parameters must satisfy 1 <= a < p and 0 <= b < p");
+  if ((int64_t)cfg->P * cfg->r * cfg->c > (int64_t)1 << 40) return bad("P*r*c too large");
+
+  gs_ctx* x = new (std::nothrow) gs_ctx();
+  if (!x) {
+    g_create_error = "host allocation failed";
+    return GS_ERR_OUT_OF_MEMORY;
+  }
+  x->d = cfg->d;
+  x->c = cfg->c;
+  x->k_max = cfg->k_max;
+  x->P = cfg->P;
+  x->r = cfg->r;
+  x->rho = cfg->rho;
+  x->reset_momentum = cfg->reset_momentum ? 1 : 0;
+  x->hs.r = cfg->r;
+  for (int j = 0; j < cfg->r; ++j) {
+    x->hs.row[j].a = cfg->hash_a[j];
+    x->hs.row[j].b = cfg->hash_b[j];
+    x->hs.row[j].a2 = cfg->sign_a[j];
+    x->hs.row[j].b2 = cfg->sign_b[j];
+  }
+  set_divisor(x->hs, (uint32_t)cfg->c);
+
+  hipError_t e = hipGetDevice(&x->device);
+  if (e == hipSuccess) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, x->device);
+    if (e == hipSuccess) x->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
+  }
+  if (e != hipSuccess) {
+    g_create_error = std::string("HIP device query failed: ") + hipGetErrorString(e);
+    delete x;
+    return GS_ERR_DEVICE;
+  }
+
+  x->cand_cap = x->d;
+  x->emit_blocks = gs::emit_blocks_for(x->d);
+  const int64_t words = (x->d + 31) / 32;
+  hipError_t ea = hipSuccess;
+  auto chk = [&](hipError_t r) {
+    if (ea == hipSuccess) ea = r;
+  };
+  chk(alloc(&x->keys, x->d));
+  chk(alloc(&x->hist, gs::kDigit1Bins));
+  chk(alloc(&x->ctl, 1));
+  chk(alloc(&x->cand_key, x->cand_cap));
+  chk(alloc(&x->cand_idx, x->cand_cap));
+  chk(alloc(&x->bitmap, words));
+  chk(alloc(&x->blockcnt, x->emit_blocks));
+  chk(alloc(&x->acc64, (int64_t)x->P * x->r * x->c));
+  if (ea == hipSuccess) ea = hipMemset(x->hist, 0, gs::kDigit1Bins * sizeof(uint32_t));
+  if (ea == hipSuccess) ea = hipMemset(x->ctl, 0, sizeof(gs::SelectCtl));
+  if (ea == hipSuccess) ea = hipDeviceSynchronize();
+  if (ea != hipSuccess) {
+    const bool oom = ea == hipErrorOutOfMemory || ea == hipErrorMemoryAllocation;
+    g_create_error = std::string("device scratch allocation failed: ") + hipGetErrorString(ea);
+    (void)hipGetLastError();
+    free_scratch(x);
+    delete x;
+    return oom ? GS_ERR_OUT_OF_MEMORY : GS_ERR_DEVICE;
+  }
+  *out = x;
+  return GS_OK;
+}
+
+gs_status gs_destroy(gs_ctx* x) {
+  if (!x) return GS_OK;
+  hipError_t e = hipDeviceSynchronize();
+  free_scratch(x);
+  delete x;
+  return e == hipSuccess ? GS_OK : GS_ERR_DEVICE;
+}
+
+gs_status gs_accumulate(gs_ctx* x, void* stream, const float* g, float* u, float* v) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!g || !u || !v) return fail(x, GS_ERR_INVALID_ARG, "gs_accumulate: NULL array");
+  return device_status(x, gs::launch_accumulate(x, as_stream(stream), g, u, v), "gs_accumulate");
+}
+
+gs_status gs_sketch(gs_ctx* x, void* stream, const float* v, float* tables) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!v || !tables) return fail(x, GS_ERR_INVALID_ARG, "gs_sketch: NULL array");
+  return device_status(x, gs::launch_sketch(x, as_stream(stream), v, tables), "gs_sketch");
+}
+
+gs_status gs_merge(gs_ctx* x, void* stream, const float* tables, float* merged) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!tables || !merged) return fail(x, GS_ERR_INVALID_ARG, "gs_merge: NULL array");
+  return device_status(x, gs::launch_merge(x, as_stream(stream), tables, merged), "gs_merge");
+}
+
+gs_status gs_unsketch_topk(gs_ctx* x, void* stream, const float* merged, int64_t k, float* est, int32_t* idx) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!merged || !idx) return fail(x, GS_ERR_INVALID_ARG, "gs_unsketch_topk: NULL array");
+  if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_unsketch_topk: k must satisfy 1 <= k <= k_max");
+  return device_status(x, gs::launch_unsketch_topk(x, as_stream(stream), merged, k, est, idx), "gs_unsketch_topk");
+}
+
+gs_status gs_gather_reset(gs_ctx* x, void* stream, const int32_t* idx, int64_t k, float* u, float* v,
+                          float* values) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!idx || !u || !v || !values) return fail(x, GS_ERR_INVALID_ARG, "gs_gather_reset: NULL array");
+  if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_gather_reset: k must satisfy 1 <= k <= k_max");
+  return device_status(x, gs::launch_gather_reset(x, as_stream(stream), idx, k, u, v, values), "gs_gather_reset");
+}
+
+gs_status gs_step(gs_ctx* x, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
+                  int32_t* idx, float* values) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!g || !u || !v || !merged || !idx || !values) return fail(x, GS_ERR_INVALID_ARG, "gs_step: NULL array");
+  if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_step: k must satisfy 1 <= k <= k_max");
+  hipStream_t s = as_stream(stream);
+  hipError_t e = gs::launch_accumulate(x, s, g, u, v);
+  if (e == hipSuccess) e = gs::launch_sketch_acc(x, s, v);
+  if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
+  if (e == hipSuccess) e = gs::launch_unsketch_topk(x, s, merged, k, nullptr, idx);
+  if (e == hipSuccess) e = gs::launch_gather_reset(x, s, idx, k, u, v, values);
+  return device_status(x, e, "gs_step");
+}
+
+gs_status gs_step_profiled(gs_ctx* x, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
+                           int32_t* idx, float* values, float* stage_ms) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!g || !u || !v || !merged || !idx || !values || !stage_ms)
+    return fail(x, GS_ERR_INVALID_ARG, "gs_step_profiled: NULL array");
+  if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_step_profiled: k must satisfy 1 <= k <= k_max");
+  hipStream_t s = as_stream(stream);
+  hipEvent_t ev[GS_NUM_STAGES + 1] = {};
+  hipError_t e = hipSuccess;
+  for (int t = 0; t <= GS_NUM_STAGES && e == hipSuccess; ++t) e = hipEventCreate(&ev[t]);
+  if (e == hipSuccess) e = hipEventRecord(ev[0], s);
+  if (e == hipSuccess) e = gs::launch_accumulate(x, s, g, u, v);
+  if (e == hipSuccess) e = hipEventRecord(ev[1], s);
+  if (e == hipSuccess) e = gs::launch_sketch_acc(x, s, v);
+  if (e == hipSuccess) e = hipEventRecord(ev[2], s);
+  if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
+  if (e == hipSuccess) e = hipEventRecord(ev[3], s);
+  if (e == hipSuccess) e = gs::launch_unsketch_topk(x, s, merged, k, nullptr, idx);
+  if (e == hipSuccess) e = hipEventRecord(ev[4], s);
+  if (e == hipSuccess) e = gs::launch_gather_reset(x, s, idx, k, u, v, values);
+  if (e == hipSuccess) e = hipEventRecord(ev[5], s);
+  if (e == hipSuccess) e = hipEventSynchronize(ev[5]);
+  for (int t = 0; t < GS_NUM_STAGES && e == hipSuccess; ++t) e = hipEventElapsedTime(&stage_ms[t], ev[t], ev[t + 1]);
+  for (int t = 0; t <= GS_NUM_STAGES; ++t)
+    if (ev[t]) (void)hipEventDestroy(ev[t]);
+  return device_status(x, e, "gs_step_profiled");
+}
+
+}  // extern "C"

@@ -1,0 +1,66 @@
+// gs_internal.hpp -- host-side context and kernel launchers shared by the library's
+// translation units. Not part of the public ABI (include/gs.h is).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "gs_device.hpp"
+
+// Top-k selection works on 32-bit keys (the bits of |estimate|) in three radix digits.
+namespace gs {
+constexpr int kDigit1Shift = 20;  // digit 1: key bits 31..20 (11 bits: the sign bit is 0)
+constexpr int kDigit1Bins = 2048;
+constexpr int kDigitBins = 1024;  // digits 2 and 3: key bits 19..10 and 9..0
+
+// Device-resident control block of the selection (one per context).
+struct SelectCtl {
+  uint32_t k;           // number to select
+  uint32_t b1;          // digit-1 bucket holding the k-th key
+  uint32_t above1;      // keys in digit-1 buckets above b1
+  uint32_t n_cand;      // candidates appended by the compaction pass (digit 1 >= b1)
+  uint32_t tau;         // the k-th largest key
+  uint32_t iota;        // largest index taken among keys equal to tau
+  uint32_t status;      // 0 ok; nonzero: candidate overflow (must not happen)
+  uint32_t pad;
+};
+}  // namespace gs
+
+struct gs_ctx {
+  int device = 0;
+  int64_t d = 0, c = 0, k_max = 0;
+  int32_t P = 0, r = 0;
+  float rho = 0.f;
+  int32_t reset_momentum = 1;
+  gs::HashSet hs{};
+  int num_cus = 256;
+
+  // scratch (device)
+  uint32_t* keys = nullptr;       // [d]
+  uint32_t* hist = nullptr;       // [kDigit1Bins], zero between calls
+  gs::SelectCtl* ctl = nullptr;   // [1]
+  uint32_t* cand_key = nullptr;   // [cand_cap]
+  int32_t* cand_idx = nullptr;    // [cand_cap]
+  int64_t cand_cap = 0;
+  uint32_t* bitmap = nullptr;     // [ceil(d/32)]
+  uint32_t* blockcnt = nullptr;   // [emit blocks]
+  int64_t emit_blocks = 0;
+  double* acc64 = nullptr;        // [P][r][c] fp64 cell accumulators of the sketch
+
+  std::string last_error;
+};
+
+namespace gs {
+// Launchers (each enqueues on `s` and returns hipGetLastError()).
+hipError_t launch_accumulate(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v);
+hipError_t launch_fill_zero(hipStream_t s, float* p, int64_t n);
+hipError_t launch_sketch_acc(const gs_ctx* x, hipStream_t s, const float* v);
+hipError_t launch_sketch(const gs_ctx* x, hipStream_t s, const float* v, float* tables);
+hipError_t launch_merge_acc(const gs_ctx* x, hipStream_t s, float* merged);
+hipError_t launch_merge(const gs_ctx* x, hipStream_t s, const float* tables, float* merged);
+hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, float* est, int32_t* idx);
+hipError_t launch_gather_reset(const gs_ctx* x, hipStream_t s, const int32_t* idx, int64_t k, float* u, float* v,
+                               float* values);
+int64_t emit_blocks_for(int64_t d);
+}  // namespace gs

@@ -1,0 +1,368 @@
+// k_select.hip -- HEAVYMIX estimate and deterministic top-k selection (Alg. 2).
+//
+// Estimate: est_i = median over rows of s_j(i) * S[j][h_j(i)] (register sorting network).
+// Selection: the k largest |est_i|, ties toward the lower index, output ascending. Keys are
+// the bit patterns of |est_i| (non-negative floats order like unsigned integers). The k-th
+// key is found by a most-significant-digit radix select entirely on the device (no host
+// synchronisation inside the call):
+//   1. unsketch: keys + histogram of digit 1 (key bits 31..20) in LDS, flushed to global;
+//   2. select1 (one block): the digit-1 bucket b1 holding the k-th key;
+//   3. compact: every key with digit 1 >= b1 is appended to a candidate list (wave ballot,
+//      one atomic per wave); the output bitmap is cleared on the way;
+//   4. select2 (one block): digits 2 and 3 over the candidates give the k-th key tau and how
+//      many keys equal to tau are taken; if not all of them, three index digits find the
+//      largest index iota taken among them (lowest indices win);
+//   5. finalize: candidates with key > tau, or key == tau and index <= iota, set their bit;
+//   6. emit: the bitmap is turned into ascending indices (per-block popcounts, then a
+//      block-local scan offset by the preceding blocks' totals).
+#include "gs_internal.hpp"
+
+namespace gs {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kSelBlock = 1024;
+constexpr int kEmitWordsPerThread = 4;
+constexpr int kEmitWordsPerBlock = kSelBlock * kEmitWordsPerThread;
+
+int grid_for(int64_t work_items, int per_block, int cap) {
+  int64_t b = (work_items + per_block - 1) / per_block;
+  if (b < 1) b = 1;
+  if (b > cap) b = cap;
+  return (int)b;
+}
+
+// Inclusive prefix sum of x over the threads of a block of BS threads (BS a multiple of 64,
+// at most 64 waves). sh must hold BS/64 words. All threads must call it.
+template <int BS>
+__device__ uint32_t block_scan_incl(uint32_t x, uint32_t* sh, uint32_t& total) {
+  constexpr int kWaves = BS / 64;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sh[wid] = x;
+  __syncthreads();
+  if (wid == 0) {
+    uint32_t w = lane < kWaves ? sh[lane] : 0u;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(w, o, 64);
+      if (lane >= o) w += y;
+    }
+    if (lane < kWaves) sh[lane] = w;
+  }
+  __syncthreads();
+  total = sh[kWaves - 1];
+  const uint32_t add = wid ? sh[wid - 1] : 0u;
+  __syncthreads();
+  return x + add;
+}
+
+// Scan the LDS histogram h[nbins] (nbins = 1024 or 2048) in descending or ascending bin
+// order and find the first bin at which the running count reaches `need` (1 <= need <=
+// total). res[0] = that bin, res[1] = count in the bins before it (in scan order).
+__device__ void find_bucket(const uint32_t* h, int nbins, bool descending, uint32_t need, uint32_t* shw,
+                            uint32_t* res) {
+  const int per = nbins / kSelBlock;
+  uint32_t cnt[2] = {0u, 0u};
+  int bin[2] = {0, 0};
+  uint32_t sum = 0;
+  for (int m = 0; m < per; ++m) {
+    const int pos = threadIdx.x * per + m;
+    bin[m] = descending ? nbins - 1 - pos : pos;
+    cnt[m] = h[bin[m]];
+    sum += cnt[m];
+  }
+  uint32_t total;
+  const uint32_t incl = block_scan_incl<kSelBlock>(sum, shw, total);
+  const uint32_t excl = incl - sum;
+  if (excl < need && need <= incl) {
+    uint32_t run = excl;
+    for (int m = 0; m < per; ++m) {
+      if (run + cnt[m] >= need) {
+        res[0] = (uint32_t)bin[m];
+        res[1] = run;
+        break;
+      }
+      run += cnt[m];
+    }
+  }
+  __syncthreads();
+}
+
+// ------------------------------------------------------------------------------------
+// 1. Estimate (HEAVYMIX query) + keys + digit-1 histogram.
+
+template <int R>
+__global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __restrict__ merged, int64_t d,
+                                                     float* __restrict__ est, uint32_t* __restrict__ keys,
+                                                     uint32_t* __restrict__ hist) {
+  __shared__ uint32_t h[kDigit1Bins];
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
+  __syncthreads();
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < d; i += stride) {
+    float val[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      uint32_t col, sflip;
+      hash_ij(hs, j, (uint32_t)i, col, sflip);
+      val[j] = apply_sign(merged[(int64_t)j * hs.c + col], sflip);
+    }
+    sort_net<R>(val);
+    const float e = median_sorted<R>(val);
+    if (est) est[i] = e;
+    const uint32_t key = abs_key(e);
+    keys[i] = key;
+    atomicAdd(&h[key >> kDigit1Shift], 1u);
+  }
+  __syncthreads();
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) {
+    const uint32_t n = h[b];
+    if (n) atomicAdd(&hist[b], n);
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// 2. Digit-1 bucket of the k-th key. Clears the histogram for the next call and the
+// candidate counter for the compaction pass.
+
+__global__ void __launch_bounds__(kSelBlock) k_select1(uint32_t* __restrict__ hist, SelectCtl* __restrict__ ctl,
+                                                       uint32_t k) {
+  __shared__ uint32_t h[kDigit1Bins];
+  __shared__ uint32_t shw[kSelBlock / 64];
+  __shared__ uint32_t res[2];
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) {
+    h[b] = hist[b];
+    hist[b] = 0u;
+  }
+  __syncthreads();
+  find_bucket(h, kDigit1Bins, true, k, shw, res);
+  if (threadIdx.x == 0) {
+    ctl->k = k;
+    ctl->b1 = res[0];
+    ctl->above1 = res[1];
+    ctl->n_cand = 0u;
+    ctl->status = 0u;
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// 3. Candidate compaction (digit 1 >= b1) and bitmap clearing.
+
+__global__ void __launch_bounds__(kBlock) k_compact(const uint32_t* __restrict__ keys, int64_t d,
+                                                    SelectCtl* __restrict__ ctl, uint32_t* __restrict__ cand_key,
+                                                    int32_t* __restrict__ cand_idx, int64_t cap,
+                                                    uint32_t* __restrict__ bitmap) {
+  const uint32_t b1 = ctl->b1;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave0 = ((int64_t)blockIdx.x * kBlock + (threadIdx.x & ~63));
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t base = wave0; base < d; base += stride) {  // uniform per wave
+    const int64_t i = base + lane;
+    const bool valid = i < d;
+    const uint32_t key = valid ? keys[i] : 0u;
+    const bool take = valid && (key >> kDigit1Shift) >= b1;
+    const uint64_t m = __ballot(take);
+    if (m) {
+      const int leader = __ffsll((unsigned long long)m) - 1;
+      uint32_t slot = 0;
+      if (lane == leader) slot = atomicAdd(&ctl->n_cand, (uint32_t)__popcll(m));
+      slot = __shfl(slot, leader, 64);
+      if (take) {
+        const int64_t pos = (int64_t)slot + __popcll(m & ((1ull << lane) - 1ull));
+        if (pos < cap) {
+          cand_key[pos] = key;
+          cand_idx[pos] = (int32_t)i;
+        }
+      }
+    }
+    if (valid && (i & 31) == 0) bitmap[i >> 5] = 0u;
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// 4. Digits 2 and 3 of the k-th key, then the index cut among equal keys.
+
+__global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restrict__ cand_key,
+                                                       const int32_t* __restrict__ cand_idx,
+                                                       SelectCtl* __restrict__ ctl, int64_t cap) {
+  __shared__ uint32_t h[2048];
+  __shared__ uint32_t shw[kSelBlock / 64];
+  __shared__ uint32_t res[2];
+  const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
+  const uint32_t b1 = ctl->b1;
+  const uint32_t need1 = ctl->k - ctl->above1;
+
+  // digit 2 (key bits 19..10) among keys in bucket b1, scanned from the top
+  for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
+  __syncthreads();
+  for (int64_t t = threadIdx.x; t < n; t += kSelBlock) {
+    const uint32_t key = cand_key[t];
+    if ((key >> 20) == b1) atomicAdd(&h[(key >> 10) & 1023u], 1u);
+  }
+  __syncthreads();
+  find_bucket(h, kDigitBins, true, need1, shw, res);
+  const uint32_t pre2 = (b1 << 10) | res[0];
+  const uint32_t need2 = need1 - res[1];
+  __syncthreads();
+
+  // digit 3 (key bits 9..0) among keys with the 22-bit prefix pre2
+  for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
+  __syncthreads();
+  for (int64_t t = threadIdx.x; t < n; t += kSelBlock) {
+    const uint32_t key = cand_key[t];
+    if ((key >> 10) == pre2) atomicAdd(&h[key & 1023u], 1u);
+  }
+  __syncthreads();
+  find_bucket(h, kDigitBins, true, need2, shw, res);
+  const uint32_t tau = (pre2 << 10) | res[0];
+  const uint32_t need3 = need2 - res[1];  // how many keys equal to tau are taken
+  const uint32_t n_eq = h[res[0]];
+  __syncthreads();
+
+  uint32_t iota = 0x7fffffffu;
+  if (need3 < n_eq) {
+    // ascending index digits among keys equal to tau: bits 30..21, 20..10, 9..0
+    for (int b = threadIdx.x; b < 1024; b += kSelBlock) h[b] = 0u;
+    __syncthreads();
+    for (int64_t t = threadIdx.x; t < n; t += kSelBlock)
+      if (cand_key[t] == tau) atomicAdd(&h[(uint32_t)cand_idx[t] >> 21], 1u);
+    __syncthreads();
+    find_bucket(h, 1024, false, need3, shw, res);
+    const uint32_t c1 = res[0];
+    const uint32_t needc = need3 - res[1];
+    __syncthreads();
+
+    for (int b = threadIdx.x; b < 2048; b += kSelBlock) h[b] = 0u;
+    __syncthreads();
+    for (int64_t t = threadIdx.x; t < n; t += kSelBlock) {
+      const uint32_t ix = (uint32_t)cand_idx[t];
+      if (cand_key[t] == tau && (ix >> 21) == c1) atomicAdd(&h[(ix >> 10) & 2047u], 1u);
+    }
+    __syncthreads();
+    find_bucket(h, 2048, false, needc, shw, res);
+    const uint32_t pre_i = (c1 << 11) | res[0];
+    const uint32_t needd = needc - res[1];
+    __syncthreads();
+
+    for (int b = threadIdx.x; b < 1024; b += kSelBlock) h[b] = 0u;
+    __syncthreads();
+    for (int64_t t = threadIdx.x; t < n; t += kSelBlock) {
+      const uint32_t ix = (uint32_t)cand_idx[t];
+      if (cand_key[t] == tau && (ix >> 10) == pre_i) atomicAdd(&h[ix & 1023u], 1u);
+    }
+    __syncthreads();
+    find_bucket(h, 1024, false, needd, shw, res);
+    iota = (pre_i << 10) | res[0];
+  }
+  if (threadIdx.x == 0) {
+    ctl->tau = tau;
+    ctl->iota = iota;
+    if ((uint64_t)ctl->n_cand > (uint64_t)cap) ctl->status = 1u;
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// 5. Mark the selected candidates.
+
+__global__ void __launch_bounds__(kBlock) k_finalize(const uint32_t* __restrict__ cand_key,
+                                                     const int32_t* __restrict__ cand_idx,
+                                                     const SelectCtl* __restrict__ ctl, int64_t cap,
+                                                     uint32_t* __restrict__ bitmap) {
+  const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
+  const uint32_t tau = ctl->tau, iota = ctl->iota;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n; t += stride) {
+    const uint32_t key = cand_key[t];
+    const uint32_t ix = (uint32_t)cand_idx[t];
+    if (key > tau || (key == tau && ix <= iota)) atomicOr(&bitmap[ix >> 5], 1u << (ix & 31u));
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// 6. Bitmap -> ascending index list.
+
+__global__ void __launch_bounds__(kSelBlock) k_emit_count(const uint32_t* __restrict__ bitmap, int64_t words,
+                                                          uint32_t* __restrict__ blockcnt) {
+  __shared__ uint32_t shw[kSelBlock / 64];
+  const int64_t w0 = (int64_t)blockIdx.x * kEmitWordsPerBlock + (int64_t)threadIdx.x * kEmitWordsPerThread;
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int m = 0; m < kEmitWordsPerThread; ++m)
+    if (w0 + m < words) cnt += __popc(bitmap[w0 + m]);
+  uint32_t total;
+  block_scan_incl<kSelBlock>(cnt, shw, total);
+  if (threadIdx.x == 0) blockcnt[blockIdx.x] = total;
+}
+
+__global__ void __launch_bounds__(kSelBlock) k_emit_write(const uint32_t* __restrict__ bitmap, int64_t words,
+                                                          const uint32_t* __restrict__ blockcnt,
+                                                          int32_t* __restrict__ idx, uint32_t k) {
+  __shared__ uint32_t shw[kSelBlock / 64];
+  uint32_t before = 0;
+  for (int b = threadIdx.x; b < (int)blockIdx.x; b += kSelBlock) before += blockcnt[b];
+  uint32_t base;
+  block_scan_incl<kSelBlock>(before, shw, base);
+  const int64_t w0 = (int64_t)blockIdx.x * kEmitWordsPerBlock + (int64_t)threadIdx.x * kEmitWordsPerThread;
+  uint32_t wv[kEmitWordsPerThread];
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int m = 0; m < kEmitWordsPerThread; ++m) {
+    wv[m] = (w0 + m < words) ? bitmap[w0 + m] : 0u;
+    cnt += __popc(wv[m]);
+  }
+  uint32_t total;
+  uint32_t pos = base + block_scan_incl<kSelBlock>(cnt, shw, total) - cnt;
+#pragma unroll
+  for (int m = 0; m < kEmitWordsPerThread; ++m) {
+    uint32_t w = wv[m];
+    while (w) {
+      const int bit = __ffs(w) - 1;
+      if (pos < k) idx[pos] = (int32_t)((w0 + m) * 32 + bit);
+      ++pos;
+      w &= w - 1u;
+    }
+  }
+}
+
+template <int R>
+void launch_unsketch_r(gs_ctx* x, hipStream_t s, const float* merged, float* est) {
+  hipLaunchKernelGGL(k_unsketch<R>, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->hs, merged,
+                     x->d, est, x->keys, x->hist);
+}
+
+}  // namespace
+
+int64_t emit_blocks_for(int64_t d) {
+  const int64_t words = (d + 31) / 32;
+  return (words + kEmitWordsPerBlock - 1) / kEmitWordsPerBlock;
+}
+
+hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, float* est, int32_t* idx) {
+  switch (x->r) {
+#define GS_R_CASE(RR) \
+  case RR: launch_unsketch_r<RR>(x, s, merged, est); break;
+    GS_R_CASE(1) GS_R_CASE(2) GS_R_CASE(3) GS_R_CASE(4) GS_R_CASE(5) GS_R_CASE(6) GS_R_CASE(7) GS_R_CASE(8)
+    GS_R_CASE(9) GS_R_CASE(10) GS_R_CASE(11) GS_R_CASE(12) GS_R_CASE(13) GS_R_CASE(14) GS_R_CASE(15) GS_R_CASE(16)
+#undef GS_R_CASE
+    default: return hipErrorInvalidValue;
+  }
+  hipLaunchKernelGGL(k_select1, dim3(1), dim3(kSelBlock), 0, s, x->hist, x->ctl, (uint32_t)k);
+  hipLaunchKernelGGL(k_compact, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->keys, x->d,
+                     x->ctl, x->cand_key, x->cand_idx, x->cand_cap, x->bitmap);
+  hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap);
+  hipLaunchKernelGGL(k_finalize, dim3(4 * x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl,
+                     x->cand_cap, x->bitmap);
+  const int64_t words = (x->d + 31) / 32;
+  hipLaunchKernelGGL(k_emit_count, dim3((unsigned)x->emit_blocks), dim3(kSelBlock), 0, s, x->bitmap, words,
+                     x->blockcnt);
+  hipLaunchKernelGGL(k_emit_write, dim3((unsigned)x->emit_blocks), dim3(kSelBlock), 0, s, x->bitmap, words,
+                     x->blockcnt, idx, (uint32_t)k);
+  return hipGetLastError();
+}
+
+}  // namespace gs

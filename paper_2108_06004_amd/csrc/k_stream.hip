@@ -1,0 +1,279 @@
+// k_stream.hip -- streaming kernels of the hot path: accumulation, table clearing, Count
+// Sketch insertion, binomial-tree merge, exact-value gather with reset.
+#include "gs_internal.hpp"
+
+namespace gs {
+namespace {
+
+constexpr int kBlock = 256;
+
+int grid_for(int64_t work_items, int per_block, int cap) {
+  int64_t b = (work_items + per_block - 1) / per_block;
+  if (b < 1) b = 1;
+  if (b > cap) b = cap;
+  return (int)b;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// ------------------------------------------------------------------------------------
+// Momentum + error accumulation (Sec. II sketching paragraph): u = rho*u + g; v = v + u,
+// each operation rounded to fp32 (the library is built with -ffp-contract=off, so no
+// multiply-add is fused). The update is elementwise, so the [P][d] arrays are streamed as
+// one flat vector of n = P*d floats, four per lane.
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__global__ void __launch_bounds__(kBlock) k_accumulate4(const f4* __restrict__ g, f4* __restrict__ u,
+                                                        f4* __restrict__ v, int64_t n4, float rho) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n4; t += stride) {
+    const f4 gg = __builtin_nontemporal_load(g + t);
+    f4 uu = u[t], vv = v[t];
+    uu = rho * uu + gg;
+    vv = vv + uu;
+    u[t] = uu;
+    v[t] = vv;
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_accumulate1(const float* __restrict__ g, float* __restrict__ u,
+                                                        float* __restrict__ v, int64_t lo, int64_t n, float rho) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = lo + (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n; t += stride) {
+    const float un = rho * u[t] + g[t];
+    u[t] = un;
+    v[t] = v[t] + un;
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_fill_zero(float* __restrict__ p, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  const int64_t n4 = n / 4;
+  float4* p4 = reinterpret_cast<float4*>(p);
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n4; t += stride) p4[t] = make_float4(0.f, 0.f, 0.f, 0.f);
+  const int64_t t = 4 * n4 + (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (t < n) p[t] = 0.f;
+}
+
+__global__ void __launch_bounds__(kBlock) k_fill_zero1(float* __restrict__ p, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n; t += stride) p[t] = 0.f;
+}
+
+// ------------------------------------------------------------------------------------
+// Count Sketch insertion (Sec. III-A; Alg. 1 sketch step). One lane per coordinate i: the
+// r hashes of i are computed once and shared by all P workers (every worker uses the same
+// hash family, which is what makes the sketches mergeable); each contribution
+// s_j(i) * v[q][i] is added to acc[q][j][h_j(i)] with a device-scope fp64 atomic. Cells are
+// summed in double precision and rounded once to fp32 afterwards (k_round_tables or the
+// merge), so the result does not depend on the atomic order beyond fp64 rounding.
+
+__global__ void __launch_bounds__(kBlock) k_sketch_atomic(HashSet hs, const float* __restrict__ v,
+                                                          double* __restrict__ acc, int64_t d, int P) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  const int64_t rc = (int64_t)hs.r * hs.c;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < d; i += stride) {
+    for (int j = 0; j < hs.r; ++j) {
+      uint32_t col, sflip;
+      hash_ij(hs, j, (uint32_t)i, col, sflip);
+      double* cell = acc + (int64_t)j * hs.c + col;
+      for (int q = 0; q < P; ++q)
+        unsafeAtomicAdd(cell + q * rc, (double)apply_sign(v[(int64_t)q * d + i], sflip));
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_round_tables(const double* __restrict__ acc, float* __restrict__ tables,
+                                                         int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n; t += stride) tables[t] = (float)acc[t];
+}
+
+__global__ void __launch_bounds__(kBlock) k_zero64(double* __restrict__ p, int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n; t += stride) p[t] = 0.0;
+}
+
+// ------------------------------------------------------------------------------------
+// Binomial-tree merge of the P worker tables (Alg. 1 reduction loop), one lane per cell.
+
+template <int P>
+__global__ void __launch_bounds__(kBlock) k_merge(const float* __restrict__ tables, float* __restrict__ merged,
+                                                  int64_t rc) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < rc; e += stride) {
+    float x[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) x[q] = tables[q * rc + e];
+    merged[e] = tree_sum<P>(x);
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_merge_dyn(const float* __restrict__ tables, float* __restrict__ merged,
+                                                      int64_t rc, int P) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < rc; e += stride) {
+    float x[kMaxWorkers];
+    for (int q = 0; q < P; ++q) x[q] = tables[q * rc + e];
+    merged[e] = tree_sum_dyn(x, P);
+  }
+}
+
+// Same tree, reading the fp64 cell accumulators of gs_step: each worker's cell is rounded
+// to fp32 first (its table value), then the fp32 values are summed in tree order.
+template <int P>
+__global__ void __launch_bounds__(kBlock) k_merge64(const double* __restrict__ acc, float* __restrict__ merged,
+                                                    int64_t rc) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < rc; e += stride) {
+    float x[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) x[q] = (float)acc[q * rc + e];
+    merged[e] = tree_sum<P>(x);
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_merge64_dyn(const double* __restrict__ acc, float* __restrict__ merged,
+                                                        int64_t rc, int P) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < rc; e += stride) {
+    float x[kMaxWorkers];
+    for (int q = 0; q < P; ++q) x[q] = (float)acc[q * rc + e];
+    merged[e] = tree_sum_dyn(x, P);
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Exact values of the selected coordinates and their reset (Alg. 2, second round).
+
+template <int P>
+__global__ void __launch_bounds__(kBlock) k_gather_reset(const int32_t* __restrict__ idx, int64_t k,
+                                                         float* __restrict__ u, float* __restrict__ v,
+                                                         float* __restrict__ values, int64_t d, int reset_u) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < k; t += stride) {
+    const int64_t i = idx[t];
+    float x[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) x[q] = v[q * d + i];
+    values[t] = tree_sum<P>(x);
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      v[q * d + i] = 0.f;
+      if (reset_u) u[q * d + i] = 0.f;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_gather_reset_dyn(const int32_t* __restrict__ idx, int64_t k,
+                                                             float* __restrict__ u, float* __restrict__ v,
+                                                             float* __restrict__ values, int64_t d, int reset_u,
+                                                             int P) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < k; t += stride) {
+    const int64_t i = idx[t];
+    float x[kMaxWorkers];
+    for (int q = 0; q < P; ++q) x[q] = v[q * d + i];
+    values[t] = tree_sum_dyn(x, P);
+    for (int q = 0; q < P; ++q) {
+      v[q * d + i] = 0.f;
+      if (reset_u) u[q * d + i] = 0.f;
+    }
+  }
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------------
+// Launchers
+
+hipError_t launch_accumulate(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v) {
+  const int64_t n = (int64_t)x->P * x->d;
+  if (aligned16(g) && aligned16(u) && aligned16(v)) {
+    const int64_t n4 = n / 4;
+    if (n4 > 0) {
+      hipLaunchKernelGGL(k_accumulate4, dim3(grid_for(n4, kBlock, 4 * x->num_cus * 2)), dim3(kBlock), 0, s,
+                         reinterpret_cast<const f4*>(g), reinterpret_cast<f4*>(u),
+                         reinterpret_cast<f4*>(v), n4, x->rho);
+    }
+    if (4 * n4 < n) hipLaunchKernelGGL(k_accumulate1, dim3(1), dim3(kBlock), 0, s, g, u, v, 4 * n4, n, x->rho);
+  } else {
+    hipLaunchKernelGGL(k_accumulate1, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, g, u, v,
+                       (int64_t)0, n, x->rho);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(hipStream_t s, float* p, int64_t n) {
+  if (n <= 0) return hipSuccess;
+  if (aligned16(p))
+    hipLaunchKernelGGL(k_fill_zero, dim3(grid_for(n / 4 + 1, kBlock, 2048)), dim3(kBlock), 0, s, p, n);
+  else
+    hipLaunchKernelGGL(k_fill_zero1, dim3(grid_for(n, kBlock, 2048)), dim3(kBlock), 0, s, p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_sketch_acc(const gs_ctx* x, hipStream_t s, const float* v) {
+  const int64_t n = (int64_t)x->P * x->r * x->c;
+  hipLaunchKernelGGL(k_zero64, dim3(grid_for(n, kBlock, 2048)), dim3(kBlock), 0, s, x->acc64, n);
+  hipLaunchKernelGGL(k_sketch_atomic, dim3(grid_for(x->d, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, x->hs, v,
+                     x->acc64, x->d, x->P);
+  return hipGetLastError();
+}
+
+hipError_t launch_sketch(const gs_ctx* x, hipStream_t s, const float* v, float* tables) {
+  hipError_t e = launch_sketch_acc(x, s, v);
+  if (e != hipSuccess) return e;
+  const int64_t n = (int64_t)x->P * x->r * x->c;
+  hipLaunchKernelGGL(k_round_tables, dim3(grid_for(n, kBlock, 2048)), dim3(kBlock), 0, s, x->acc64, tables, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge(const gs_ctx* x, hipStream_t s, const float* tables, float* merged) {
+  const int64_t rc = (int64_t)x->r * x->c;
+  const dim3 grid(grid_for(rc, kBlock, 8 * x->num_cus)), block(kBlock);
+  switch (x->P) {
+#define GS_MERGE_CASE(PP) \
+  case PP: hipLaunchKernelGGL(k_merge<PP>, grid, block, 0, s, tables, merged, rc); break;
+    GS_MERGE_CASE(1) GS_MERGE_CASE(2) GS_MERGE_CASE(3) GS_MERGE_CASE(4) GS_MERGE_CASE(5) GS_MERGE_CASE(6)
+    GS_MERGE_CASE(7) GS_MERGE_CASE(8) GS_MERGE_CASE(9) GS_MERGE_CASE(10) GS_MERGE_CASE(11) GS_MERGE_CASE(12)
+    GS_MERGE_CASE(13) GS_MERGE_CASE(14) GS_MERGE_CASE(15) GS_MERGE_CASE(16)
+#undef GS_MERGE_CASE
+    default: hipLaunchKernelGGL(k_merge_dyn, grid, block, 0, s, tables, merged, rc, x->P); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_acc(const gs_ctx* x, hipStream_t s, float* merged) {
+  const int64_t rc = (int64_t)x->r * x->c;
+  const dim3 grid(grid_for(rc, kBlock, 8 * x->num_cus)), block(kBlock);
+  switch (x->P) {
+#define GS_MERGE_CASE(PP) \
+  case PP: hipLaunchKernelGGL(k_merge64<PP>, grid, block, 0, s, x->acc64, merged, rc); break;
+    GS_MERGE_CASE(1) GS_MERGE_CASE(2) GS_MERGE_CASE(3) GS_MERGE_CASE(4) GS_MERGE_CASE(5) GS_MERGE_CASE(6)
+    GS_MERGE_CASE(7) GS_MERGE_CASE(8) GS_MERGE_CASE(9) GS_MERGE_CASE(10) GS_MERGE_CASE(11) GS_MERGE_CASE(12)
+    GS_MERGE_CASE(13) GS_MERGE_CASE(14) GS_MERGE_CASE(15) GS_MERGE_CASE(16)
+#undef GS_MERGE_CASE
+    default: hipLaunchKernelGGL(k_merge64_dyn, grid, block, 0, s, x->acc64, merged, rc, x->P); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_reset(const gs_ctx* x, hipStream_t s, const int32_t* idx, int64_t k, float* u, float* v,
+                               float* values) {
+  const dim3 grid(grid_for(k, kBlock, 4 * x->num_cus)), block(kBlock);
+  const int ru = x->reset_momentum ? 1 : 0;
+  switch (x->P) {
+#define GS_GATHER_CASE(PP) \
+  case PP: hipLaunchKernelGGL(k_gather_reset<PP>, grid, block, 0, s, idx, k, u, v, values, x->d, ru); break;
+    GS_GATHER_CASE(1) GS_GATHER_CASE(2) GS_GATHER_CASE(3) GS_GATHER_CASE(4) GS_GATHER_CASE(5) GS_GATHER_CASE(6)
+    GS_GATHER_CASE(7) GS_GATHER_CASE(8) GS_GATHER_CASE(9) GS_GATHER_CASE(10) GS_GATHER_CASE(11) GS_GATHER_CASE(12)
+    GS_GATHER_CASE(13) GS_GATHER_CASE(14) GS_GATHER_CASE(15) GS_GATHER_CASE(16)
+#undef GS_GATHER_CASE
+    default: hipLaunchKernelGGL(k_gather_reset_dyn, grid, block, 0, s, idx, k, u, v, values, x->d, ru, x->P); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace gs
