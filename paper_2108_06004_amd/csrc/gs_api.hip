@@ -46,7 +46,8 @@ hipError_t alloc(T** p, int64_t count) {
 }
 
 void free_scratch(gs_ctx* x) {
-  void* ptrs[] = {x->keys, x->hist, x->ctl, x->cand_key, x->cand_idx, x->bitmap, x->blockcnt, x->acc64};
+  void* ptrs[] = {x->keys, x->hist, x->ctl, x->cand_key, x->cand_idx, x->bitmap, x->blockcnt, x->acc64,
+                  x->list, x->tile_off, x->vI, x->partial};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   x->keys = nullptr;
@@ -57,6 +58,10 @@ void free_scratch(gs_ctx* x) {
   x->bitmap = nullptr;
   x->blockcnt = nullptr;
   x->acc64 = nullptr;
+  x->list = nullptr;
+  x->tile_off = nullptr;
+  x->vI = nullptr;
+  x->partial = nullptr;
 }
 
 bool valid_ab(const uint32_t* a, const uint32_t* b, int r) {
@@ -151,10 +156,20 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   chk(alloc(&x->cand_idx, x->cand_cap));
   chk(alloc(&x->bitmap, words));
   chk(alloc(&x->blockcnt, x->emit_blocks));
-  chk(alloc(&x->acc64, (int64_t)x->P * x->r * x->c));
+  x->plan = gs::make_pull_plan(x->d, x->P, x->r, x->c, x->num_cus);
+  x->use_pull = (int64_t)x->plan.T * (int64_t)sizeof(uint32_t) <= gs::kMaxFillLds;
+  if (x->use_pull) {
+    chk(alloc(&x->list, (int64_t)x->r * x->d));
+    chk(alloc(&x->tile_off, (int64_t)x->plan.T + 1));
+    chk(alloc(&x->vI, x->d * x->plan.PP));
+    chk(alloc(&x->partial, (int64_t)x->plan.S * x->r * x->c * x->P));
+  } else {
+    chk(alloc(&x->acc64, (int64_t)x->P * x->r * x->c));
+  }
   if (ea == hipSuccess) ea = hipMemset(x->hist, 0, gs::kDigit1Bins * sizeof(uint32_t));
   if (ea == hipSuccess) ea = hipMemset(x->ctl, 0, sizeof(gs::SelectCtl));
   if (ea == hipSuccess) ea = hipDeviceSynchronize();
+  if (ea == hipSuccess && x->use_pull) ea = gs::build_pull_lists(x);
   if (ea != hipSuccess) {
     const bool oom = ea == hipErrorOutOfMemory || ea == hipErrorMemoryAllocation;
     g_create_error = std::string("device scratch allocation failed: ") + hipGetErrorString(ea);
@@ -186,7 +201,16 @@ gs_status gs_sketch(gs_ctx* x, void* stream, const float* v, float* tables) {
   if (!x) return GS_ERR_INVALID_ARG;
   x->last_error.clear();
   if (!v || !tables) return fail(x, GS_ERR_INVALID_ARG, "gs_sketch: NULL array");
-  return device_status(x, gs::launch_sketch(x, as_stream(stream), v, tables), "gs_sketch");
+  hipStream_t s = as_stream(stream);
+  hipError_t e;
+  if (x->use_pull) {
+    e = gs::launch_interleave(x, s, v);
+    if (e == hipSuccess) e = gs::launch_pull(x, s);
+    if (e == hipSuccess) e = gs::launch_merge_partials(x, s, nullptr, tables);
+  } else {
+    e = gs::launch_sketch(x, s, v, tables);
+  }
+  return device_status(x, e, "gs_sketch");
 }
 
 gs_status gs_merge(gs_ctx* x, void* stream, const float* tables, float* merged) {
@@ -220,9 +244,16 @@ gs_status gs_step(gs_ctx* x, void* stream, const float* g, float* u, float* v, i
   if (!g || !u || !v || !merged || !idx || !values) return fail(x, GS_ERR_INVALID_ARG, "gs_step: NULL array");
   if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_step: k must satisfy 1 <= k <= k_max");
   hipStream_t s = as_stream(stream);
-  hipError_t e = gs::launch_accumulate(x, s, g, u, v);
-  if (e == hipSuccess) e = gs::launch_sketch_acc(x, s, v);
-  if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
+  hipError_t e;
+  if (x->use_pull) {
+    e = gs::launch_accumulate_vi(x, s, g, u, v);
+    if (e == hipSuccess) e = gs::launch_pull(x, s);
+    if (e == hipSuccess) e = gs::launch_merge_partials(x, s, merged, nullptr);
+  } else {
+    e = gs::launch_accumulate(x, s, g, u, v);
+    if (e == hipSuccess) e = gs::launch_sketch_acc(x, s, v);
+    if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
+  }
   if (e == hipSuccess) e = gs::launch_unsketch_topk(x, s, merged, k, nullptr, idx);
   if (e == hipSuccess) e = gs::launch_gather_reset(x, s, idx, k, u, v, values);
   return device_status(x, e, "gs_step");
@@ -240,11 +271,11 @@ gs_status gs_step_profiled(gs_ctx* x, void* stream, const float* g, float* u, fl
   hipError_t e = hipSuccess;
   for (int t = 0; t <= GS_NUM_STAGES && e == hipSuccess; ++t) e = hipEventCreate(&ev[t]);
   if (e == hipSuccess) e = hipEventRecord(ev[0], s);
-  if (e == hipSuccess) e = gs::launch_accumulate(x, s, g, u, v);
+  if (e == hipSuccess) e = x->use_pull ? gs::launch_accumulate_vi(x, s, g, u, v) : gs::launch_accumulate(x, s, g, u, v);
   if (e == hipSuccess) e = hipEventRecord(ev[1], s);
-  if (e == hipSuccess) e = gs::launch_sketch_acc(x, s, v);
+  if (e == hipSuccess) e = x->use_pull ? gs::launch_pull(x, s) : gs::launch_sketch_acc(x, s, v);
   if (e == hipSuccess) e = hipEventRecord(ev[2], s);
-  if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
+  if (e == hipSuccess) e = x->use_pull ? gs::launch_merge_partials(x, s, merged, nullptr) : gs::launch_merge_acc(x, s, merged);
   if (e == hipSuccess) e = hipEventRecord(ev[3], s);
   if (e == hipSuccess) e = gs::launch_unsketch_topk(x, s, merged, k, nullptr, idx);
   if (e == hipSuccess) e = hipEventRecord(ev[4], s);

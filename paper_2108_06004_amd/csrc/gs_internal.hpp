@@ -25,6 +25,18 @@ struct SelectCtl {
   uint32_t status;      // 0 ok; nonzero: candidate overflow (must not happen)
   uint32_t pad;
 };
+
+// Geometry of the gather-based sketch: tiles of W columns of one row, all P workers, fp64.
+struct PullPlan {
+  int32_t P, PP;          // workers; vI row length (P rounded up to a multiple of 4)
+  int32_t W;              // columns per tile
+  int32_t tiles_per_row;  // ceil(c / W)
+  int32_t T;              // r * tiles_per_row
+  int32_t S;              // list segments per tile (work items = T * S)
+  int32_t NB;             // build chunks
+  int64_t chunk;          // coordinates per build chunk
+};
+constexpr int64_t kMaxFillLds = 160 * 1024;  // LDS of the list-fill kernel holds T cursors
 }  // namespace gs
 
 struct gs_ctx {
@@ -46,7 +58,14 @@ struct gs_ctx {
   uint32_t* bitmap = nullptr;     // [ceil(d/32)]
   uint32_t* blockcnt = nullptr;   // [emit blocks]
   int64_t emit_blocks = 0;
-  double* acc64 = nullptr;        // [P][r][c] fp64 cell accumulators of the sketch
+  // gather-based sketch (used when the plan fits; otherwise fp64 atomics into acc64)
+  bool use_pull = false;
+  gs::PullPlan plan{};
+  uint32_t* list = nullptr;       // [r*d] coordinates of each tile, ascending
+  int64_t* tile_off = nullptr;    // [T+1]
+  float* vI = nullptr;            // [d][PP] worker-interleaved accumulators
+  double* partial = nullptr;      // [S][r][c][P] fp64 tile sums
+  double* acc64 = nullptr;        // [P][r][c] fp64 cell accumulators of the atomic path
 
   std::string last_error;
 };
@@ -63,4 +82,10 @@ hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, i
 hipError_t launch_gather_reset(const gs_ctx* x, hipStream_t s, const int32_t* idx, int64_t k, float* u, float* v,
                                float* values);
 int64_t emit_blocks_for(int64_t d);
+PullPlan make_pull_plan(int64_t d, int32_t P, int32_t r, int64_t c, int num_cus);
+hipError_t build_pull_lists(gs_ctx* x);
+hipError_t launch_accumulate_vi(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v);
+hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v);
+hipError_t launch_pull(const gs_ctx* x, hipStream_t s);
+hipError_t launch_merge_partials(const gs_ctx* x, hipStream_t s, float* merged, float* tables);
 }  // namespace gs

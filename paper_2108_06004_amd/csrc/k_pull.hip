@@ -1,0 +1,435 @@
+// k_pull.hip -- Count Sketch insertion as a gather ("pull") into LDS-resident tiles.
+//
+// The sketch S^q[j][col] = sum over {i : h_j(i) = col} of s_j(i) v^q_i (Sec. III-A) is
+// computed per column tile instead of by scattering: a tile is a range of W columns of one
+// row j, held for all P workers in LDS as fp64 accumulators. Because the hash family is
+// fixed for the life of a context, the set of coordinates that land in each tile is fixed
+// too; gs_create builds it once as per-tile coordinate lists in ascending order (three
+// passes: per-chunk counts, offsets, an in-order fill). Each step then
+//   1. accumulates (u, v) and writes v worker-interleaved, vI[i][q] (one contiguous row of
+//      P floats per coordinate), so one gather serves every worker;
+//   2. runs one workgroup per (tile, list segment): gather vI rows of the listed
+//      coordinates, add s_j(i) * vI[i][q] into the LDS tile with fp64 LDS atomics, and
+//      write the tile out (no global atomics);
+//   3. sums the segments of each cell in fixed order (fp64), rounds once to fp32 (the
+//      worker's table value) and merges the workers in the binomial-tree order.
+// All tiles walk their lists in ascending coordinate order at similar rates, so at any
+// moment the gathers of all tiles fall in a narrow band of vI that stays in cache.
+#include "gs_internal.hpp"
+
+namespace gs {
+namespace {
+
+constexpr int kBlock = 256;
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+int grid_for(int64_t work_items, int per_block, int cap) {
+  int64_t b = (work_items + per_block - 1) / per_block;
+  if (b < 1) b = 1;
+  if (b > cap) b = cap;
+  return (int)b;
+}
+
+__device__ __forceinline__ void tile_of(const HashSet& hs, const PullPlan& pl, int j, uint32_t i, uint32_t& col,
+                                        uint32_t& sflip, uint32_t& tile) {
+  hash_ij(hs, j, i, col, sflip);
+  tile = (uint32_t)j * pl.tiles_per_row + col / (uint32_t)pl.W;
+}
+
+// ------------------------------------------------------------------------------------
+// Static list build (gs_create).
+
+// counts[b][t]: entries of build chunk b that fall in tile t.
+__global__ void __launch_bounds__(kBlock) k_build_count(HashSet hs, PullPlan pl, int64_t d,
+                                                        uint32_t* __restrict__ counts) {
+  const int64_t b = blockIdx.x;
+  const int64_t lo = b * pl.chunk, hi = min(d, lo + pl.chunk);
+  for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock) {
+    for (int j = 0; j < hs.r; ++j) {
+      uint32_t col, sflip, t;
+      tile_of(hs, pl, j, (uint32_t)i, col, sflip, t);
+      atomicAdd(&counts[b * pl.T + t], 1u);
+    }
+  }
+}
+
+// Per tile: exclusive prefix of counts over chunks (in place) and the tile total.
+__global__ void __launch_bounds__(kBlock) k_build_prefix(PullPlan pl, uint32_t* __restrict__ counts,
+                                                         uint32_t* __restrict__ total) {
+  const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  if (t >= pl.T) return;
+  uint32_t run = 0;
+  for (int64_t b = 0; b < pl.NB; ++b) {
+    const uint32_t cnt = counts[b * pl.T + t];
+    counts[b * pl.T + t] = run;
+    run += cnt;
+  }
+  total[t] = run;
+}
+
+// Tile start offsets (exclusive scan of the totals) by one block; off[T] = r*d.
+__global__ void __launch_bounds__(1024) k_build_offsets(PullPlan pl, const uint32_t* __restrict__ total,
+                                                        int64_t* __restrict__ off) {
+  __shared__ int64_t part[1024];
+  const int64_t per = (pl.T + 1023) / 1024;
+  const int64_t lo = threadIdx.x * per, hi = min((int64_t)pl.T, lo + per);
+  int64_t s = 0;
+  for (int64_t t = lo; t < hi; ++t) s += total[t];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t run = 0;
+    for (int w = 0; w < 1024; ++w) {
+      const int64_t x = part[w];
+      part[w] = run;
+      run += x;
+    }
+    off[pl.T] = run;
+  }
+  __syncthreads();
+  int64_t run = part[threadIdx.x];
+  for (int64_t t = lo; t < hi; ++t) {
+    off[t] = run;
+    run += total[t];
+  }
+}
+
+// In-order fill: one wave per build chunk walks its coordinates in ascending order; lanes
+// take their list slots one after another (lane order = coordinate order), so every
+// tile's list comes out sorted by coordinate.
+__global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int64_t d,
+                                                   const uint32_t* __restrict__ prefix,
+                                                   const int64_t* __restrict__ off, uint32_t* __restrict__ list) {
+  extern __shared__ uint32_t cursor[];  // [T]
+  const int64_t b = blockIdx.x;
+  const int lane = threadIdx.x;
+  for (int64_t t = lane; t < pl.T; t += 64) cursor[t] = prefix[b * pl.T + t];
+  __syncthreads();
+  const int64_t lo = b * pl.chunk, hi = min(d, lo + pl.chunk);
+  for (int64_t base = lo; base < hi; base += 64) {
+    const int64_t i = base + lane;
+    const bool valid = i < hi;
+    for (int j = 0; j < hs.r; ++j) {
+      uint32_t col = 0, sflip = 0, t = 0;
+      if (valid) tile_of(hs, pl, j, (uint32_t)i, col, sflip, t);
+      uint32_t slot = 0;
+      for (int l = 0; l < 64; ++l) {
+        if (lane == l && valid) {
+          slot = cursor[t];
+          cursor[t] = slot + 1;
+        }
+        __builtin_amdgcn_wave_barrier();
+      }
+      if (valid) list[off[t] + slot] = (uint32_t)i;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// Per step: accumulation that also writes the worker-interleaved copy of v.
+// One lane handles 4 consecutive coordinates of every worker (float4 per worker row).
+
+template <int P>
+__global__ void __launch_bounds__(kBlock) k_accumulate_vi(const float* __restrict__ g, float* __restrict__ u,
+                                                          float* __restrict__ v, float* __restrict__ vI, int64_t d,
+                                                          float rho) {
+  constexpr int PP = (P + 3) & ~3;  // vI row length
+  const int64_t n4 = d / 4;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n4; t += stride) {
+    float vv[P][4];
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      const int64_t o = q * n4 + t;
+      const f4 gg = __builtin_nontemporal_load(reinterpret_cast<const f4*>(g) + o);
+      f4 uu = reinterpret_cast<const f4*>(u)[o];
+      f4 w = reinterpret_cast<const f4*>(v)[o];
+      uu = rho * uu + gg;
+      w = w + uu;
+      reinterpret_cast<f4*>(u)[o] = uu;
+      reinterpret_cast<f4*>(v)[o] = w;
+      vv[q][0] = w.x;
+      vv[q][1] = w.y;
+      vv[q][2] = w.z;
+      vv[q][3] = w.w;
+    }
+    f4* dst = reinterpret_cast<f4*>(vI + (4 * t) * PP);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+#pragma unroll
+      for (int q0 = 0; q0 < PP; q0 += 4) {
+        f4 x;
+        x.x = q0 + 0 < P ? vv[q0 + 0 < P ? q0 + 0 : 0][m] : 0.f;
+        x.y = q0 + 1 < P ? vv[q0 + 1 < P ? q0 + 1 : 0][m] : 0.f;
+        x.z = q0 + 2 < P ? vv[q0 + 2 < P ? q0 + 2 : 0][m] : 0.f;
+        x.w = q0 + 3 < P ? vv[q0 + 3 < P ? q0 + 3 : 0][m] : 0.f;
+        dst[(m * PP + q0) / 4] = x;
+      }
+    }
+  }
+}
+
+// Generic (any P, any d, any alignment): one lane per (coordinate, worker).
+__global__ void __launch_bounds__(kBlock) k_accumulate_vi_any(const float* __restrict__ g, float* __restrict__ u,
+                                                              float* __restrict__ v, float* __restrict__ vI,
+                                                              int64_t d, int P, int PP, float rho, int do_acc) {
+  const int64_t n = (int64_t)P * d;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n; e += stride) {
+    const int64_t q = e / d, i = e - q * d;
+    float w;
+    if (do_acc) {
+      const float un = rho * u[e] + g[e];
+      u[e] = un;
+      w = v[e] + un;
+      v[e] = w;
+    } else {
+      w = v[e];
+    }
+    vI[i * PP + q] = w;
+  }
+}
+
+// ------------------------------------------------------------------------------------
+// The pull: one workgroup per (tile, segment).
+
+template <int PP>
+__device__ __forceinline__ void load_row(const float* __restrict__ vI, uint32_t i, float (&x)[PP]) {
+  const f4* p = reinterpret_cast<const f4*>(vI + (int64_t)i * PP);
+#pragma unroll
+  for (int m = 0; m < PP / 4; ++m) {
+    const f4 y = p[m];
+    x[4 * m + 0] = y.x;
+    x[4 * m + 1] = y.y;
+    x[4 * m + 2] = y.z;
+    x[4 * m + 3] = y.w;
+  }
+}
+
+template <int PP>
+__global__ void __launch_bounds__(kBlock) k_pull(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
+                                                 const int64_t* __restrict__ off, const float* __restrict__ vI,
+                                                 double* __restrict__ partial) {
+  extern __shared__ double acc[];  // [W][P]
+  const int P = pl.P;
+  const int64_t item = blockIdx.x;
+  const int64_t t = item / pl.S, s = item - t * pl.S;
+  const int j = (int)(t / pl.tiles_per_row);
+  const int64_t col0 = (t - (int64_t)j * pl.tiles_per_row) * pl.W;
+  const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - col0);
+  for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) acc[e] = 0.0;
+  __syncthreads();
+  const int64_t lo = off[t], n = off[t + 1] - lo;
+  const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
+  for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
+    const uint32_t i = list[e];
+    uint32_t col, sflip;
+    hash_ij(hs, j, i, col, sflip);
+    float x[PP];
+    load_row<PP>(vI, i, x);
+    double* cell = acc + (int64_t)(col - col0) * P;
+#pragma unroll
+    for (int q = 0; q < PP; ++q)
+      if (q < P) atomicAdd(cell + q, (double)apply_sign(x[q], sflip));
+  }
+  __syncthreads();
+  double* dst = partial + ((s * hs.r + j) * (int64_t)hs.c + col0) * P;
+  for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) dst[e] = acc[e];
+}
+
+// Runtime-P variant (P > 16): rows of PP floats read element by element.
+__global__ void __launch_bounds__(kBlock) k_pull_any(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
+                                                     const int64_t* __restrict__ off, const float* __restrict__ vI,
+                                                     double* __restrict__ partial) {
+  extern __shared__ double acc[];
+  const int P = pl.P, PP = pl.PP;
+  const int64_t item = blockIdx.x;
+  const int64_t t = item / pl.S, s = item - t * pl.S;
+  const int j = (int)(t / pl.tiles_per_row);
+  const int64_t col0 = (t - (int64_t)j * pl.tiles_per_row) * pl.W;
+  const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - col0);
+  for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) acc[e] = 0.0;
+  __syncthreads();
+  const int64_t lo = off[t], n = off[t + 1] - lo;
+  const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
+  for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
+    const uint32_t i = list[e];
+    uint32_t col, sflip;
+    hash_ij(hs, j, i, col, sflip);
+    double* cell = acc + (int64_t)(col - col0) * P;
+    for (int q = 0; q < P; ++q) atomicAdd(cell + q, (double)apply_sign(vI[(int64_t)i * PP + q], sflip));
+  }
+  __syncthreads();
+  double* dst = partial + ((s * hs.r + j) * (int64_t)hs.c + col0) * P;
+  for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) dst[e] = acc[e];
+}
+
+// ------------------------------------------------------------------------------------
+// Segment sum + single rounding + tree merge. partial is [S][r][c][P] fp64.
+
+template <int P>
+__global__ void __launch_bounds__(kBlock) k_merge_partials(const double* __restrict__ partial, int S, int64_t rc,
+                                                           float* __restrict__ merged, float* __restrict__ tables) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < rc; e += stride) {
+    float x[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) {
+      double a = partial[e * P + q];
+      for (int s = 1; s < S; ++s) a += partial[(s * rc + e) * P + q];
+      x[q] = (float)a;
+    }
+    if (tables) {
+#pragma unroll
+      for (int q = 0; q < P; ++q) tables[q * rc + e] = x[q];
+    }
+    if (merged) merged[e] = tree_sum<P>(x);
+  }
+}
+
+__global__ void __launch_bounds__(kBlock) k_merge_partials_any(const double* __restrict__ partial, int S, int64_t rc,
+                                                               int P, float* __restrict__ merged,
+                                                               float* __restrict__ tables) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < rc; e += stride) {
+    float x[kMaxWorkers];
+    for (int q = 0; q < P; ++q) {
+      double a = partial[e * P + q];
+      for (int s = 1; s < S; ++s) a += partial[(s * rc + e) * P + q];
+      x[q] = (float)a;
+      if (tables) tables[q * rc + e] = x[q];
+    }
+    if (merged) merged[e] = tree_sum_dyn(x, P);
+  }
+}
+
+template <int P>
+hipError_t launch_acc_vi_p(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v) {
+  const int64_t n4 = x->d / 4;
+  hipLaunchKernelGGL(k_accumulate_vi<P>, dim3(grid_for(n4, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, g, u, v,
+                     x->vI, x->d, x->rho);
+  return hipGetLastError();
+}
+
+template <int PP>
+void launch_pull_pp(const gs_ctx* x, hipStream_t s) {
+  const PullPlan& pl = x->plan;
+  hipLaunchKernelGGL(k_pull<PP>, dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kBlock),
+                     (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, x->vI, x->partial);
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------------
+
+PullPlan make_pull_plan(int64_t d, int32_t P, int32_t r, int64_t c, int num_cus) {
+  PullPlan pl{};
+  pl.P = P;
+  pl.PP = (P + 3) & ~3;
+  // A tile holds W columns x P workers of fp64 accumulators in at most 64 KiB of LDS, so two
+  // workgroups share a CU.
+  int64_t W = 65536 / (8 * (int64_t)P);
+  if (W > c) W = c;
+  if (W < 1) W = 1;
+  pl.W = (int32_t)W;
+  pl.tiles_per_row = (int32_t)((c + W - 1) / W);
+  pl.T = r * pl.tiles_per_row;
+  // enough (tile, segment) work items to occupy every CU
+  const int64_t want = num_cus;
+  int64_t S = (want + pl.T - 1) / pl.T;
+  const int64_t per_tile = (int64_t)r * d / pl.T;
+  if (S > per_tile / 256) S = per_tile / 256;  // keep segments at least 256 entries long
+  if (S < 1) S = 1;
+  pl.S = (int32_t)S;
+  // build chunks: ~64 Ki coordinates each
+  pl.chunk = 65536;
+  pl.NB = (int32_t)((d + pl.chunk - 1) / pl.chunk);
+  return pl;
+}
+
+hipError_t build_pull_lists(gs_ctx* x) {
+  const PullPlan& pl = x->plan;
+  const size_t fill_lds = (size_t)pl.T * sizeof(uint32_t);
+  hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_build_fill),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)fill_lds);
+  if (ea != hipSuccess) return ea;
+  uint32_t* counts = nullptr;
+  uint32_t* total = nullptr;
+  hipError_t e = hipMalloc(reinterpret_cast<void**>(&counts), (size_t)pl.NB * pl.T * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&total), (size_t)pl.T * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMemset(counts, 0, (size_t)pl.NB * pl.T * sizeof(uint32_t));
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(k_build_count, dim3(pl.NB), dim3(kBlock), 0, 0, x->hs, pl, x->d, counts);
+    hipLaunchKernelGGL(k_build_prefix, dim3((pl.T + kBlock - 1) / kBlock), dim3(kBlock), 0, 0, pl, counts, total);
+    hipLaunchKernelGGL(k_build_offsets, dim3(1), dim3(1024), 0, 0, pl, total, x->tile_off);
+    hipLaunchKernelGGL(k_build_fill, dim3(pl.NB), dim3(64), (size_t)pl.T * sizeof(uint32_t), 0, x->hs, pl, x->d,
+                       counts, x->tile_off, x->list);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (counts) (void)hipFree(counts);
+  if (total) (void)hipFree(total);
+  return e;
+}
+
+hipError_t launch_accumulate_vi(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v) {
+  const bool fast = (x->d % 4 == 0) && ((uintptr_t)g % 16 == 0) && ((uintptr_t)u % 16 == 0) &&
+                    ((uintptr_t)v % 16 == 0) && x->P <= 16;
+  if (fast) {
+    switch (x->P) {
+#define GS_ACCVI_CASE(PP) \
+  case PP: return launch_acc_vi_p<PP>(x, s, g, u, v);
+      GS_ACCVI_CASE(1) GS_ACCVI_CASE(2) GS_ACCVI_CASE(3) GS_ACCVI_CASE(4) GS_ACCVI_CASE(5) GS_ACCVI_CASE(6)
+      GS_ACCVI_CASE(7) GS_ACCVI_CASE(8) GS_ACCVI_CASE(9) GS_ACCVI_CASE(10) GS_ACCVI_CASE(11) GS_ACCVI_CASE(12)
+      GS_ACCVI_CASE(13) GS_ACCVI_CASE(14) GS_ACCVI_CASE(15) GS_ACCVI_CASE(16)
+#undef GS_ACCVI_CASE
+      default: break;
+    }
+  }
+  const int64_t n = (int64_t)x->P * x->d;
+  hipLaunchKernelGGL(k_accumulate_vi_any, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, g, u, v,
+                     x->vI, x->d, x->P, x->plan.PP, x->rho, 1);
+  return hipGetLastError();
+}
+
+hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v) {
+  const int64_t n = (int64_t)x->P * x->d;
+  hipLaunchKernelGGL(k_accumulate_vi_any, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, nullptr,
+                     nullptr, const_cast<float*>(v), x->vI, x->d, x->P, x->plan.PP, x->rho, 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_pull(const gs_ctx* x, hipStream_t s) {
+  switch (x->plan.PP) {
+    case 4: launch_pull_pp<4>(x, s); break;
+    case 8: launch_pull_pp<8>(x, s); break;
+    case 12: launch_pull_pp<12>(x, s); break;
+    case 16: launch_pull_pp<16>(x, s); break;
+    default: {
+      const PullPlan& pl = x->plan;
+      hipLaunchKernelGGL(k_pull_any, dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kBlock),
+                         (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, x->vI, x->partial);
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_partials(const gs_ctx* x, hipStream_t s, float* merged, float* tables) {
+  const int64_t rc = (int64_t)x->r * x->c;
+  const dim3 grid(grid_for(rc, kBlock, 8 * x->num_cus)), block(kBlock);
+  const int S = x->plan.S;
+  switch (x->P) {
+#define GS_MP_CASE(PP) \
+  case PP: hipLaunchKernelGGL(k_merge_partials<PP>, grid, block, 0, s, x->partial, S, rc, merged, tables); break;
+    GS_MP_CASE(1) GS_MP_CASE(2) GS_MP_CASE(3) GS_MP_CASE(4) GS_MP_CASE(5) GS_MP_CASE(6) GS_MP_CASE(7) GS_MP_CASE(8)
+    GS_MP_CASE(9) GS_MP_CASE(10) GS_MP_CASE(11) GS_MP_CASE(12) GS_MP_CASE(13) GS_MP_CASE(14) GS_MP_CASE(15)
+    GS_MP_CASE(16)
+#undef GS_MP_CASE
+    default:
+      hipLaunchKernelGGL(k_merge_partials_any, grid, block, 0, s, x->partial, S, rc, x->P, merged, tables);
+      break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace gs
