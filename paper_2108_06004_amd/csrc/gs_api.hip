@@ -25,17 +25,15 @@ gs_status device_status(gs_ctx* x, hipError_t e, const char* where) {
   return fail(x, GS_ERR_DEVICE, std::string(where) + ": " + hipGetErrorString(e));
 }
 
-// Granlund-Montgomery reciprocal for 31-bit dividends: l = ceil(log2 c), m = ceil(2^(31+l)/c).
+// Granlund-Montgomery reciprocal for 31-bit dividends: l = ceil(log2 c), m = ceil(2^(31+l)/c)
+// (m < 2^32; for c = 1, l = 0 and m = 2^31), and floor(x / c) = floor(x * m / 2^(31+l)).
 void set_divisor(gs::HashSet& hs, uint32_t c) {
-  hs.c = c;
-  hs.magic = 0;
-  hs.shift = 0;
-  if (c < 2) return;
   uint32_t l = 0;
   while ((1ull << l) < c) ++l;
   const uint64_t num = 1ull << (31 + l);
+  hs.c = c;
   hs.magic = (uint32_t)((num + c - 1) / c);
-  hs.shift = l - 1;
+  hs.shift = 31 + l;
 }
 
 template <typename T>

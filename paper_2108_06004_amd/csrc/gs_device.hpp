@@ -26,10 +26,20 @@ struct RowHash {
 struct HashSet {
   RowHash row[kMaxRows];
   uint32_t c;      // columns
-  uint32_t magic;  // ceil(2^(31+l) / c), l = ceil(log2 c); unused when c == 1
-  uint32_t shift;  // l - 1
+  uint32_t magic;  // ceil(2^(31+l) / c) with l = ceil(log2 c); 2^31 when c == 1 (l = 0)
+  uint32_t shift;  // 31 + l
   int32_t r;       // rows
 };
+
+// The per-row constants a kernel keeps in registers for its hot loop.
+struct RowConst {
+  uint32_t a, b, a2, b2, c, magic, shift;
+};
+
+__device__ __forceinline__ RowConst row_const(const HashSet& hs, int j) {
+  const RowHash rh = hs.row[j];
+  return RowConst{rh.a, rh.b, rh.a2, rh.b2, hs.c, hs.magic, hs.shift};
+}
 
 // (a*i + b) mod p for a, b < p and i < 2^31.
 __device__ __forceinline__ uint32_t mod_mersenne_affine(uint32_t a, uint32_t b, uint32_t i) {
@@ -39,18 +49,21 @@ __device__ __forceinline__ uint32_t mod_mersenne_affine(uint32_t a, uint32_t b, 
   return z >= kMersenne ? z - kMersenne : z;
 }
 
-__device__ __forceinline__ uint32_t mod_c(uint32_t x, const HashSet& hs) {
-  if (hs.c == 1) return 0;
-  const uint32_t q = __umulhi(x, hs.magic) >> hs.shift;
-  return x - q * hs.c;
+// x mod c for x < 2^31: q = floor(x * magic / 2^shift) is floor(x / c) exactly.
+__device__ __forceinline__ uint32_t mod_c(uint32_t x, uint32_t c, uint32_t magic, uint32_t shift) {
+  const uint32_t q = (uint32_t)(((uint64_t)x * magic) >> shift);
+  return x - q * c;
 }
 
-// Column of coordinate i in row j, and the sign as a float sign-bit mask
+// Column of coordinate i in a row, and the sign as a float sign-bit mask
 // (0 for +1, 0x80000000 for -1).
+__device__ __forceinline__ void hash_row(const RowConst& k, uint32_t i, uint32_t& col, uint32_t& sflip) {
+  col = mod_c(mod_mersenne_affine(k.a, k.b, i), k.c, k.magic, k.shift);
+  sflip = ((mod_mersenne_affine(k.a2, k.b2, i) & 1u) ^ 1u) << 31;
+}
+
 __device__ __forceinline__ void hash_ij(const HashSet& hs, int j, uint32_t i, uint32_t& col, uint32_t& sflip) {
-  const RowHash rh = hs.row[j];
-  col = mod_c(mod_mersenne_affine(rh.a, rh.b, i), hs);
-  sflip = ((mod_mersenne_affine(rh.a2, rh.b2, i) & 1u) ^ 1u) << 31;
+  hash_row(row_const(hs, j), i, col, sflip);
 }
 
 __device__ __forceinline__ float apply_sign(float x, uint32_t sflip) {

@@ -37,6 +37,7 @@ struct PullPlan {
   int64_t chunk;          // coordinates per build chunk
 };
 constexpr int64_t kMaxFillLds = 160 * 1024;  // LDS of the list-fill kernel holds T cursors
+constexpr int kTilesPerCu = 1;               // resident pull workgroups per CU (LDS-limited)
 }  // namespace gs
 
 struct gs_ctx {

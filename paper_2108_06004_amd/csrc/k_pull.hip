@@ -9,8 +9,8 @@
 //   1. accumulates (u, v) and writes v worker-interleaved, vI[i][q] (one contiguous row of
 //      P floats per coordinate), so one gather serves every worker;
 //   2. runs one workgroup per (tile, list segment): gather vI rows of the listed
-//      coordinates, add s_j(i) * vI[i][q] into the LDS tile with fp64 LDS atomics, and
-//      write the tile out (no global atomics);
+//      coordinates, add s_j(i) * vI[i][q] into the LDS tile (worker-major, fp64, LDS
+//      atomics) and write the tile out (no global atomics);
 //   3. sums the segments of each cell in fixed order (fp64), rounds once to fp32 (the
 //      worker's table value) and merges the workers in the binomial-tree order.
 // All tiles walk their lists in ascending coordinate order at similar rates, so at any
@@ -21,6 +21,8 @@ namespace gs {
 namespace {
 
 constexpr int kBlock = 256;
+constexpr int kPullBlock = 256;  // threads of a pull workgroup (one tile per CU, see make_pull_plan)
+constexpr int kPullUnroll = 4;   // list entries per lane group in flight
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 int grid_for(int64_t work_items, int per_block, int cap) {
@@ -142,12 +144,12 @@ __global__ void __launch_bounds__(kBlock) k_accumulate_vi(const float* __restric
     for (int q = 0; q < P; ++q) {
       const int64_t o = q * n4 + t;
       const f4 gg = __builtin_nontemporal_load(reinterpret_cast<const f4*>(g) + o);
-      f4 uu = reinterpret_cast<const f4*>(u)[o];
-      f4 w = reinterpret_cast<const f4*>(v)[o];
+      f4 uu = __builtin_nontemporal_load(reinterpret_cast<const f4*>(u) + o);
+      f4 w = __builtin_nontemporal_load(reinterpret_cast<const f4*>(v) + o);
       uu = rho * uu + gg;
       w = w + uu;
-      reinterpret_cast<f4*>(u)[o] = uu;
-      reinterpret_cast<f4*>(v)[o] = w;
+      __builtin_nontemporal_store(uu, reinterpret_cast<f4*>(u) + o);
+      __builtin_nontemporal_store(w, reinterpret_cast<f4*>(v) + o);
       vv[q][0] = w.x;
       vv[q][1] = w.y;
       vv[q][2] = w.z;
@@ -206,35 +208,66 @@ __device__ __forceinline__ void load_row(const float* __restrict__ vI, uint32_t 
   }
 }
 
-template <int PP>
-__global__ void __launch_bounds__(kBlock) k_pull(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
-                                                 const int64_t* __restrict__ off, const float* __restrict__ vI,
-                                                 double* __restrict__ partial) {
-  extern __shared__ double acc[];  // [W][P]
-  const int P = pl.P;
+// L = PP/4 adjacent lanes share one list entry; lane `sub` of the group gathers workers
+// [4 sub, 4 sub + 4) of the row (16 B) and adds them into the tile.
+template <int P, int U>
+__global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
+                                                     const int64_t* __restrict__ off, const float* __restrict__ vI,
+                                                     double* __restrict__ partial) {
+  extern __shared__ double acc[];  // [P][W]: worker-major, so lanes adding for one worker hit spread banks
+  constexpr int PP = (P + 3) & ~3;
+  constexpr int L = PP / 4;
+  constexpr int64_t B = kPullBlock / L;  // entries per block pass
+  const int sub = threadIdx.x % L;
+  const int64_t tid = threadIdx.x / L;
   const int64_t item = blockIdx.x;
   const int64_t t = item / pl.S, s = item - t * pl.S;
   const int j = (int)(t / pl.tiles_per_row);
+  const RowConst k = row_const(hs, j);
   const int64_t col0 = (t - (int64_t)j * pl.tiles_per_row) * pl.W;
   const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - col0);
-  for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) acc[e] = 0.0;
+  for (int64_t e = threadIdx.x; e < wt * P; e += kPullBlock) acc[e] = 0.0;
   __syncthreads();
   const int64_t lo = off[t], n = off[t + 1] - lo;
   const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
-  for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
-    const uint32_t i = list[e];
-    uint32_t col, sflip;
-    hash_ij(hs, j, i, col, sflip);
-    float x[PP];
-    load_row<PP>(vI, i, x);
-    double* cell = acc + (int64_t)(col - col0) * P;
+  double* const mycol = acc + (int64_t)(4 * sub) * wt - col0;
+  int64_t eb = e0 + tid;
+  for (; eb + (U - 1) * B < e1; eb += U * B) {
+    uint32_t i[U];
 #pragma unroll
-    for (int q = 0; q < PP; ++q)
-      if (q < P) atomicAdd(cell + q, (double)apply_sign(x[q], sflip));
+    for (int m = 0; m < U; ++m) i[m] = list[eb + m * B];
+    f4 x[U];
+#pragma unroll
+    for (int m = 0; m < U; ++m) x[m] = reinterpret_cast<const f4*>(vI + (int64_t)i[m] * PP)[sub];
+#pragma unroll
+    for (int m = 0; m < U; ++m) {
+      uint32_t col, sflip;
+      hash_row(k, i[m], col, sflip);
+      double* cell = mycol + col;
+      const float xs[4] = {x[m].x, x[m].y, x[m].z, x[m].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (P % 4 == 0 || 4 * sub + q < P) atomicAdd(cell + q * wt, (double)apply_sign(xs[q], sflip));
+    }
+  }
+  for (; eb < e1; eb += B) {
+    const uint32_t i = list[eb];
+    const f4 x = reinterpret_cast<const f4*>(vI + (int64_t)i * PP)[sub];
+    uint32_t col, sflip;
+    hash_row(k, i, col, sflip);
+    double* cell = mycol + col;
+    const float xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (P % 4 == 0 || 4 * sub + q < P) atomicAdd(cell + q * wt, (double)apply_sign(xs[q], sflip));
   }
   __syncthreads();
-  double* dst = partial + ((s * hs.r + j) * (int64_t)hs.c + col0) * P;
-  for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) dst[e] = acc[e];
+  const int64_t rc = (int64_t)hs.r * hs.c;
+  double* dst = partial + s * P * rc + (int64_t)j * hs.c + col0;
+  for (int64_t e = threadIdx.x; e < wt * P; e += kPullBlock) {
+    const int64_t q = e / wt, o = e - q * wt;
+    dst[q * rc + o] = acc[e];
+  }
 }
 
 // Runtime-P variant (P > 16): rows of PP floats read element by element.
@@ -252,20 +285,25 @@ __global__ void __launch_bounds__(kBlock) k_pull_any(HashSet hs, PullPlan pl, co
   __syncthreads();
   const int64_t lo = off[t], n = off[t + 1] - lo;
   const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
+  const RowConst k = row_const(hs, j);
   for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
     const uint32_t i = list[e];
     uint32_t col, sflip;
-    hash_ij(hs, j, i, col, sflip);
-    double* cell = acc + (int64_t)(col - col0) * P;
-    for (int q = 0; q < P; ++q) atomicAdd(cell + q, (double)apply_sign(vI[(int64_t)i * PP + q], sflip));
+    hash_row(k, i, col, sflip);
+    double* cell = acc + (col - col0);
+    for (int q = 0; q < P; ++q) atomicAdd(cell + q * wt, (double)apply_sign(vI[(int64_t)i * PP + q], sflip));
   }
   __syncthreads();
-  double* dst = partial + ((s * hs.r + j) * (int64_t)hs.c + col0) * P;
-  for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) dst[e] = acc[e];
+  const int64_t rc = (int64_t)hs.r * hs.c;
+  double* dst = partial + s * P * rc + (int64_t)j * hs.c + col0;
+  for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) {
+    const int64_t q = e / wt, o = e - q * wt;
+    dst[q * rc + o] = acc[e];
+  }
 }
 
 // ------------------------------------------------------------------------------------
-// Segment sum + single rounding + tree merge. partial is [S][r][c][P] fp64.
+// Segment sum + single rounding + tree merge. partial is [S][P][r][c] fp64.
 
 template <int P>
 __global__ void __launch_bounds__(kBlock) k_merge_partials(const double* __restrict__ partial, int S, int64_t rc,
@@ -275,8 +313,8 @@ __global__ void __launch_bounds__(kBlock) k_merge_partials(const double* __restr
     float x[P];
 #pragma unroll
     for (int q = 0; q < P; ++q) {
-      double a = partial[e * P + q];
-      for (int s = 1; s < S; ++s) a += partial[(s * rc + e) * P + q];
+      double a = partial[q * rc + e];
+      for (int s = 1; s < S; ++s) a += partial[((int64_t)s * P + q) * rc + e];
       x[q] = (float)a;
     }
     if (tables) {
@@ -294,8 +332,8 @@ __global__ void __launch_bounds__(kBlock) k_merge_partials_any(const double* __r
   for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < rc; e += stride) {
     float x[kMaxWorkers];
     for (int q = 0; q < P; ++q) {
-      double a = partial[e * P + q];
-      for (int s = 1; s < S; ++s) a += partial[(s * rc + e) * P + q];
+      double a = partial[q * rc + e];
+      for (int s = 1; s < S; ++s) a += partial[((int64_t)s * P + q) * rc + e];
       x[q] = (float)a;
       if (tables) tables[q * rc + e] = x[q];
     }
@@ -311,11 +349,17 @@ hipError_t launch_acc_vi_p(const gs_ctx* x, hipStream_t s, const float* g, float
   return hipGetLastError();
 }
 
-template <int PP>
-void launch_pull_pp(const gs_ctx* x, hipStream_t s) {
+template <int P>
+void launch_pull_p(const gs_ctx* x, hipStream_t s) {
   const PullPlan& pl = x->plan;
-  hipLaunchKernelGGL(k_pull<PP>, dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kBlock),
+  hipLaunchKernelGGL((k_pull<P, kPullUnroll>), dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kPullBlock),
                      (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, x->vI, x->partial);
+}
+
+template <int P>
+hipError_t allow_pull_lds(size_t bytes) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull<P, kPullUnroll>),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
 }  // namespace
@@ -326,25 +370,51 @@ PullPlan make_pull_plan(int64_t d, int32_t P, int32_t r, int64_t c, int num_cus)
   PullPlan pl{};
   pl.P = P;
   pl.PP = (P + 3) & ~3;
-  // A tile holds W columns x P workers of fp64 accumulators in at most 64 KiB of LDS, so two
-  // workgroups share a CU.
-  int64_t W = 65536 / (8 * (int64_t)P);
+  // Tiles hold W columns x P workers of fp64 accumulators. Up to kTilesPerCu tiles of at
+  // most 160 KiB / kTilesPerCu share a CU; W is then shrunk so that the tiles fill whole
+  // rounds of resident workgroups (no ragged last round).
+  const int64_t cu_lds = 160 * 1024;
+  const int64_t max_w = (cu_lds / kTilesPerCu) / (8 * (int64_t)P);
+  int64_t W = max_w < 1 ? 1 : max_w;
   if (W > c) W = c;
-  if (W < 1) W = 1;
+  const int64_t slots = (int64_t)kTilesPerCu * num_cus;
+  int64_t tiles = (int64_t)r * ((c + W - 1) / W);
+  if (tiles > slots) {
+    const int64_t rounds = (tiles + slots - 1) / slots;
+    const int64_t per_row = (rounds * slots) / r;  // tiles per row that fill `rounds` rounds
+    if (per_row >= 1) {
+      const int64_t w2 = (c + per_row - 1) / per_row;
+      if (w2 >= 1 && w2 <= W) W = w2;
+    }
+  }
   pl.W = (int32_t)W;
   pl.tiles_per_row = (int32_t)((c + W - 1) / W);
   pl.T = r * pl.tiles_per_row;
-  // enough (tile, segment) work items to occupy every CU
-  const int64_t want = num_cus;
-  int64_t S = (want + pl.T - 1) / pl.T;
+  // small sketches: split each tile's list into segments so every CU gets work
+  int64_t S = (slots + pl.T - 1) / pl.T;
   const int64_t per_tile = (int64_t)r * d / pl.T;
-  if (S > per_tile / 256) S = per_tile / 256;  // keep segments at least 256 entries long
+  if (S > per_tile / 512) S = per_tile / 512;  // keep segments at least 512 entries long
   if (S < 1) S = 1;
   pl.S = (int32_t)S;
-  // build chunks: ~64 Ki coordinates each
+  // build chunks: 64 Ki coordinates each
   pl.chunk = 65536;
   pl.NB = (int32_t)((d + pl.chunk - 1) / pl.chunk);
   return pl;
+}
+
+hipError_t prepare_pull_kernels(const gs_ctx* x) {
+  const size_t bytes = (size_t)x->plan.W * x->plan.P * sizeof(double);
+  switch (x->P) {
+#define GS_ALLOW_CASE(PP) \
+  case PP: return allow_pull_lds<PP>(bytes);
+    GS_ALLOW_CASE(1) GS_ALLOW_CASE(2) GS_ALLOW_CASE(3) GS_ALLOW_CASE(4) GS_ALLOW_CASE(5) GS_ALLOW_CASE(6)
+    GS_ALLOW_CASE(7) GS_ALLOW_CASE(8) GS_ALLOW_CASE(9) GS_ALLOW_CASE(10) GS_ALLOW_CASE(11) GS_ALLOW_CASE(12)
+    GS_ALLOW_CASE(13) GS_ALLOW_CASE(14) GS_ALLOW_CASE(15) GS_ALLOW_CASE(16)
+#undef GS_ALLOW_CASE
+    default:
+      return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull_any),
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  }
 }
 
 hipError_t build_pull_lists(gs_ctx* x) {
@@ -352,6 +422,8 @@ hipError_t build_pull_lists(gs_ctx* x) {
   const size_t fill_lds = (size_t)pl.T * sizeof(uint32_t);
   hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_build_fill),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)fill_lds);
+  if (ea != hipSuccess) return ea;
+  ea = prepare_pull_kernels(x);
   if (ea != hipSuccess) return ea;
   uint32_t* counts = nullptr;
   uint32_t* total = nullptr;
@@ -400,11 +472,13 @@ hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v) {
 }
 
 hipError_t launch_pull(const gs_ctx* x, hipStream_t s) {
-  switch (x->plan.PP) {
-    case 4: launch_pull_pp<4>(x, s); break;
-    case 8: launch_pull_pp<8>(x, s); break;
-    case 12: launch_pull_pp<12>(x, s); break;
-    case 16: launch_pull_pp<16>(x, s); break;
+  switch (x->P) {
+#define GS_PULL_CASE(PP) \
+  case PP: launch_pull_p<PP>(x, s); break;
+    GS_PULL_CASE(1) GS_PULL_CASE(2) GS_PULL_CASE(3) GS_PULL_CASE(4) GS_PULL_CASE(5) GS_PULL_CASE(6) GS_PULL_CASE(7)
+    GS_PULL_CASE(8) GS_PULL_CASE(9) GS_PULL_CASE(10) GS_PULL_CASE(11) GS_PULL_CASE(12) GS_PULL_CASE(13)
+    GS_PULL_CASE(14) GS_PULL_CASE(15) GS_PULL_CASE(16)
+#undef GS_PULL_CASE
     default: {
       const PullPlan& pl = x->plan;
       hipLaunchKernelGGL(k_pull_any, dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kBlock),

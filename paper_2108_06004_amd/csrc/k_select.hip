@@ -102,6 +102,9 @@ __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __
                                                      uint32_t* __restrict__ hist) {
   __shared__ uint32_t h[kDigit1Bins];
   for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
+  RowConst kr[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
   __syncthreads();
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < d; i += stride) {
@@ -109,7 +112,7 @@ __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __
 #pragma unroll
     for (int j = 0; j < R; ++j) {
       uint32_t col, sflip;
-      hash_ij(hs, j, (uint32_t)i, col, sflip);
+      hash_row(kr[j], (uint32_t)i, col, sflip);
       val[j] = apply_sign(merged[(int64_t)j * hs.c + col], sflip);
     }
     sort_net<R>(val);
@@ -153,34 +156,80 @@ __global__ void __launch_bounds__(kSelBlock) k_select1(uint32_t* __restrict__ hi
 // ------------------------------------------------------------------------------------
 // 3. Candidate compaction (digit 1 >= b1) and bitmap clearing.
 
+// Each block scans a contiguous range of keys and collects its candidates in an LDS buffer
+// (one LDS atomic per wave), flushing it to the global list with a single global atomic
+// when it could overflow and at the end: the global counter sees a few hundred atomics
+// instead of one per wave.
+constexpr int kCompactBuf = 4096;
+
 __global__ void __launch_bounds__(kBlock) k_compact(const uint32_t* __restrict__ keys, int64_t d,
                                                     SelectCtl* __restrict__ ctl, uint32_t* __restrict__ cand_key,
                                                     int32_t* __restrict__ cand_idx, int64_t cap,
-                                                    uint32_t* __restrict__ bitmap) {
+                                                    uint32_t* __restrict__ bitmap, int64_t per_block) {
+  __shared__ uint32_t bkey[kCompactBuf];
+  __shared__ int32_t bidx[kCompactBuf];
+  __shared__ uint32_t bn;
+  __shared__ uint32_t gbase;
   const uint32_t b1 = ctl->b1;
-  const int lane = threadIdx.x & 63;
-  const int64_t wave0 = ((int64_t)blockIdx.x * kBlock + (threadIdx.x & ~63));
-  const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t base = wave0; base < d; base += stride) {  // uniform per wave
-    const int64_t i = base + lane;
-    const bool valid = i < d;
-    const uint32_t key = valid ? keys[i] : 0u;
-    const bool take = valid && (key >> kDigit1Shift) >= b1;
-    const uint64_t m = __ballot(take);
-    if (m) {
-      const int leader = __ffsll((unsigned long long)m) - 1;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const uint64_t below = (1ull << lane) - 1ull;
+  if (threadIdx.x == 0) bn = 0;
+  __syncthreads();
+  const int64_t lo = (int64_t)blockIdx.x * per_block, hi = min(d, lo + per_block);
+  for (int64_t blk = lo; blk < hi; blk += 4 * kBlock) {  // block-uniform: 1024 keys per pass
+    const int64_t base = blk + (int64_t)wid * 256;
+    const int64_t i0 = base + 4 * lane;
+    uint32_t key[4];
+    if (i0 + 3 < hi) {
+      const uint4 k4 = *reinterpret_cast<const uint4*>(keys + i0);
+      key[0] = k4.x; key[1] = k4.y; key[2] = k4.z; key[3] = k4.w;
+    } else {
+#pragma unroll
+      for (int m = 0; m < 4; ++m) key[m] = (i0 + m < hi) ? keys[i0 + m] : 0u;
+    }
+    bool take[4];
+    uint64_t mask[4];
+    uint32_t cnt[4], total = 0;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+      take[m] = (i0 + m < hi) && (key[m] >> kDigit1Shift) >= b1;
+      mask[m] = __ballot(take[m]);
+      cnt[m] = (uint32_t)__popcll(mask[m]);
+      total += cnt[m];
+    }
+    if (total) {
       uint32_t slot = 0;
-      if (lane == leader) slot = atomicAdd(&ctl->n_cand, (uint32_t)__popcll(m));
-      slot = __shfl(slot, leader, 64);
-      if (take) {
-        const int64_t pos = (int64_t)slot + __popcll(m & ((1ull << lane) - 1ull));
-        if (pos < cap) {
-          cand_key[pos] = key;
-          cand_idx[pos] = (int32_t)i;
+      if (lane == 0) slot = atomicAdd(&bn, total);
+      slot = __shfl(slot, 0, 64);
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        if (take[m]) {
+          const uint32_t pos = slot + (uint32_t)__popcll(mask[m] & below);
+          bkey[pos] = key[m];
+          bidx[pos] = (int32_t)(i0 + m);
         }
+        slot += cnt[m];
       }
     }
-    if (valid && (i & 31) == 0) bitmap[i >> 5] = 0u;
+    if (lane < 8 && base + 32 * lane < hi) bitmap[(base >> 5) + lane] = 0u;
+    __syncthreads();
+    const uint32_t n = bn;
+    const bool last = blk + 4 * kBlock >= hi;
+    if (n > kCompactBuf - 4 * kBlock || (last && n > 0)) {  // the next pass could overflow, or done
+      if (threadIdx.x == 0) gbase = atomicAdd(&ctl->n_cand, n);
+      __syncthreads();
+      const uint32_t g0 = gbase;
+      for (uint32_t t = threadIdx.x; t < n; t += kBlock) {
+        const int64_t pos = (int64_t)g0 + t;
+        if (pos < cap) {
+          cand_key[pos] = bkey[t];
+          cand_idx[pos] = bidx[t];
+        }
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) bn = 0;
+    }
+    __syncthreads();
   }
 }
 
@@ -352,8 +401,15 @@ hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, i
     default: return hipErrorInvalidValue;
   }
   hipLaunchKernelGGL(k_select1, dim3(1), dim3(kSelBlock), 0, s, x->hist, x->ctl, (uint32_t)k);
-  hipLaunchKernelGGL(k_compact, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->keys, x->d,
-                     x->ctl, x->cand_key, x->cand_idx, x->cand_cap, x->bitmap);
+  {
+    // contiguous ranges, a multiple of 1024 keys each (so bitmap words never straddle blocks)
+    const int64_t nb = grid_for(x->d, 4 * kBlock, 4 * x->num_cus);
+    int64_t per_block = (x->d + nb - 1) / nb;
+    per_block = (per_block + 4 * kBlock - 1) / (4 * kBlock) * (4 * kBlock);
+    const int64_t grid = (x->d + per_block - 1) / per_block;
+    hipLaunchKernelGGL(k_compact, dim3((unsigned)grid), dim3(kBlock), 0, s, x->keys, x->d, x->ctl, x->cand_key,
+                       x->cand_idx, x->cand_cap, x->bitmap, per_block);
+  }
   hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap);
   hipLaunchKernelGGL(k_finalize, dim3(4 * x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl,
                      x->cand_cap, x->bitmap);
