@@ -45,7 +45,7 @@ hipError_t alloc(T** p, int64_t count) {
 
 void free_scratch(gs_ctx* x) {
   void* ptrs[] = {x->keys, x->hist, x->ctl, x->cand_key, x->cand_idx, x->bitmap, x->blockcnt, x->acc64,
-                  x->list, x->tile_off, x->vI, x->partial};
+                  x->list, x->tile_off, x->vI, x->partial, x->sample_keys, x->heavy};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   x->keys = nullptr;
@@ -60,6 +60,8 @@ void free_scratch(gs_ctx* x) {
   x->tile_off = nullptr;
   x->vI = nullptr;
   x->partial = nullptr;
+  x->sample_keys = nullptr;
+  x->heavy = nullptr;
 }
 
 bool valid_ab(const uint32_t* a, const uint32_t* b, int r) {
@@ -154,6 +156,8 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   chk(alloc(&x->cand_idx, x->cand_cap));
   chk(alloc(&x->bitmap, words));
   chk(alloc(&x->blockcnt, x->emit_blocks));
+  chk(alloc(&x->sample_keys, gs::kSampleMax));
+  chk(alloc(&x->heavy, ((int64_t)x->r * x->c + 63) / 64 * 2));
   x->plan = gs::make_pull_plan(x->d, x->P, x->r, x->c, x->num_cus);
   x->use_pull = (int64_t)x->plan.T * (int64_t)sizeof(uint32_t) <= gs::kMaxFillLds;
   if (x->use_pull) {
@@ -168,6 +172,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   if (ea == hipSuccess) ea = hipMemset(x->ctl, 0, sizeof(gs::SelectCtl));
   if (ea == hipSuccess) ea = hipDeviceSynchronize();
   if (ea == hipSuccess && x->use_pull) ea = gs::build_pull_lists(x);
+  if (ea == hipSuccess) ea = gs::prepare_prune(x);
   if (ea != hipSuccess) {
     const bool oom = ea == hipErrorOutOfMemory || ea == hipErrorMemoryAllocation;
     g_create_error = std::string("device scratch allocation failed: ") + hipGetErrorString(ea);

@@ -23,8 +23,11 @@ struct SelectCtl {
   uint32_t tau;         // the k-th largest key
   uint32_t iota;        // largest index taken among keys equal to tau
   uint32_t status;      // 0 ok; nonzero: candidate overflow (must not happen)
+  uint32_t tau0;        // pruning bound: a key no larger than the k-th key (when no fallback)
+  uint32_t fallback;    // 1: fewer than k coordinates reach tau0, run the unpruned selection
   uint32_t pad;
 };
+constexpr int kSampleMax = 16384;  // sampled estimates for the pruning bound
 
 // Geometry of the gather-based sketch: tiles of W columns of one row, all P workers, fp64.
 struct PullPlan {
@@ -58,6 +61,12 @@ struct gs_ctx {
   int64_t cand_cap = 0;
   uint32_t* bitmap = nullptr;     // [ceil(d/32)]
   uint32_t* blockcnt = nullptr;   // [emit blocks]
+  uint32_t* sample_keys = nullptr;  // [kSampleMax]
+  uint32_t* heavy = nullptr;        // [ceil(r*c/64)*2] heavy-cell bitmap
+  int64_t prune_map_words = 0;      // words of the heavy bitmap
+  int prune_map_in_lds = 0;         // 1: the pruned pass keeps the bitmap in LDS
+  int prune_buf_cap = 0;            // LDS candidate buffer entries of the pruned pass
+  size_t prune_lds = 0;             // dynamic LDS bytes of the pruned pass
   int64_t emit_blocks = 0;
   // gather-based sketch (used when the plan fits; otherwise fp64 atomics into acc64)
   bool use_pull = false;
@@ -83,6 +92,7 @@ hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, i
 hipError_t launch_gather_reset(const gs_ctx* x, hipStream_t s, const int32_t* idx, int64_t k, float* u, float* v,
                                float* values);
 int64_t emit_blocks_for(int64_t d);
+hipError_t prepare_prune(gs_ctx* x);
 PullPlan make_pull_plan(int64_t d, int32_t P, int32_t r, int64_t c, int num_cus);
 hipError_t build_pull_lists(gs_ctx* x);
 hipError_t launch_accumulate_vi(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v);

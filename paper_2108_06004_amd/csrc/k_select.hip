@@ -15,6 +15,8 @@
 //   5. finalize: candidates with key > tau, or key == tau and index <= iota, set their bit;
 //   6. emit: the bitmap is turned into ascending indices (per-block popcounts, then a
 //      block-local scan offset by the preceding blocks' totals).
+#include <cmath>
+
 #include "gs_internal.hpp"
 
 namespace gs {
@@ -99,7 +101,8 @@ __device__ void find_bucket(const uint32_t* h, int nbins, bool descending, uint3
 template <int R>
 __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __restrict__ merged, int64_t d,
                                                      float* __restrict__ est, uint32_t* __restrict__ keys,
-                                                     uint32_t* __restrict__ hist) {
+                                                     uint32_t* __restrict__ hist, const SelectCtl* __restrict__ gate) {
+  if (gate && gate->fallback == 0u) return;  // the pruned selection sufficed
   __shared__ uint32_t h[kDigit1Bins];
   for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
   RowConst kr[R];
@@ -134,7 +137,8 @@ __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __
 // candidate counter for the compaction pass.
 
 __global__ void __launch_bounds__(kSelBlock) k_select1(uint32_t* __restrict__ hist, SelectCtl* __restrict__ ctl,
-                                                       uint32_t k) {
+                                                       uint32_t k, int gated) {
+  if (gated && ctl->fallback == 0u) return;
   __shared__ uint32_t h[kDigit1Bins];
   __shared__ uint32_t shw[kSelBlock / 64];
   __shared__ uint32_t res[2];
@@ -165,7 +169,8 @@ constexpr int kCompactBuf = 4096;
 __global__ void __launch_bounds__(kBlock) k_compact(const uint32_t* __restrict__ keys, int64_t d,
                                                     SelectCtl* __restrict__ ctl, uint32_t* __restrict__ cand_key,
                                                     int32_t* __restrict__ cand_idx, int64_t cap,
-                                                    uint32_t* __restrict__ bitmap, int64_t per_block) {
+                                                    uint32_t* __restrict__ bitmap, int64_t per_block, int gated) {
+  if (gated && ctl->fallback == 0u) return;
   __shared__ uint32_t bkey[kCompactBuf];
   __shared__ int32_t bidx[kCompactBuf];
   __shared__ uint32_t bn;
@@ -333,6 +338,239 @@ __global__ void __launch_bounds__(kBlock) k_finalize(const uint32_t* __restrict_
 }
 
 // ------------------------------------------------------------------------------------
+// Pruned estimate (used when no estimate vector is requested). A coordinate whose median
+// over rows has |est| >= tau0 has at least ceil(r/2) cells with |cell| >= tau0 (odd r: the
+// median and the values beyond it; even r: the upper (or lower) half, since
+// fl(fl(m1 + m2) * 0.5) never exceeds m2 in magnitude). So with tau0 no larger than the
+// k-th |est|, only coordinates with ceil(r/2) "heavy" cells can be selected, and a bitmap
+// of heavy cells replaces most table reads. tau0 is the rho-th largest of M sampled exact
+// estimates, rho ~ 2 M k / d plus a margin; if fewer than k coordinates reach tau0 the
+// unpruned kernels (gated on ctl->fallback) redo the selection, so the result is exact
+// either way.
+
+template <int R>
+__device__ __forceinline__ uint32_t estimate_key(const RowConst (&kr)[R], const float* __restrict__ merged,
+                                                 uint32_t i) {
+  float val[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    uint32_t col, sflip;
+    hash_row(kr[j], i, col, sflip);
+    val[j] = apply_sign(merged[(int64_t)j * kr[j].c + col], sflip);
+  }
+  sort_net<R>(val);
+  return abs_key(median_sorted<R>(val));
+}
+
+template <int R>
+__global__ void __launch_bounds__(kBlock) k_sample(HashSet hs, const float* __restrict__ merged, int64_t d, int M,
+                                                   uint32_t* __restrict__ out) {
+  RowConst kr[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
+  const int s = blockIdx.x * kBlock + threadIdx.x;
+  if (s >= M) return;
+  out[s] = estimate_key<R>(kr, merged, (uint32_t)(((int64_t)s * d) / M));
+}
+
+// tau0 = the rho-th largest sampled key (three radix digits in one block).
+__global__ void __launch_bounds__(kSelBlock) k_tau0(const uint32_t* __restrict__ sample, int M, uint32_t rho,
+                                                    SelectCtl* __restrict__ ctl, uint32_t k) {
+  __shared__ uint32_t key[kSampleMax];
+  __shared__ uint32_t h[kDigit1Bins];
+  __shared__ uint32_t shw[kSelBlock / 64];
+  __shared__ uint32_t res[2];
+  for (int t = threadIdx.x; t < M; t += kSelBlock) key[t] = sample[t];
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) h[b] = 0u;
+  __syncthreads();
+  for (int t = threadIdx.x; t < M; t += kSelBlock) atomicAdd(&h[key[t] >> 20], 1u);
+  __syncthreads();
+  find_bucket(h, kDigit1Bins, true, rho, shw, res);
+  const uint32_t b1 = res[0], need2 = rho - res[1];
+  __syncthreads();
+  for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
+  __syncthreads();
+  for (int t = threadIdx.x; t < M; t += kSelBlock)
+    if ((key[t] >> 20) == b1) atomicAdd(&h[(key[t] >> 10) & 1023u], 1u);
+  __syncthreads();
+  find_bucket(h, kDigitBins, true, need2, shw, res);
+  const uint32_t pre = (b1 << 10) | res[0], need3 = need2 - res[1];
+  __syncthreads();
+  for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
+  __syncthreads();
+  for (int t = threadIdx.x; t < M; t += kSelBlock)
+    if ((key[t] >> 10) == pre) atomicAdd(&h[key[t] & 1023u], 1u);
+  __syncthreads();
+  find_bucket(h, kDigitBins, true, need3, shw, res);
+  if (threadIdx.x == 0) {
+    ctl->tau0 = (pre << 10) | res[0];
+    ctl->k = k;
+    ctl->n_cand = 0u;
+    ctl->fallback = 0u;
+    ctl->status = 0u;
+  }
+}
+
+// Heavy-cell bitmap: bit e of the flat [r][c] sketch is |merged[e]| >= tau0 (one ballot
+// per 64 cells).
+__global__ void __launch_bounds__(kBlock) k_heavy(const float* __restrict__ merged, int64_t rc,
+                                                  const SelectCtl* __restrict__ ctl, uint32_t* __restrict__ heavy) {
+  const uint32_t tau0 = ctl->tau0;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t base = ((int64_t)blockIdx.x * kBlock + threadIdx.x) & ~63ll; base < rc; base += stride) {
+    const int64_t e = base + (threadIdx.x & 63);
+    const bool hv = e < rc && abs_key(merged[e]) >= tau0;
+    const uint64_t m = __ballot(hv);
+    if ((threadIdx.x & 63) == 0) {
+      heavy[(base >> 5)] = (uint32_t)m;
+      heavy[(base >> 5) + 1] = (uint32_t)(m >> 32);
+    }
+  }
+}
+
+// The pruned pass: every coordinate checks its r heavy bits (early exit once ceil(r/2)
+// is out of reach); survivors compute their exact estimate and, if it reaches tau0, are
+// appended to the candidate list through an LDS buffer (one global atomic per flush).
+// The output bitmap words are cleared on the way. dynamic LDS: [map words?][buf keys][buf idx]
+constexpr int kPruneBlock = 1024;  // 16 waves per CU; the heavy bitmap fills the LDS
+
+template <int R>
+__global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, const float* __restrict__ merged, int64_t d,
+                                                   SelectCtl* __restrict__ ctl, const uint32_t* __restrict__ heavy,
+                                                   int64_t map_words, int map_in_lds, int buf_cap,
+                                                   uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx,
+                                                   int64_t cap, uint32_t* __restrict__ bitmap) {
+  constexpr int U = 4;  // coordinates per lane per pass: independent hash chains in flight
+  extern __shared__ uint32_t sm[];
+  __shared__ uint32_t bn, gbase;
+  const uint32_t* map = heavy;
+  uint32_t* bkey = sm;
+  if (map_in_lds) {
+    // map_words is even and the map 8-byte aligned: copy 16 bytes per lane, 8 loads in flight
+    const int64_t n4 = map_words / 4;
+    const uint4* src = reinterpret_cast<const uint4*>(heavy);
+    uint4* dst = reinterpret_cast<uint4*>(sm);
+    int64_t w = threadIdx.x;
+    for (; w + 7 * kPruneBlock < n4; w += 8 * kPruneBlock) {
+      uint4 t[8];
+#pragma unroll
+      for (int m = 0; m < 8; ++m) t[m] = src[w + m * kPruneBlock];
+#pragma unroll
+      for (int m = 0; m < 8; ++m) dst[w + m * kPruneBlock] = t[m];
+    }
+    for (; w < n4; w += kPruneBlock) dst[w] = src[w];
+    for (int64_t x = 4 * n4 + threadIdx.x; x < map_words; x += kPruneBlock) sm[x] = heavy[x];
+    map = sm;
+    bkey = sm + map_words;
+  }
+  int32_t* bidx = reinterpret_cast<int32_t*>(bkey + buf_cap);
+  RowConst kr[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
+  const uint32_t tau0 = ctl->tau0;
+  constexpr int need = (R + 1) / 2;
+  if (threadIdx.x == 0) bn = 0;
+  __syncthreads();
+  const int64_t stride = (int64_t)gridDim.x * kPruneBlock * U;
+  for (int64_t base = (int64_t)blockIdx.x * kPruneBlock * U; base < d; base += stride) {  // block-uniform
+    int cnt[U];
+#pragma unroll
+    for (int m = 0; m < U; ++m) {
+      const int64_t i = base + threadIdx.x + (int64_t)m * kPruneBlock;
+      cnt[m] = 0;
+#pragma unroll
+      for (int j = 0; j < R; ++j) {
+        const uint32_t col = mod_c(mod_mersenne_affine(kr[j].a, kr[j].b, (uint32_t)i), kr[j].c, kr[j].magic,
+                                   kr[j].shift);
+        const int64_t e = (int64_t)j * kr[j].c + col;
+        cnt[m] += (map[e >> 5] >> (e & 31)) & 1u;
+      }
+      if (i >= d) cnt[m] = 0;
+    }
+#pragma unroll
+    for (int m = 0; m < U; ++m) {
+      const int64_t i = base + threadIdx.x + (int64_t)m * kPruneBlock;
+      if (cnt[m] >= need) {
+        const uint32_t key = estimate_key<R>(kr, merged, (uint32_t)i);
+        if (key >= tau0) {
+          const uint32_t pos = atomicAdd(&bn, 1u);
+          if (pos < (uint32_t)buf_cap) {
+            bkey[pos] = key;
+            bidx[pos] = (int32_t)i;
+          } else {  // buffer full within this pass (dense candidates): append directly
+            const uint32_t gpos = atomicAdd(&ctl->n_cand, 1u);
+            if ((int64_t)gpos < cap) {
+              cand_key[gpos] = key;
+              cand_idx[gpos] = (int32_t)i;
+            }
+          }
+        }
+      }
+      if (i < d && (i & 31) == 0) bitmap[i >> 5] = 0u;
+    }
+    __syncthreads();
+    const uint32_t n = min(bn, (uint32_t)buf_cap);
+    const bool last = base + stride >= d;
+    if (n >= (uint32_t)(buf_cap / 2) || (last && n > 0)) {
+      if (threadIdx.x == 0) gbase = atomicAdd(&ctl->n_cand, n);
+      __syncthreads();
+      const uint32_t g0 = gbase;
+      for (uint32_t t = threadIdx.x; t < n; t += kPruneBlock) {
+        const int64_t pos = (int64_t)g0 + t;
+        if (pos < cap) {
+          cand_key[pos] = bkey[t];
+          cand_idx[pos] = bidx[t];
+        }
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) bn = 0;
+    }
+    __syncthreads();
+  }
+}
+
+// Digit-1 histogram of the candidates (skipped when the fallback will run).
+__global__ void __launch_bounds__(kBlock) k_cand_hist(const uint32_t* __restrict__ cand_key,
+                                                      const SelectCtl* __restrict__ ctl, int64_t cap,
+                                                      uint32_t* __restrict__ hist) {
+  if (ctl->n_cand < ctl->k) return;
+  __shared__ uint32_t h[kDigit1Bins];
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
+  __syncthreads();
+  const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n; t += stride)
+    atomicAdd(&h[cand_key[t] >> kDigit1Shift], 1u);
+  __syncthreads();
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) {
+    const uint32_t c = h[b];
+    if (c) atomicAdd(&hist[b], c);
+  }
+}
+
+// Digit-1 bucket over the candidates, or raise the fallback flag.
+__global__ void __launch_bounds__(kSelBlock) k_select1p(uint32_t* __restrict__ hist, SelectCtl* __restrict__ ctl) {
+  __shared__ uint32_t h[kDigit1Bins];
+  __shared__ uint32_t shw[kSelBlock / 64];
+  __shared__ uint32_t res[2];
+  const uint32_t k = ctl->k;
+  if (ctl->n_cand < k) {
+    if (threadIdx.x == 0) ctl->fallback = 1u;
+    return;
+  }
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) {
+    h[b] = hist[b];
+    hist[b] = 0u;
+  }
+  __syncthreads();
+  find_bucket(h, kDigit1Bins, true, k, shw, res);
+  if (threadIdx.x == 0) {
+    ctl->b1 = res[0];
+    ctl->above1 = res[1];
+  }
+}
+
+// ------------------------------------------------------------------------------------
 // 6. Bitmap -> ascending index list.
 
 __global__ void __launch_bounds__(kSelBlock) k_emit_count(const uint32_t* __restrict__ bitmap, int64_t words,
@@ -379,9 +617,39 @@ __global__ void __launch_bounds__(kSelBlock) k_emit_write(const uint32_t* __rest
 }
 
 template <int R>
-void launch_unsketch_r(gs_ctx* x, hipStream_t s, const float* merged, float* est) {
+void launch_unsketch_r(gs_ctx* x, hipStream_t s, const float* merged, float* est, const SelectCtl* gate) {
   hipLaunchKernelGGL(k_unsketch<R>, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->hs, merged,
-                     x->d, est, x->keys, x->hist);
+                     x->d, est, x->keys, x->hist, gate);
+}
+
+template <int R>
+void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k) {
+  const int M = (int)(x->d < kSampleMax ? x->d : kSampleMax);
+  const double mk = (double)M * (double)k / (double)x->d;
+  // expected sampled keys above the k-th key: mk (sd ~ sqrt(mk)); the margin is ~8 sd
+  double rho_d = std::ceil(1.2 * mk + 5.0 * std::sqrt(mk) + 8.0);
+  if (rho_d > M) rho_d = M;
+  if (rho_d < 1) rho_d = 1;
+  hipLaunchKernelGGL(k_sample<R>, dim3((M + kBlock - 1) / kBlock), dim3(kBlock), 0, s, x->hs, merged, x->d, M,
+                     x->sample_keys);
+  hipLaunchKernelGGL(k_tau0, dim3(1), dim3(kSelBlock), 0, s, x->sample_keys, M, (uint32_t)rho_d, x->ctl, (uint32_t)k);
+  const int64_t rc = (int64_t)x->r * x->c;
+  hipLaunchKernelGGL(k_heavy, dim3(grid_for(rc, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, merged, rc, x->ctl,
+                     x->heavy);
+  // with the bitmap in LDS one block fits a CU: launch one per CU so the map is loaded once
+  const int pgrid = grid_for(x->d, 4 * kPruneBlock, x->prune_map_in_lds ? x->num_cus : 2 * x->num_cus);
+  hipLaunchKernelGGL(k_pruned<R>, dim3(pgrid), dim3(kPruneBlock), x->prune_lds, s, x->hs,
+                     merged, x->d, x->ctl, x->heavy, x->prune_map_words, x->prune_map_in_lds, x->prune_buf_cap,
+                     x->cand_key, x->cand_idx, x->cand_cap, x->bitmap);
+  hipLaunchKernelGGL(k_cand_hist, dim3(grid_for(4 * k, kBlock, x->num_cus)), dim3(kBlock), 0, s, x->cand_key, x->ctl,
+                     x->cand_cap, x->hist);
+  hipLaunchKernelGGL(k_select1p, dim3(1), dim3(kSelBlock), 0, s, x->hist, x->ctl);
+}
+
+template <int R>
+hipError_t allow_prune_lds(size_t bytes) {
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pruned<R>), hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)bytes);
 }
 
 }  // namespace
@@ -391,16 +659,51 @@ int64_t emit_blocks_for(int64_t d) {
   return (words + kEmitWordsPerBlock - 1) / kEmitWordsPerBlock;
 }
 
-hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, float* est, int32_t* idx) {
+hipError_t prepare_prune(gs_ctx* x) {
+  const int64_t rc = (int64_t)x->r * x->c;
+  const int64_t words = (rc + 63) / 64 * 2;
+  const int64_t lds_max = 160 * 1024 - 256;
+  x->prune_map_words = words;
+  int64_t buf = (lds_max - words * 4) / 8;
+  if (buf > 4096) buf = 4096;
+  if (buf >= 256) {
+    x->prune_map_in_lds = 1;
+    x->prune_buf_cap = (int)buf;
+    x->prune_lds = (size_t)(words * 4 + buf * 8);
+  } else {
+    x->prune_map_in_lds = 0;
+    x->prune_buf_cap = 4096;
+    x->prune_lds = 4096 * 8;
+  }
   switch (x->r) {
 #define GS_R_CASE(RR) \
-  case RR: launch_unsketch_r<RR>(x, s, merged, est); break;
+  case RR: return allow_prune_lds<RR>(x->prune_lds);
     GS_R_CASE(1) GS_R_CASE(2) GS_R_CASE(3) GS_R_CASE(4) GS_R_CASE(5) GS_R_CASE(6) GS_R_CASE(7) GS_R_CASE(8)
     GS_R_CASE(9) GS_R_CASE(10) GS_R_CASE(11) GS_R_CASE(12) GS_R_CASE(13) GS_R_CASE(14) GS_R_CASE(15) GS_R_CASE(16)
 #undef GS_R_CASE
     default: return hipErrorInvalidValue;
   }
-  hipLaunchKernelGGL(k_select1, dim3(1), dim3(kSelBlock), 0, s, x->hist, x->ctl, (uint32_t)k);
+}
+
+hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, float* est, int32_t* idx) {
+  // With an estimate vector requested every coordinate is estimated (unpruned path).
+  // Otherwise the pruned path runs and the unpruned kernels only act if it raised the
+  // fallback flag.
+  const bool prune = (est == nullptr);
+  const SelectCtl* gate = prune ? x->ctl : nullptr;
+  switch (x->r) {
+#define GS_R_CASE(RR) \
+  case RR:                                            \
+    if (prune) launch_prune_r<RR>(x, s, merged, k);  \
+    launch_unsketch_r<RR>(x, s, merged, est, gate);  \
+    break;
+    GS_R_CASE(1) GS_R_CASE(2) GS_R_CASE(3) GS_R_CASE(4) GS_R_CASE(5) GS_R_CASE(6) GS_R_CASE(7) GS_R_CASE(8)
+    GS_R_CASE(9) GS_R_CASE(10) GS_R_CASE(11) GS_R_CASE(12) GS_R_CASE(13) GS_R_CASE(14) GS_R_CASE(15) GS_R_CASE(16)
+#undef GS_R_CASE
+    default: return hipErrorInvalidValue;
+  }
+  const int gated = prune ? 1 : 0;
+  hipLaunchKernelGGL(k_select1, dim3(1), dim3(kSelBlock), 0, s, x->hist, x->ctl, (uint32_t)k, gated);
   {
     // contiguous ranges, a multiple of 1024 keys each (so bitmap words never straddle blocks)
     const int64_t nb = grid_for(x->d, 4 * kBlock, 4 * x->num_cus);
@@ -408,7 +711,7 @@ hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, i
     per_block = (per_block + 4 * kBlock - 1) / (4 * kBlock) * (4 * kBlock);
     const int64_t grid = (x->d + per_block - 1) / per_block;
     hipLaunchKernelGGL(k_compact, dim3((unsigned)grid), dim3(kBlock), 0, s, x->keys, x->d, x->ctl, x->cand_key,
-                       x->cand_idx, x->cand_cap, x->bitmap, per_block);
+                       x->cand_idx, x->cand_cap, x->bitmap, per_block, gated);
   }
   hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap);
   hipLaunchKernelGGL(k_finalize, dim3(4 * x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl,

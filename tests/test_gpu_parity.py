@@ -151,6 +151,10 @@ def chain_check(dv: Dev, g, u0, v0, k, rho, reset_momentum=True, full_tables=Tru
         assert np.array_equal(eg, oracle.unsketch(mg, hp, d)), f"{label}: estimates not exact"
     check_topk_of(eg, ig, k, label)
     ref_idx = ig
+    # without an estimate vector the pruned selection runs: it must give the same set
+    idx_p = torch.empty(k, dtype=torch.int32, device=DEV)
+    dv.ctx.unsketch_topk(dv.merged, k, idx_p)
+    assert np.array_equal(host(idx_p), ig), f"{label}: pruned selection differs from the full one"
     n_tie = 0
     if end_to_end and ora_tables is not None:
         est_o = oracle.unsketch(ora_merged, hp, d)
@@ -300,6 +304,8 @@ EDGE = [
     (3001, 17, 5, 97, 60),      # P beyond the unrolled instances
     (100_003, 1, 1, 30_011, 7), # r = 1: one signed lookup
     (65_536, 2, 16, 4096, 655), # maximum r
+    (20_000, 2, 3, 500, 19_999),  # k near d: the sampled pruning bound admits fewer than k
+    (50_000, 3, 5, 300, 40_000),  # coordinates, so the unpruned selection takes over
 ]
 
 
