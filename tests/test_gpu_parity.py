@@ -280,14 +280,15 @@ def test_full_size_step(name, step):
 def test_full_size_rowsparse_sampled():
     # 66M coordinates x 16 workers: the oracle checks 4,000 sampled cells per worker, the
     # estimates at 200,000 sampled coordinates plus the selection, the merge, the top-k
-    # of the GPU's estimates and the reset in full.
+    # of the GPU's estimates and the reset in full; the fused step (chunked, overlapped
+    # accumulation and sketch) against the separate calls.
     w = synth.WORKLOADS["rowsparse-d66M-P16"]
     hp = synth.hash_params(w)
     dv = Dev(w.d, w.P, w.r, w.c, w.k, hp, w.rho)
     u = np.zeros((w.P, w.d), np.float32)
     v = np.zeros((w.P, w.d), np.float32)
     chain_check(dv, synth.gradients(w, 0), u, v, w.k, w.rho, full_tables=False, ncells=4000, n_est=200_000,
-                end_to_end=False, fused=False, label=f"{w.name} step 0")
+                end_to_end=False, fused=True, label=f"{w.name} step 0")
     dv.close()
 
 
