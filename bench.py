@@ -15,8 +15,11 @@ Algorithmic bytes per step: B = 20*P*d + 8*P*r*c + 8*r*c + 12*P*k + 8*k.
 from __future__ import annotations
 
 import argparse
+import glob
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -45,6 +48,45 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def kernel_source_digest() -> str:
+    """SHA-256 over the HIP sources (file names and contents, sorted)."""
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2108_06004_amd", "csrc", "*"))):
+        h.update(os.path.basename(p).encode())
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def stage_kernels(w) -> dict:
+    """The kernels each stage of the fused step launches (names as rocprofv3 reports them)."""
+    return {
+        "accumulate": [f"k_accumulate_vi<{w.P}>"],
+        "sketch": [f"k_pull<{w.P}, 4>"],
+        "merge": [f"k_merge_partials<{w.P}>"],
+        "select": [f"k_sample<{w.r}>", "k_tau0", "k_heavy", f"k_pruned<{w.r}>", "k_cand_hist", "k_select1p",
+                   "k_select2", "k_finalize", "k_emit_count", "k_emit_write"],
+        "gather_reset": [f"k_gather_reset<{w.P}>"],
+    }
+
+
+def measured_traffic(w, stage: str):
+    """HBM-side bytes per launch of `stage` from the committed counter summary, or None when
+    there is none for this workload or the kernels changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_gs_step_{w.name}.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"source_sha256: ([0-9a-f]{64})", text)
+    if not m or m.group(1) != kernel_source_digest():
+        return None
+    table = {name.strip(): float(val) for name, val in re.findall(r"traffic: (.+?) \| ([0-9.]+)", text)}
+    names = stage_kernels(w)[stage]
+    if not all(n in table for n in names):
+        return None
+    return sum(table[n] for n in names)
+
+
 def cpu_baseline(w, g, budget_s: float) -> dict:
     """Time the oracle (as it stands) on one step of the same workload, single-threaded."""
     import oracle
@@ -69,6 +111,9 @@ def main():
     ap.add_argument("--workload", default="laplace53-d25.6M-P8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=None, help="steps of the per-stage timing pass")
+    ap.add_argument("--calibration-copy", action="store_true",
+                    help="before warm-up, run one plain device copy of the gradient buffer (P*d*4 bytes read and "
+                         "written) to calibrate rocprofv3 FETCH_SIZE / WRITE_SIZE counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the P workers are simulated on one device); --gpus {args.gpus} "
@@ -95,6 +140,12 @@ def main():
     vals = torch.empty(w.k, dtype=torch.float32, device=dev)
     ctx = gs.GsContext(w.d, w.P, w.r, w.c, w.k, hp, rho=w.rho)
     torch.cuda.synchronize()
+    if args.calibration_copy:
+        scratch = torch.empty_like(g_dev[0])
+        scratch.copy_(g_dev[0])
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy: {g_dev[0].numel() * 4} bytes read and written")
+        del scratch
 
     log(f"[bench] warmup {args.warmup}")
     for s in range(args.warmup):
@@ -129,7 +180,7 @@ def main():
         sb["accumulate"] += sb.pop("sketch") - 4 * w.P * w.d
         stage_ms.pop("sketch")
     dom = max(stage_ms, key=lambda s_: stage_ms[s_])
-    achieved = sb[dom] / (stage_ms[dom] * 1e-3) / 1e9
+    achieved = sb[dom] / (stage_ms[dom] * 1e-3) / 1e9 if stage_ms[dom] > 0 else 0.0
     ctx.close()
 
     B = 20 * w.P * w.d + 8 * w.P * w.r * w.c + 8 * w.r * w.c + 12 * w.P * w.k + 8 * w.k
@@ -155,8 +206,9 @@ def main():
         "hbm_frac": B / t / 1e9 / HBM_PEAK_GBS,
         "wall_s_timed": wall,
         "stage_ms": stage_ms,
-        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+        "roofline": {"bound": "hbm", "kernel": " + ".join(stage_kernels(w)[dom]), "stage": dom,
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(w, dom), "traffic_unit": "bytes per launch",
                      "bytes_per_launch": sb[dom], "mean_ms": stage_ms[dom]},
         "cpu_baseline": None,
     }

@@ -344,7 +344,8 @@ __global__ void __launch_bounds__(kBlock) k_merge_partials_any(const double* __r
 template <int P>
 hipError_t launch_acc_vi_p(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v) {
   const int64_t n4 = x->d / 4;
-  hipLaunchKernelGGL(k_accumulate_vi<P>, dim3(grid_for(n4, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, g, u, v,
+  // about one pass per lane: the most loads in flight (measured best on the 25.6M x 8 stream)
+  hipLaunchKernelGGL(k_accumulate_vi<P>, dim3(grid_for(n4, kBlock, 64 * x->num_cus)), dim3(kBlock), 0, s, g, u, v,
                      x->vI, x->d, x->rho);
   return hipGetLastError();
 }
