@@ -6,7 +6,9 @@ d = 25,600,000 (ResNet-50-sized), P = 8 workers, r x c = 5 x 256,000, k = 25,600
 Laplace(0, b_s) with 53 log-uniform layer scales in [1e-5, 1e-2] (synthetic, seeded).
 
 Prints one JSON line with
-  value        gradient coordinates per second, P*d / (time per step)
+  value        gradient coordinates per second, P*d / (mean time per step over the timed steps);
+               the median and minimum step times are reported beside it
+  copy_frac    algorithmic GB/s as a fraction of a plain device copy timed in the same run
   roofline     the dominant stage's algorithmic bytes / its mean duration (HIP events on
                the stream the kernels run on) against MI355X's 8 TB/s HBM peak
   cpu_baseline the plain CPU oracle (single thread) timed on a bounded sample
@@ -98,9 +100,19 @@ def cpu_baseline(w, g, budget_s: float) -> dict:
     t0 = time.perf_counter()
     oracle.step(g, u, v, hp, w.c, w.k, rho=w.rho, want_tables=False, want_est=False)
     dt = time.perf_counter() - t0
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": w.P * w.d / dt, "unit": "coords/s", "cores": 1, "kind": "oracle",
             "sample": f"one full step of {w.name} (P*d = {w.P * w.d} coordinates) from zero state, "
-                      f"{dt:.1f} s single-threaded", "seconds": round(dt, 3)}
+                      f"{dt:.1f} s single-threaded", "seconds": round(dt, 3),
+            "host_nproc": os.cpu_count(), "host_cpu": model}
 
 
 def main():
@@ -154,16 +166,19 @@ def main():
 
     log(f"[bench] timing {args.steps} steps")
     stream = torch.cuda.current_stream()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    e0.record(stream)
+    ev[0].record(stream)
     for s in range(args.steps):
         ctx.step(g_dev[s % nb], u, v, w.k, merged, idx, vals)
-    e1.record(stream)
+        ev[s + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
-    ms = e0.elapsed_time(e1) / args.steps
+    ms = ev[0].elapsed_time(ev[-1]) / args.steps
+    per_step = sorted(ev[s].elapsed_time(ev[s + 1]) for s in range(args.steps))
+    ms_median = per_step[len(per_step) // 2] if len(per_step) % 2 else \
+        0.5 * (per_step[len(per_step) // 2 - 1] + per_step[len(per_step) // 2])
 
     # per-stage timing pass: the same kernels, events between stages on the same stream
     nprof = args.profile_steps if args.profile_steps is not None else args.steps
@@ -183,6 +198,21 @@ def main():
     achieved = sb[dom] / (stage_ms[dom] * 1e-3) / 1e9 if stage_ms[dom] > 0 else 0.0
     ctx.close()
 
+    # device copy bandwidth in the same run (read + write of one P*d fp32 buffer)
+    src = g_dev[0]
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ncopy = 10
+    torch.cuda.synchronize()
+    c0.record(stream)
+    for _ in range(ncopy):
+        dst.copy_(src)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * src.numel() * 4 / (c0.elapsed_time(c1) / ncopy * 1e-3) / 1e9
+    del dst
+
     B = 20 * w.P * w.d + 8 * w.P * w.r * w.c + 8 * w.r * w.c + 12 * w.P * w.k + 8 * w.k
     t = ms * 1e-3
     out = {
@@ -193,6 +223,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms,
+        "ms_per_step_median": ms_median,
+        "ms_per_step_min": per_step[0],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -204,6 +236,8 @@ def main():
         "algorithmic_bytes_per_step": B,
         "achieved_gbs": B / t / 1e9,
         "hbm_frac": B / t / 1e9 / HBM_PEAK_GBS,
+        "copy_gbs": copy_gbs,
+        "copy_frac": B / t / 1e9 / copy_gbs,
         "wall_s_timed": wall,
         "stage_ms": stage_ms,
         "roofline": {"bound": "hbm", "kernel": " + ".join(stage_kernels(w)[dom]), "stage": dom,
