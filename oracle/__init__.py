@@ -57,6 +57,8 @@ def _load():
         "ora_gather_reset": (ctypes.c_int, [i32, i64, i64, vp, i32, vp, vp, vp]),
         "ora_l2sq_estimate": (f64, [i32, i64, vp]),
         "ora_heavy_count": (i64, [i64, i64, vp, f64]),
+        "ora_row_sq_sum": (f64, [i64, vp]),
+        "ora_heavymix": (ctypes.c_int, [i64, i32, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
         "ora_step": (ctypes.c_int, [i32, i64, i32, i64, i64, f32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                     vp, vp, vp]),
     }
@@ -211,6 +213,32 @@ def l2sq_estimate(merged: np.ndarray) -> float:
 def heavy_count(est: np.ndarray, k: int, l2sq: float) -> int:
     est = _f32(est)
     return int(_load().ora_heavy_count(est.size, k, _p(est), l2sq))
+
+
+def row_sq_sum(row) -> float:
+    """Sum of squares of one sketch row in the pairwise-tree order (fp64)."""
+    row = _f32(row)
+    return float(_load().ora_row_sq_sum(row.size, _p(row)))
+
+
+def heavymix(merged: np.ndarray, hp: dict, d: int, k: int, rnd: np.ndarray) -> dict:
+    """HEAVYMIX as printed (Alg. 2): heavy set by est^2 >= l2sq/k plus a fill of the
+    non-heavy coordinates with the largest draws rnd[i] >> 1 (ties to the lower index).
+
+    Returns {"idx": ascending int32[k], "n_heavy": |H|, "l2sq": the l2-norm-squared
+    estimate, "est": the estimates}."""
+    merged = _f32(merged)
+    a, b, a2, b2 = _hp(hp)
+    r, c = merged.shape
+    rnd = np.ascontiguousarray(rnd, dtype=np.uint32)
+    assert rnd.size == d
+    est = np.empty(d, dtype=np.float32)
+    idx = np.empty(k, dtype=np.int32)
+    nh = ctypes.c_int64(0)
+    l2 = ctypes.c_double(0.0)
+    _check(_load().ora_heavymix(d, r, c, k, _p(a), _p(b), _p(a2), _p(b2), _p(merged), _p(rnd), _p(est), _p(idx),
+                                ctypes.addressof(nh), ctypes.addressof(l2)), "heavymix")
+    return {"idx": idx, "n_heavy": int(nh.value), "l2sq": float(l2.value), "est": est}
 
 
 def step(g, u, v, hp: dict, c: int, k: int, rho: float = 0.9, reset_momentum: bool = True,

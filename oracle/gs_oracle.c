@@ -28,6 +28,8 @@
  *   merge, gather binomial-tree order (above), fp32 additions
  *   estimate      median over rows of s_j(i) * S[j][h_j(i)]; even r: fl(fl(m1+m2)*0.5f)
  *   Top_k         the k largest |estimate|, ties to the lower index, returned ascending
+ *   HEAVYMIX      as printed, with a fixed pairwise order for the row sums of squares and
+ *                 the random fill taken from caller-supplied draws (see ora_heavymix)
  *   reset         v (and u when reset_momentum) zeroed at Top_k on every worker
  *
  * Build: gcc -O2 -ffp-contract=off -std=c11 (no -ffast-math). On x86-64 float arithmetic
@@ -302,19 +304,51 @@ int ora_gather_reset(int32_t P, int64_t d, int64_t k, const int32_t* idx, int32_
 }
 
 /* ---------------------------------------------------------------------------------- */
-/* HEAVYMIX diagnostics (Alg. 2, heavy test): the l2-norm-squared estimate taken as the
- * median over rows of the sum of squared cells, and the size of the heavy set
- * H = { i : est_i^2 >= l2sq / k }. Reported only; the selection above does not use them. */
+/* HEAVYMIX as printed (Alg. 2): query every estimate, split the coordinates by the heavy
+ * test into H and NH, and take Top_k = H plus a random l-subset of NH, l = k - |H|.
+ *
+ * The l2-norm-squared estimate: for each row j the sum over columns of S[j][col]^2, the
+ * median of these r row sums (even r: fl(fl(m1 + m2) * 0.5)), all in fp64. A square of an
+ * fp32 value is exact in fp64; the row sum is taken in a fixed order, a pairwise tree: the
+ * c squares, padded with zeros to the next power of two, are added in adjacent pairs, level
+ * by level, until one value remains. The fixed order makes the heavy decision below a
+ * function of S alone.
+ *
+ * Heavy test: theta = fl(l2sq / k); i is heavy when est_i^2 >= theta (est_i^2 exact in
+ * fp64). The paper's test compares the queried square of the estimate with l2sq / k.
+ *
+ * Random fill: rnd[i] is the caller's random draw for coordinate i (one uniform 32-bit
+ * word each). The fill takes the l non-heavy coordinates with the largest rnd[i] >> 1,
+ * ties to the lower index: with independent uniform draws this is a uniformly random
+ * l-subset of NH (ties, which need equal 31-bit draws, aside).
+ *
+ * When |H| >= k (l would be zero or negative) Top_k is the k members of H with the
+ * largest |est_i|, ties to the lower index; every member of H outranks every member of
+ * NH, so this is the deterministic top-k. Top_k is returned in ascending order. */
+
+/* In-place pairwise (adjacent pairs) tree sum of n = 2^m values; destroys buf. */
+static double pairwise_sum(double* buf, int64_t n) {
+  for (int64_t w = n; w > 1; w /= 2)
+    for (int64_t m = 0; m < w / 2; ++m) buf[m] = buf[2 * m] + buf[2 * m + 1];
+  return buf[0];
+}
+
+double ora_row_sq_sum(int64_t c, const float* row) {
+  int64_t n = 1;
+  while (n < c) n *= 2;
+  double* buf = (double*)calloc((size_t)n, sizeof(double));
+  if (!buf) return -1.0;
+  for (int64_t t = 0; t < c; ++t) buf[t] = (double)row[t] * (double)row[t];
+  const double s = pairwise_sum(buf, n);
+  free(buf);
+  return s;
+}
 
 double ora_l2sq_estimate(int32_t r, int64_t c, const float* merged) {
   double* rows = (double*)malloc((size_t)r * sizeof(double));
   double res = 0.0;
   if (!rows) return -1.0;
-  for (int32_t j = 0; j < r; ++j) {
-    double s = 0.0;
-    for (int64_t t = 0; t < c; ++t) s += (double)merged[(int64_t)j * c + t] * (double)merged[(int64_t)j * c + t];
-    rows[j] = s;
-  }
+  for (int32_t j = 0; j < r; ++j) rows[j] = ora_row_sq_sum(c, merged + (int64_t)j * c);
   for (int32_t a = 1; a < r; ++a) {
     double x = rows[a];
     int32_t b = a - 1;
@@ -327,12 +361,70 @@ double ora_l2sq_estimate(int32_t r, int64_t c, const float* merged) {
 }
 
 int64_t ora_heavy_count(int64_t d, int64_t k, const float* est, double l2sq) {
+  const double theta = l2sq / (double)k;
   int64_t n = 0;
   for (int64_t i = 0; i < d; ++i) {
     double e = (double)est[i];
-    if (e * e >= l2sq / (double)k) ++n;
+    if (e * e >= theta) ++n;
   }
   return n;
+}
+
+typedef struct { uint32_t key; int64_t idx; } ora_uk;
+
+static int cmp_uk(const void* pa, const void* pb) {
+  const ora_uk* a = (const ora_uk*)pa;
+  const ora_uk* b = (const ora_uk*)pb;
+  if (a->key > b->key) return -1;
+  if (a->key < b->key) return 1;
+  return (a->idx > b->idx) - (a->idx < b->idx);
+}
+
+int ora_heavymix(int64_t d, int32_t r, int64_t c, int64_t k, const uint32_t* ha, const uint32_t* hb,
+                 const uint32_t* sa, const uint32_t* sb, const float* merged, const uint32_t* rnd, float* est,
+                 int32_t* idx_out, int64_t* n_heavy, double* l2sq_out) {
+  if (k < 1 || k > d) return 1;
+  float* es = est ? est : (float*)malloc((size_t)d * sizeof(float));
+  ora_kv* heavy = (ora_kv*)malloc((size_t)d * sizeof(ora_kv));
+  ora_uk* light = (ora_uk*)malloc((size_t)d * sizeof(ora_uk));
+  int rc = (!es || !heavy || !light) ? 1 : 0;
+  int64_t nh = 0, nl = 0;
+  double l2 = 0.0;
+  if (!rc) rc = ora_unsketch(d, r, c, ha, hb, sa, sb, merged, es);
+  if (!rc) {
+    /* step 1: query the estimates (above); step 2: H and NH */
+    l2 = ora_l2sq_estimate(r, c, merged);
+    const double theta = l2 / (double)k;
+    for (int64_t i = 0; i < d; ++i) {
+      const double e = (double)es[i];
+      if (e * e >= theta) {
+        heavy[nh].key = es[i] < 0.0f ? -es[i] : es[i] + 0.0f;
+        heavy[nh].idx = i;
+        ++nh;
+      } else {
+        light[nl].key = rnd[i] >> 1;
+        light[nl].idx = i;
+        ++nl;
+      }
+    }
+    /* step 3: Top_k = H plus rand_l(NH) */
+    int64_t t = 0;
+    if (nh >= k) {
+      qsort(heavy, (size_t)nh, sizeof(ora_kv), cmp_kv);
+      for (; t < k; ++t) idx_out[t] = (int32_t)heavy[t].idx;
+    } else {
+      for (int64_t m = 0; m < nh; ++m) idx_out[t++] = (int32_t)heavy[m].idx;
+      qsort(light, (size_t)nl, sizeof(ora_uk), cmp_uk);
+      for (int64_t m = 0; t < k; ++m) idx_out[t++] = (int32_t)light[m].idx;
+    }
+    qsort(idx_out, (size_t)k, sizeof(int32_t), cmp_i32);
+  }
+  if (n_heavy) *n_heavy = nh;
+  if (l2sq_out) *l2sq_out = l2;
+  if (!est) free(es);
+  free(heavy);
+  free(light);
+  return rc;
 }
 
 /* ---------------------------------------------------------------------------------- */

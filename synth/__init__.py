@@ -7,7 +7,8 @@ method's arithmetic. It provides
   number of consecutive steps) with their input recipes, and
 * ``hash_params`` -- the seeded (a, b) pairs of the bucket and sign hash families
   (``1 <= a < p``, ``0 <= b < p`` with ``p = 2**31 - 1``), and
-* ``gradients`` -- the P workers' fp32 gradients of one step, as a [P][d] array.
+* ``gradients`` -- the P workers' fp32 gradients of one step, as a [P][d] array, and
+* ``fill_draws`` -- the uniform 32-bit random draws of HEAVYMIX's random fill for one step.
 
 Generation is counter-based (SplitMix64, see ``synth.c``), so any step and worker can be
 produced independently and reproducibly. Distributions stand in for the gradients of the
@@ -34,6 +35,7 @@ TAG_HASH = ord("H")
 TAG_SCALE = ord("S")
 TAG_INDEX = ord("X")
 TAG_ROWS = ord("R")
+TAG_FILL = ord("F")
 
 KIND_T3, KIND_LAPLACE, KIND_NORMAL = 0, 1, 2
 
@@ -172,6 +174,15 @@ def hash_params(w: Workload | int, r: int | None = None) -> dict[str, np.ndarray
         "a2": (np.uint64(1) + ws[:, 2] % (p - np.uint64(1))).astype(np.uint32),
         "b2": (ws[:, 3] % p).astype(np.uint32),
     }
+
+
+def fill_draws(w: Workload | int, step: int, d: int | None = None) -> np.ndarray:
+    """The random draws of HEAVYMIX's fill for one step: one uniform 32-bit word per
+    coordinate (the high half of word i of the 'F' stream of that step). Accepts a
+    Workload, or a bare seed plus d."""
+    seed = w.seed if isinstance(w, Workload) else int(w)
+    n = w.d if isinstance(w, Workload) else int(d)
+    return (words(key(seed, TAG_FILL, step), 0, n) >> np.uint64(32)).astype(np.uint32)
 
 
 def _log_uniform_scales(seed: int, nseg: int, lo_exp: float, hi_exp: float) -> np.ndarray:

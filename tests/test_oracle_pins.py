@@ -447,7 +447,29 @@ def test_planted_workload_selects_every_planted_coordinate():
     assert np.all(np.abs(res["values"][pos] - 0.4 * psgn) < 0.05)
 
 
-def test_heavymix_diagnostics():
+# ---------------------------------------------------------------------------------------
+# HEAVYMIX as printed (Alg. 2): l2sq estimate, heavy set H, random fill from NH
+
+def test_l2sq_row_order_worked_by_hand(golden_dir):
+    for name, expected, *vals in _read_golden(os.path.join(golden_dir, "l2sq_row_order.txt")):
+        row = np.array([float(x) for x in vals], dtype=np.float32)
+        assert oracle.row_sq_sum(row) == float(int(expected)), name
+        # r = 1: the l2sq estimate is the row's sum
+        assert oracle.l2sq_estimate(row[None, :]) == float(int(expected)), name
+
+
+def test_l2sq_integer_tables_exact_median_of_row_sums():
+    # integer cells: every partial sum is an integer below 2^53, so any order is exact and
+    # the estimate is the median of the exact row sums (mean of the middle two for even r)
+    rng = np.random.default_rng(31)
+    for r in (1, 4, 5, 7):
+        m = rng.integers(-3000, 3001, size=(r, 1234)).astype(np.float32)
+        rows = sorted(int(np.sum(m[j].astype(np.int64) ** 2)) for j in range(r))
+        want = float(rows[r // 2]) if r % 2 else (rows[r // 2 - 1] + rows[r // 2]) / 2
+        assert oracle.l2sq_estimate(m) == want
+
+
+def test_l2sq_estimates_the_norm():
     rng = np.random.default_rng(22)
     d, c, r = 20_000, 2000, 5
     hp = _hp(rng, r)
@@ -459,3 +481,120 @@ def test_heavymix_diagnostics():
     est = oracle.unsketch(merged, hp, d)
     k = 100
     assert oracle.heavy_count(est, k, l2) == int(np.sum(est.astype(np.float64) ** 2 >= l2 / k))
+
+
+def _hand_example():
+    """d = 16, r = 3, a collision-free sketch of x = {3: 1, 9: -1, 12: 0.625}, so every
+    estimate equals x exactly (Sec. III-A) and each row's sum of squares is
+    1 + 1 + 0.390625 = 2.390625 exactly."""
+    d, c, r = 16, 4096, 3
+    rng = np.random.default_rng(7)
+    for _ in range(100):
+        hp = _hp(rng, r)
+        if all(len(set(oracle.buckets(int(hp["a"][j]), int(hp["b"][j]), c, range(d)))) == d for j in range(r)):
+            break
+    else:
+        raise AssertionError("no collision-free hash found")
+    x = np.zeros((1, d), np.float32)
+    x[0, 3], x[0, 9], x[0, 12] = 1.0, -1.0, 0.625
+    merged = oracle.sketch(x, hp, c)[0]
+    rnd = np.arange(d, dtype=np.uint32)  # small draws ...
+    rnd[[3, 7, 9, 11]] = 0xFFFFFFFF        # ... except these (>> 1: all 0x7FFFFFFF)
+    rnd[5] = 0xFFFFFFFE                    # (>> 1: also 0x7FFFFFFF, a tie)
+    rnd[12] = 0x80000000
+    return hp, merged, rnd, d
+
+
+def test_heavymix_worked_example():
+    hp, merged, rnd, d = _hand_example()
+    # k = 4: theta = 2.390625 / 4 = 0.59765625. H = {3, 9} (1 >= theta; 0.625^2 = 0.390625 is
+    # not, although 0.625 >= theta, so the test is on the square). l = 2 from NH: the largest
+    # draws >> 1 are 0x7FFFFFFF at 5, 7 and 11; ties go to the lower index: 5 and 7.
+    res = oracle.heavymix(merged, hp, d, 4, rnd)
+    assert res["l2sq"] == 2.390625
+    assert res["n_heavy"] == 2
+    assert res["idx"].tolist() == [3, 5, 7, 9]
+    # k = 2: theta = 1.1953125 > 1, so H is empty and the fill takes all 2 from NH = every
+    # coordinate: the largest draws are at 3, 5, 7, 9, 11; the two lowest indices win.
+    res = oracle.heavymix(merged, hp, d, 2, rnd)
+    assert res["n_heavy"] == 0 and res["idx"].tolist() == [3, 5]
+    # k = 16 = d: every coordinate is selected
+    res = oracle.heavymix(merged, hp, d, 16, rnd)
+    assert res["idx"].tolist() == list(range(16))
+
+
+def test_heavymix_k_equal_spikes_are_exactly_heavy():
+    # k equal spikes of a collision-free vector: l2sq = k s^2, theta = s^2, every spike is
+    # heavy (s^2 >= s^2) and nothing else is, so |H| = k and the fill is empty.
+    rng = np.random.default_rng(41)
+    d, c, r, k = 3000, 6000, 5, 40
+    hp = _hp(rng, r)
+    K = _collision_free_support(hp, c, d, k, rng)
+    x = np.zeros((1, d), np.float32)
+    x[0, K] = np.where(rng.random(k) < 0.5, -0.75, 0.75).astype(np.float32)
+    merged = oracle.sketch(x, hp, c)[0]
+    assert np.array_equal(oracle.unsketch(merged, hp, d), x[0])  # every estimate exact
+    rnd = synth.fill_draws(5, 0, d)
+    res = oracle.heavymix(merged, hp, d, k, rnd)
+    assert res["n_heavy"] == k
+    assert res["idx"].tolist() == sorted(K.tolist())
+
+
+def test_heavymix_all_zero_sketch_selects_lowest_indices():
+    # l2sq = 0, theta = 0, every est^2 = 0 >= 0: all coordinates heavy; Top_k = the k largest
+    # |est| with ties to the lower index = {0 .. k-1}.
+    rng = np.random.default_rng(3)
+    d, c, r, k = 500, 64, 5, 37
+    hp = _hp(rng, r)
+    res = oracle.heavymix(np.zeros((r, c), np.float32), hp, d, k, synth.fill_draws(9, 0, d))
+    assert res["n_heavy"] == d and res["l2sq"] == 0.0
+    assert res["idx"].tolist() == list(range(k))
+
+
+def test_heavymix_with_large_heavy_set_is_topk_by_magnitude():
+    # whenever |H| >= k the selection is the k largest |est| (every member of H outranks
+    # NH). A narrow sketch (c < k) makes theta = l2sq / k small enough for |H| > k.
+    rng = np.random.default_rng(44)
+    d, c, r = 4000, 50, 5
+    hp = _hp(rng, r)
+    merged = rng.standard_normal((r, c)).astype(np.float32)
+    est = oracle.unsketch(merged, hp, d)
+    l2 = oracle.l2sq_estimate(merged)
+    seen = set()
+    for k in range(20, 4001, 45):
+        nh = oracle.heavy_count(est, k, l2)
+        res = oracle.heavymix(merged, hp, d, k, synth.fill_draws(11, k, d))
+        assert res["n_heavy"] == nh
+        seen.add(nh >= k)
+        if nh >= k:
+            assert np.array_equal(res["idx"], oracle.topk(est, k)[0]), k
+    assert seen == {True, False}
+
+
+def test_heavymix_fill_is_uniform_over_the_non_heavy_set():
+    # H is always taken whole; each member of NH is picked with probability l / |NH|
+    rng = np.random.default_rng(51)
+    d, c, r, k = 400, 2000, 5, 60
+    hp = _hp(rng, r)
+    x = (rng.standard_normal((1, d)) * np.where(np.arange(d) % 37 == 0, 30.0, 1.0)).astype(np.float32)
+    merged = oracle.sketch(x, hp, c)[0]
+    base = oracle.heavymix(merged, hp, d, k, synth.fill_draws(0, 0, d))
+    nh = base["n_heavy"]
+    assert 0 < nh < k
+    est = base["est"]
+    heavy = set(np.flatnonzero(est.astype(np.float64) ** 2 >= base["l2sq"] / k).tolist())
+    assert len(heavy) == nh
+    trials = 600
+    counts = np.zeros(d)
+    for t in range(trials):
+        res = oracle.heavymix(merged, hp, d, k, synth.fill_draws(1000 + t, 0, d))
+        idx = res["idx"]
+        assert idx.size == k and np.all(np.diff(idx) > 0)
+        assert heavy <= set(idx.tolist())
+        counts[idx] += 1
+    light = np.array(sorted(set(range(d)) - heavy))
+    p = (k - nh) / light.size
+    expect = trials * p
+    chi2 = float(np.sum((counts[light] - expect) ** 2 / (expect * (1 - p))))
+    dof = light.size - 1
+    assert abs(chi2 - dof) < 6 * np.sqrt(2 * dof), (chi2, dof)
