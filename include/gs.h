@@ -122,6 +122,31 @@ gs_status gs_gather_reset(gs_ctx* ctx, void* stream, const int32_t* idx, int64_t
 gs_status gs_step(gs_ctx* ctx, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
                   int32_t* idx, float* values);
 
+/* HEAVYMIX as printed (Alg. 2): query every estimate, split the coordinates into the heavy
+ * set H = { i : est_i^2 >= l2sq / k } and the rest NH, and select H plus a random fill of
+ * l = k - |H| coordinates of NH.
+ *   est_i   as in gs_unsketch_topk.
+ *   l2sq    the l2-norm-squared estimate: the median over rows of sum_col merged[j][col]^2,
+ *           in double precision, each row summed in a fixed order -- the squares (exact),
+ *           padded with zeros to the next power of two, added in adjacent pairs level by
+ *           level; for even r the mean of the two middle row sums, fl(fl(m1 + m2) * 0.5).
+ *   heavy   est_i^2 >= fl(l2sq / k), with est_i^2 exact in double precision.
+ *   fill    the l coordinates of NH with the largest rnd[i] >> 1, ties to the lower index
+ *           (a uniformly random l-subset of NH when the draws are independent and uniform).
+ *   |H|>=k  the k members of H with the largest |est_i|, ties to the lower index.
+ * merged: [r][c] input. rnd: [d] input, the caller's uniform 32-bit draws for this call (the
+ * method's random numbers; pass fresh draws for every step). est: [d] output or NULL.
+ * idx: [k] output, ascending. n_heavy: one int64 output (|H|) or NULL. l2sq: one double
+ * output or NULL. All pointers are device pointers. 1 <= k <= k_max. */
+gs_status gs_heavymix_topk(gs_ctx* ctx, void* stream, const float* merged, int64_t k, const uint32_t* rnd,
+                           float* est, int32_t* idx, int64_t* n_heavy, double* l2sq);
+
+/* One whole step with HEAVYMIX as printed in place of the deterministic top-k: accumulate,
+ * sketch, merge, gs_heavymix_topk, exact values + reset. Arguments as in gs_step plus rnd
+ * ([d] device input, this step's draws) and n_heavy (one int64 device output or NULL). */
+gs_status gs_step_heavymix(gs_ctx* ctx, void* stream, const float* g, float* u, float* v, int64_t k,
+                           const uint32_t* rnd, float* merged, int32_t* idx, float* values, int64_t* n_heavy);
+
 /* Stage timing for benchmarks and profiling. Runs exactly the kernels of gs_step, records a
  * HIP event on `stream` before the first stage and after each stage, synchronizes the stream
  * and writes the stage durations in milliseconds to the HOST array stage_ms[GS_NUM_STAGES]:

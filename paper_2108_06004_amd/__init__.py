@@ -23,7 +23,8 @@ GS_OK, GS_ERR_INVALID_ARG, GS_ERR_OUT_OF_MEMORY, GS_ERR_DEVICE, GS_ERR_UNSUPPORT
 GS_MAX_WORKERS = 64
 GS_MAX_ROWS = 16
 EXPORTED = ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
-            "gs_gather_reset", "gs_step", "gs_step_profiled", "gs_status_string", "gs_last_error")
+            "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_profiled",
+            "gs_status_string", "gs_last_error")
 GS_NUM_STAGES = 5
 STAGES = ("accumulate", "sketch", "merge", "select", "gather_reset")
 
@@ -75,8 +76,10 @@ def load_library():
     lib.gs_gather_reset.argtypes = [vp, vp, vp, i64, vp, vp, vp]
     lib.gs_step.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp]
     lib.gs_step_profiled.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp, vp]
+    lib.gs_heavymix_topk.argtypes = [vp, vp, vp, i64, vp, vp, vp, vp, vp]
+    lib.gs_step_heavymix.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp]
     for name in ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
-                 "gs_gather_reset", "gs_step", "gs_step_profiled"):
+                 "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_profiled"):
         getattr(lib, name).restype = st
     lib.gs_status_string.argtypes = [st]
     lib.gs_status_string.restype = ctypes.c_char_p
@@ -169,6 +172,20 @@ def gs_step(ctx: int, g, u, v, k: int, merged, idx, values, stream=None) -> None
            ctx, "gs_step")
 
 
+def gs_heavymix_topk(ctx: int, merged, k: int, rnd, est, idx, n_heavy, l2sq, stream=None) -> None:
+    _check(load_library().gs_heavymix_topk(ctx, _stream(stream), _ptr(merged, name="merged"), k,
+                                           _ptr(rnd, name="rnd"), _ptr(est, name="est"), _ptr(idx, name="idx"),
+                                           _ptr(n_heavy, name="n_heavy"), _ptr(l2sq, name="l2sq")),
+           ctx, "gs_heavymix_topk")
+
+
+def gs_step_heavymix(ctx: int, g, u, v, k: int, rnd, merged, idx, values, n_heavy, stream=None) -> None:
+    _check(load_library().gs_step_heavymix(ctx, _stream(stream), _ptr(g, name="g"), _ptr(u, name="u"),
+                                           _ptr(v, name="v"), k, _ptr(rnd, name="rnd"), _ptr(merged, name="merged"),
+                                           _ptr(idx, name="idx"), _ptr(values, name="values"),
+                                           _ptr(n_heavy, name="n_heavy")), ctx, "gs_step_heavymix")
+
+
 def gs_step_profiled(ctx: int, g, u, v, k: int, merged, idx, values, stream=None) -> dict:
     """gs_step with per-stage HIP-event timing (blocks until done); returns stage -> ms."""
     ms = (ctypes.c_float * GS_NUM_STAGES)()
@@ -239,6 +256,39 @@ class GsContext:
         _ptr(idx, torch.int32, k, "idx")
         gs_step(self.handle, self._f32(g, n, "g"), self._f32(u, n, "u"), self._f32(v, n, "v"), k,
                 self._f32(merged, self.r * self.c, "merged"), idx, self._f32(values, k, "values"), stream)
+
+    def heavymix_topk(self, merged, k, rnd, idx, est=None, n_heavy=None, l2sq=None, stream=None):
+        """HEAVYMIX as printed. rnd: uint32 [d] draws (torch has no uint32 arithmetic, so an
+        int32 tensor holding the same bits is accepted too). n_heavy: int64 [1], l2sq:
+        float64 [1] (optional outputs)."""
+        import torch
+
+        _ptr(idx, torch.int32, k, "idx")
+        if rnd.dtype not in (torch.int32, torch.uint32):
+            raise TypeError("rnd must hold 32-bit draws (int32 or uint32)")
+        _ptr(rnd, None, self.d, "rnd")
+        if est is not None:
+            self._f32(est, self.d, "est")
+        if n_heavy is not None:
+            _ptr(n_heavy, torch.int64, 1, "n_heavy")
+        if l2sq is not None:
+            _ptr(l2sq, torch.float64, 1, "l2sq")
+        gs_heavymix_topk(self.handle, self._f32(merged, self.r * self.c, "merged"), k, rnd, est, idx, n_heavy, l2sq,
+                         stream)
+
+    def step_heavymix(self, g, u, v, k, rnd, merged, idx, values, n_heavy=None, stream=None):
+        import torch
+
+        n = self.P * self.d
+        _ptr(idx, torch.int32, k, "idx")
+        if rnd.dtype not in (torch.int32, torch.uint32):
+            raise TypeError("rnd must hold 32-bit draws (int32 or uint32)")
+        _ptr(rnd, None, self.d, "rnd")
+        if n_heavy is not None:
+            _ptr(n_heavy, torch.int64, 1, "n_heavy")
+        gs_step_heavymix(self.handle, self._f32(g, n, "g"), self._f32(u, n, "u"), self._f32(v, n, "v"), k, rnd,
+                         self._f32(merged, self.r * self.c, "merged"), idx, self._f32(values, k, "values"), n_heavy,
+                         stream)
 
     def step_profiled(self, g, u, v, k, merged, idx, values, stream=None) -> dict:
         import torch

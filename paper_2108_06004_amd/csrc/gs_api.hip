@@ -45,7 +45,7 @@ hipError_t alloc(T** p, int64_t count) {
 
 void free_scratch(gs_ctx* x) {
   void* ptrs[] = {x->keys, x->hist, x->ctl, x->cand_key, x->cand_idx, x->bitmap, x->blockcnt, x->acc64,
-                  x->list, x->tile_off, x->vI, x->partial, x->sample_keys, x->heavy};
+                  x->list, x->tile_off, x->vI, x->partial, x->sample_keys, x->heavy, x->l2buf};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   x->keys = nullptr;
@@ -62,6 +62,7 @@ void free_scratch(gs_ctx* x) {
   x->partial = nullptr;
   x->sample_keys = nullptr;
   x->heavy = nullptr;
+  x->l2buf = nullptr;
 }
 
 bool valid_ab(const uint32_t* a, const uint32_t* b, int r) {
@@ -158,6 +159,11 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   chk(alloc(&x->blockcnt, x->emit_blocks));
   chk(alloc(&x->sample_keys, gs::kSampleMax));
   chk(alloc(&x->heavy, ((int64_t)x->r * x->c + 63) / 64 * 2));
+  {
+    const int64_t npad = gs::l2_pad(x->c);
+    x->l2_half = (int64_t)x->r * (npad > 2048 ? npad / 2048 : 1);
+    chk(alloc(&x->l2buf, 2 * x->l2_half));
+  }
   x->plan = gs::make_pull_plan(x->d, x->P, x->r, x->c, x->num_cus);
   x->use_pull = (int64_t)x->plan.T * (int64_t)sizeof(uint32_t) <= gs::kMaxFillLds;
   if (x->use_pull) {
@@ -240,13 +246,8 @@ gs_status gs_gather_reset(gs_ctx* x, void* stream, const int32_t* idx, int64_t k
   return device_status(x, gs::launch_gather_reset(x, as_stream(stream), idx, k, u, v, values), "gs_gather_reset");
 }
 
-gs_status gs_step(gs_ctx* x, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
-                  int32_t* idx, float* values) {
-  if (!x) return GS_ERR_INVALID_ARG;
-  x->last_error.clear();
-  if (!g || !u || !v || !merged || !idx || !values) return fail(x, GS_ERR_INVALID_ARG, "gs_step: NULL array");
-  if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_step: k must satisfy 1 <= k <= k_max");
-  hipStream_t s = as_stream(stream);
+// accumulate + sketch + merge of the fused step (tables kept in context scratch)
+static hipError_t launch_sketch_phase(gs_ctx* x, hipStream_t s, const float* g, float* u, float* v, float* merged) {
   hipError_t e;
   if (x->use_pull) {
     e = gs::launch_accumulate_vi(x, s, g, u, v);
@@ -257,9 +258,44 @@ gs_status gs_step(gs_ctx* x, void* stream, const float* g, float* u, float* v, i
     if (e == hipSuccess) e = gs::launch_sketch_acc(x, s, v);
     if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
   }
+  return e;
+}
+
+gs_status gs_step(gs_ctx* x, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
+                  int32_t* idx, float* values) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!g || !u || !v || !merged || !idx || !values) return fail(x, GS_ERR_INVALID_ARG, "gs_step: NULL array");
+  if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_step: k must satisfy 1 <= k <= k_max");
+  hipStream_t s = as_stream(stream);
+  hipError_t e = launch_sketch_phase(x, s, g, u, v, merged);
   if (e == hipSuccess) e = gs::launch_unsketch_topk(x, s, merged, k, nullptr, idx);
   if (e == hipSuccess) e = gs::launch_gather_reset(x, s, idx, k, u, v, values);
   return device_status(x, e, "gs_step");
+}
+
+gs_status gs_heavymix_topk(gs_ctx* x, void* stream, const float* merged, int64_t k, const uint32_t* rnd, float* est,
+                           int32_t* idx, int64_t* n_heavy, double* l2sq) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!merged || !rnd || !idx) return fail(x, GS_ERR_INVALID_ARG, "gs_heavymix_topk: NULL array");
+  if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_heavymix_topk: k must satisfy 1 <= k <= k_max");
+  return device_status(x, gs::launch_heavymix_topk(x, as_stream(stream), merged, k, rnd, est, idx, n_heavy, l2sq),
+                       "gs_heavymix_topk");
+}
+
+gs_status gs_step_heavymix(gs_ctx* x, void* stream, const float* g, float* u, float* v, int64_t k,
+                           const uint32_t* rnd, float* merged, int32_t* idx, float* values, int64_t* n_heavy) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!g || !u || !v || !rnd || !merged || !idx || !values)
+    return fail(x, GS_ERR_INVALID_ARG, "gs_step_heavymix: NULL array");
+  if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_step_heavymix: k must satisfy 1 <= k <= k_max");
+  hipStream_t s = as_stream(stream);
+  hipError_t e = launch_sketch_phase(x, s, g, u, v, merged);
+  if (e == hipSuccess) e = gs::launch_heavymix_topk(x, s, merged, k, rnd, nullptr, idx, n_heavy, nullptr);
+  if (e == hipSuccess) e = gs::launch_gather_reset(x, s, idx, k, u, v, values);
+  return device_status(x, e, "gs_step_heavymix");
 }
 
 gs_status gs_step_profiled(gs_ctx* x, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,

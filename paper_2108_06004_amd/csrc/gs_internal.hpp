@@ -10,8 +10,8 @@
 
 // Top-k selection works on 32-bit keys (the bits of |estimate|) in three radix digits.
 namespace gs {
-constexpr int kDigit1Shift = 20;  // digit 1: key bits 31..20 (11 bits: the sign bit is 0)
-constexpr int kDigit1Bins = 2048;
+constexpr int kDigit1Shift = 20;  // digit 1: key bits 31..20 (12 bits; |est| keys leave bit 31 clear,
+constexpr int kDigit1Bins = 4096; // HEAVYMIX keys use it to rank the heavy set above the fill)
 constexpr int kDigitBins = 1024;  // digits 2 and 3: key bits 19..10 and 9..0
 
 // Device-resident control block of the selection (one per context).
@@ -26,6 +26,9 @@ struct SelectCtl {
   uint32_t tau0;        // pruning bound: a key no larger than the k-th key (when no fallback)
   uint32_t fallback;    // 1: fewer than k coordinates reach tau0, run the unpruned selection
   uint32_t pad;
+  double l2sq;          // HEAVYMIX: l2-norm-squared estimate (median of the pairwise row sums)
+  double theta;         // HEAVYMIX: heavy threshold l2sq / k
+  unsigned long long n_heavy;  // HEAVYMIX: |H|
 };
 constexpr int kSampleMax = 16384;  // sampled estimates for the pruning bound
 
@@ -76,6 +79,9 @@ struct gs_ctx {
   float* vI = nullptr;            // [d][PP] worker-interleaved accumulators
   double* partial = nullptr;      // [S][r][c][P] fp64 tile sums
   double* acc64 = nullptr;        // [P][r][c] fp64 cell accumulators of the atomic path
+  // HEAVYMIX row sums of squares: two ping-pong buffers of tree-pass results
+  double* l2buf = nullptr;        // [2][l2_half]
+  int64_t l2_half = 0;            // r * max(1, npad / 2048) with npad = next power of two >= c
 
   std::string last_error;
 };
@@ -89,6 +95,9 @@ hipError_t launch_sketch(const gs_ctx* x, hipStream_t s, const float* v, float* 
 hipError_t launch_merge_acc(const gs_ctx* x, hipStream_t s, float* merged);
 hipError_t launch_merge(const gs_ctx* x, hipStream_t s, const float* tables, float* merged);
 hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, float* est, int32_t* idx);
+hipError_t launch_heavymix_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, const uint32_t* rnd,
+                                float* est, int32_t* idx, int64_t* n_heavy, double* l2sq);
+int64_t l2_pad(int64_t c);
 hipError_t launch_gather_reset(const gs_ctx* x, hipStream_t s, const int32_t* idx, int64_t k, float* u, float* v,
                                float* values);
 int64_t emit_blocks_for(int64_t d);

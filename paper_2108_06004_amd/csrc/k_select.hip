@@ -63,14 +63,14 @@ __device__ uint32_t block_scan_incl(uint32_t x, uint32_t* sh, uint32_t& total) {
   return x + add;
 }
 
-// Scan the LDS histogram h[nbins] (nbins = 1024 or 2048) in descending or ascending bin
+// Scan the LDS histogram h[nbins] (nbins = 1024, 2048 or 4096) in descending or ascending bin
 // order and find the first bin at which the running count reaches `need` (1 <= need <=
 // total). res[0] = that bin, res[1] = count in the bins before it (in scan order).
 __device__ void find_bucket(const uint32_t* h, int nbins, bool descending, uint32_t need, uint32_t* shw,
                             uint32_t* res) {
   const int per = nbins / kSelBlock;
-  uint32_t cnt[2] = {0u, 0u};
-  int bin[2] = {0, 0};
+  uint32_t cnt[4] = {0u, 0u, 0u, 0u};
+  int bin[4] = {0, 0, 0, 0};
   uint32_t sum = 0;
   for (int m = 0; m < per; ++m) {
     const int pos = threadIdx.x * per + m;
@@ -616,6 +616,125 @@ __global__ void __launch_bounds__(kSelBlock) k_emit_write(const uint32_t* __rest
   }
 }
 
+// ------------------------------------------------------------------------------------
+// HEAVYMIX as printed (Alg. 2). The l2-norm-squared estimate is the median over rows of
+// sum_col S[j][col]^2 in fp64, each row summed in one fixed order (a pairwise tree over
+// the squares padded with zeros to a power of two, adjacent pairs level by level), so the
+// heavy test est_i^2 >= l2sq / k is a function of S alone. Keys then rank the heavy set
+// above the fill: heavy i gets 0x80000000 | bits(|est_i|), the others their draw
+// rnd[i] >> 1, and the radix selection above takes the k largest, ties to the lower index:
+// all of H (or its k largest |est| when |H| >= k) plus the l = k - |H| non-heavy
+// coordinates with the largest draws.
+
+constexpr int kTreeLeaves = 2048;  // leaves per block of one tree pass (1024 threads)
+
+// One tree pass: block b reduces the aligned group of G leaves (G a power of two, at most
+// kTreeLeaves) of row j = b / (n / G) to one value, adding adjacent pairs level by level.
+// First pass (sq != nullptr): leaf t of row j is sq[j][t]^2 for t < c, else 0 (n = padded
+// width). Later passes: leaf t is in[j * n + t].
+__global__ void __launch_bounds__(kTreeLeaves / 2) k_sq_tree(const float* __restrict__ sq,
+                                                            const double* __restrict__ in, int64_t c, int64_t n,
+                                                            int64_t G, double* __restrict__ out) {
+  __shared__ double t2[kTreeLeaves / 2];
+  const int64_t groups = n / G;
+  const int64_t j = blockIdx.x / groups, base = (blockIdx.x - j * groups) * G;
+  const int tid = threadIdx.x;
+  auto leaf = [&](int64_t t) -> double {
+    if (sq) {
+      if (t >= c) return 0.0;
+      const double x = (double)sq[j * c + t];
+      return x * x;
+    }
+    return in[j * n + t];
+  };
+  if (G == 1) {
+    if (tid == 0) out[blockIdx.x] = leaf(base);
+    return;
+  }
+  int64_t w = G / 2;
+  if (tid < w) t2[tid] = leaf(base + 2 * tid) + leaf(base + 2 * tid + 1);
+  __syncthreads();
+  for (; w > 1; w /= 2) {
+    double a = 0.0;
+    if (tid < w / 2) a = t2[2 * tid] + t2[2 * tid + 1];
+    __syncthreads();
+    if (tid < w / 2) t2[tid] = a;
+    __syncthreads();
+  }
+  if (tid == 0) out[blockIdx.x] = t2[0];
+}
+
+// Median of the r row sums (insertion sort; even r: fl(fl(m1 + m2) * 0.5)), the threshold
+// theta = l2sq / k, and the heavy counter reset. One thread.
+__global__ void k_theta(const double* __restrict__ rows, int r, int64_t k, SelectCtl* __restrict__ ctl) {
+  if (threadIdx.x != 0) return;
+  double v[kMaxRows];
+  for (int j = 0; j < r; ++j) v[j] = rows[j];
+  for (int a = 1; a < r; ++a) {
+    const double x = v[a];
+    int b = a - 1;
+    while (b >= 0 && v[b] > x) {
+      v[b + 1] = v[b];
+      --b;
+    }
+    v[b + 1] = x;
+  }
+  const double med = (r & 1) ? v[r / 2] : 0.5 * (v[r / 2 - 1] + v[r / 2]);
+  ctl->l2sq = med;
+  ctl->theta = med / (double)k;
+  ctl->n_heavy = 0ull;
+}
+
+// Estimate + HEAVYMIX key + digit-1 histogram + |H|.
+template <int R>
+__global__ void __launch_bounds__(kBlock) k_unsketch_hm(HashSet hs, const float* __restrict__ merged, int64_t d,
+                                                        const uint32_t* __restrict__ rnd, float* __restrict__ est,
+                                                        uint32_t* __restrict__ keys, uint32_t* __restrict__ hist,
+                                                        SelectCtl* __restrict__ ctl) {
+  __shared__ uint32_t h[kDigit1Bins];
+  __shared__ uint32_t nh;
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
+  if (threadIdx.x == 0) nh = 0u;
+  RowConst kr[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
+  const double theta = ctl->theta;
+  __syncthreads();
+  uint32_t mine = 0;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < d; i += stride) {
+    float val[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      uint32_t col, sflip;
+      hash_row(kr[j], (uint32_t)i, col, sflip);
+      val[j] = apply_sign(merged[(int64_t)j * hs.c + col], sflip);
+    }
+    sort_net<R>(val);
+    const float e = median_sorted<R>(val);
+    if (est) est[i] = e;
+    const double ed = (double)e;
+    const bool heavy = ed * ed >= theta;
+    const uint32_t key = heavy ? (0x80000000u | abs_key(e)) : (rnd[i] >> 1);
+    mine += heavy ? 1u : 0u;
+    keys[i] = key;
+    atomicAdd(&h[key >> kDigit1Shift], 1u);
+  }
+  if (mine) atomicAdd(&nh, mine);
+  __syncthreads();
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) {
+    const uint32_t n = h[b];
+    if (n) atomicAdd(&hist[b], n);
+  }
+  if (threadIdx.x == 0 && nh) atomicAdd(&ctl->n_heavy, (unsigned long long)nh);
+}
+
+__global__ void k_hm_out(const SelectCtl* __restrict__ ctl, int64_t* __restrict__ n_heavy, double* __restrict__ l2sq) {
+  if (threadIdx.x != 0) return;
+  if (n_heavy) *n_heavy = (int64_t)ctl->n_heavy;
+  if (l2sq) *l2sq = ctl->l2sq;
+}
+
 template <int R>
 void launch_unsketch_r(gs_ctx* x, hipStream_t s, const float* merged, float* est, const SelectCtl* gate) {
   hipLaunchKernelGGL(k_unsketch<R>, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->hs, merged,
@@ -650,6 +769,30 @@ template <int R>
 hipError_t allow_prune_lds(size_t bytes) {
   return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pruned<R>), hipFuncAttributeMaxDynamicSharedMemorySize,
                              (int)bytes);
+}
+
+// select1 -> compact -> select2 -> finalize -> emit over the keys in x->keys (digit-1
+// histogram already in x->hist). gated: act only if the pruned pass raised the fallback.
+hipError_t launch_select_tail(gs_ctx* x, hipStream_t s, int64_t k, int gated, int32_t* idx) {
+  hipLaunchKernelGGL(k_select1, dim3(1), dim3(kSelBlock), 0, s, x->hist, x->ctl, (uint32_t)k, gated);
+  {
+    // contiguous ranges, a multiple of 1024 keys each (so bitmap words never straddle blocks)
+    const int64_t nb = grid_for(x->d, 4 * kBlock, 4 * x->num_cus);
+    int64_t per_block = (x->d + nb - 1) / nb;
+    per_block = (per_block + 4 * kBlock - 1) / (4 * kBlock) * (4 * kBlock);
+    const int64_t grid = (x->d + per_block - 1) / per_block;
+    hipLaunchKernelGGL(k_compact, dim3((unsigned)grid), dim3(kBlock), 0, s, x->keys, x->d, x->ctl, x->cand_key,
+                       x->cand_idx, x->cand_cap, x->bitmap, per_block, gated);
+  }
+  hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap);
+  hipLaunchKernelGGL(k_finalize, dim3(4 * x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl,
+                     x->cand_cap, x->bitmap);
+  const int64_t words = (x->d + 31) / 32;
+  hipLaunchKernelGGL(k_emit_count, dim3((unsigned)x->emit_blocks), dim3(kSelBlock), 0, s, x->bitmap, words,
+                     x->blockcnt);
+  hipLaunchKernelGGL(k_emit_write, dim3((unsigned)x->emit_blocks), dim3(kSelBlock), 0, s, x->bitmap, words,
+                     x->blockcnt, idx, (uint32_t)k);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -702,26 +845,47 @@ hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, i
 #undef GS_R_CASE
     default: return hipErrorInvalidValue;
   }
-  const int gated = prune ? 1 : 0;
-  hipLaunchKernelGGL(k_select1, dim3(1), dim3(kSelBlock), 0, s, x->hist, x->ctl, (uint32_t)k, gated);
-  {
-    // contiguous ranges, a multiple of 1024 keys each (so bitmap words never straddle blocks)
-    const int64_t nb = grid_for(x->d, 4 * kBlock, 4 * x->num_cus);
-    int64_t per_block = (x->d + nb - 1) / nb;
-    per_block = (per_block + 4 * kBlock - 1) / (4 * kBlock) * (4 * kBlock);
-    const int64_t grid = (x->d + per_block - 1) / per_block;
-    hipLaunchKernelGGL(k_compact, dim3((unsigned)grid), dim3(kBlock), 0, s, x->keys, x->d, x->ctl, x->cand_key,
-                       x->cand_idx, x->cand_cap, x->bitmap, per_block, gated);
+  return launch_select_tail(x, s, k, prune ? 1 : 0, idx);
+}
+
+hipError_t launch_heavymix_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, const uint32_t* rnd,
+                                float* est, int32_t* idx, int64_t* n_heavy, double* l2sq) {
+  // row sums of squares, pass by pass (each reduces aligned groups of up to 2048 values)
+  const int64_t npad = l2_pad(x->c);
+  int64_t n = npad;
+  const double* in = nullptr;
+  double* out = x->l2buf;
+  bool first = true;
+  while (first || n > 1) {
+    const int64_t G = n < kTreeLeaves ? n : kTreeLeaves;
+    const int64_t groups = n / G;
+    hipLaunchKernelGGL(k_sq_tree, dim3((unsigned)(x->r * groups)), dim3(kTreeLeaves / 2), 0, s,
+                       first ? merged : nullptr, in, x->c, n, G, out);
+    in = out;
+    out = (out == x->l2buf) ? x->l2buf + x->l2_half : x->l2buf;
+    n = groups;
+    first = false;
   }
-  hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap);
-  hipLaunchKernelGGL(k_finalize, dim3(4 * x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl,
-                     x->cand_cap, x->bitmap);
-  const int64_t words = (x->d + 31) / 32;
-  hipLaunchKernelGGL(k_emit_count, dim3((unsigned)x->emit_blocks), dim3(kSelBlock), 0, s, x->bitmap, words,
-                     x->blockcnt);
-  hipLaunchKernelGGL(k_emit_write, dim3((unsigned)x->emit_blocks), dim3(kSelBlock), 0, s, x->bitmap, words,
-                     x->blockcnt, idx, (uint32_t)k);
-  return hipGetLastError();
+  hipLaunchKernelGGL(k_theta, dim3(1), dim3(64), 0, s, in, x->r, k, x->ctl);
+  switch (x->r) {
+#define GS_R_CASE(RR)                                                                                              \
+  case RR:                                                                                                         \
+    hipLaunchKernelGGL(k_unsketch_hm<RR>, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->hs, \
+                       merged, x->d, rnd, est, x->keys, x->hist, x->ctl);                                          \
+    break;
+    GS_R_CASE(1) GS_R_CASE(2) GS_R_CASE(3) GS_R_CASE(4) GS_R_CASE(5) GS_R_CASE(6) GS_R_CASE(7) GS_R_CASE(8)
+    GS_R_CASE(9) GS_R_CASE(10) GS_R_CASE(11) GS_R_CASE(12) GS_R_CASE(13) GS_R_CASE(14) GS_R_CASE(15) GS_R_CASE(16)
+#undef GS_R_CASE
+    default: return hipErrorInvalidValue;
+  }
+  if (n_heavy || l2sq) hipLaunchKernelGGL(k_hm_out, dim3(1), dim3(64), 0, s, x->ctl, n_heavy, l2sq);
+  return launch_select_tail(x, s, k, 0, idx);
+}
+
+int64_t l2_pad(int64_t c) {
+  int64_t n = 1;
+  while (n < c) n *= 2;
+  return n;
 }
 
 }  // namespace gs
