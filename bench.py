@@ -123,6 +123,9 @@ def main():
     ap.add_argument("--workload", default="laplace53-d25.6M-P8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=None, help="steps of the per-stage timing pass")
+    ap.add_argument("--selection", choices=("topk", "heavymix"), default="topk",
+                    help="topk: deterministic top-k by |estimate| (gs_step); heavymix: HEAVYMIX as printed with a "
+                         "seeded random fill (gs_step_heavymix)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="before warm-up, run one plain device copy of the gradient buffer (P*d*4 bytes read and "
                          "written) to calibrate rocprofv3 FETCH_SIZE / WRITE_SIZE counters")
@@ -151,6 +154,15 @@ def main():
     idx = torch.empty(w.k, dtype=torch.int32, device=dev)
     vals = torch.empty(w.k, dtype=torch.float32, device=dev)
     ctx = gs.GsContext(w.d, w.P, w.r, w.c, w.k, hp, rho=w.rho)
+    if args.selection == "heavymix":
+        # one set of fill draws per gradient batch (fresh draws each step in real use)
+        rnd_dev = [torch.from_numpy(synth.fill_draws(w, t).view(np.int32)).to(dev) for t in range(nb)]
+
+        def run_step(s_):
+            ctx.step_heavymix(g_dev[s_ % nb], u, v, w.k, rnd_dev[s_ % nb], merged, idx, vals)
+    else:
+        def run_step(s_):
+            ctx.step(g_dev[s_ % nb], u, v, w.k, merged, idx, vals)
     torch.cuda.synchronize()
     if args.calibration_copy:
         scratch = torch.empty_like(g_dev[0])
@@ -161,7 +173,7 @@ def main():
 
     log(f"[bench] warmup {args.warmup}")
     for s in range(args.warmup):
-        ctx.step(g_dev[s % nb], u, v, w.k, merged, idx, vals)
+        run_step(s)
     torch.cuda.synchronize()
 
     log(f"[bench] timing {args.steps} steps")
@@ -171,7 +183,7 @@ def main():
     wall0 = time.perf_counter()
     ev[0].record(stream)
     for s in range(args.steps):
-        ctx.step(g_dev[s % nb], u, v, w.k, merged, idx, vals)
+        run_step(s)
         ev[s + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -180,7 +192,8 @@ def main():
     ms_median = per_step[len(per_step) // 2] if len(per_step) % 2 else \
         0.5 * (per_step[len(per_step) // 2 - 1] + per_step[len(per_step) // 2])
 
-    # per-stage timing pass: the same kernels, events between stages on the same stream
+    # per-stage timing pass: the same kernels, events between stages on the same stream (always
+    # the deterministic selection's step: the first three stages are the same kernels either way)
     nprof = args.profile_steps if args.profile_steps is not None else args.steps
     log(f"[bench] per-stage timing over {nprof} steps")
     acc = {st: 0.0 for st in gs.STAGES}
@@ -231,7 +244,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "d": w.d, "P": w.P, "r": w.r, "c": w.c, "k": w.k,
-                   "gradients": w.note},
+                   "selection": args.selection, "gradients": w.note},
         "coords_per_s_per_worker": w.d / t,
         "algorithmic_bytes_per_step": B,
         "achieved_gbs": B / t / 1e9,
@@ -240,6 +253,7 @@ def main():
         "copy_frac": B / t / 1e9 / copy_gbs,
         "wall_s_timed": wall,
         "stage_ms": stage_ms,
+        "stage_ms_from": "gs_step_profiled (deterministic top-k selection)",
         "roofline": {"bound": "hbm", "kernel": " + ".join(stage_kernels(w)[dom]), "stage": dom,
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(w, dom), "traffic_unit": "bytes per launch",

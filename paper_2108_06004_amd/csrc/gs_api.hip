@@ -44,12 +44,13 @@ hipError_t alloc(T** p, int64_t count) {
 }
 
 void free_scratch(gs_ctx* x) {
-  void* ptrs[] = {x->keys, x->hist, x->ctl, x->cand_key, x->cand_idx, x->bitmap, x->blockcnt, x->acc64,
+  void* ptrs[] = {x->keys, x->hist, x->hist2, x->ctl, x->cand_key, x->cand_idx, x->bitmap, x->blockcnt, x->acc64,
                   x->list, x->tile_off, x->vI, x->partial, x->sample_keys, x->heavy, x->l2buf};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   x->keys = nullptr;
   x->hist = nullptr;
+  x->hist2 = nullptr;
   x->ctl = nullptr;
   x->cand_key = nullptr;
   x->cand_idx = nullptr;
@@ -152,6 +153,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   };
   chk(alloc(&x->keys, x->d));
   chk(alloc(&x->hist, gs::kDigit1Bins));
+  chk(alloc(&x->hist2, gs::kDigitBins));
   chk(alloc(&x->ctl, 1));
   chk(alloc(&x->cand_key, x->cand_cap));
   chk(alloc(&x->cand_idx, x->cand_cap));
@@ -175,6 +177,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
     chk(alloc(&x->acc64, (int64_t)x->P * x->r * x->c));
   }
   if (ea == hipSuccess) ea = hipMemset(x->hist, 0, gs::kDigit1Bins * sizeof(uint32_t));
+  if (ea == hipSuccess) ea = hipMemset(x->hist2, 0, gs::kDigitBins * sizeof(uint32_t));
   if (ea == hipSuccess) ea = hipMemset(x->ctl, 0, sizeof(gs::SelectCtl));
   if (ea == hipSuccess) ea = hipDeviceSynchronize();
   if (ea == hipSuccess && x->use_pull) ea = gs::build_pull_lists(x);

@@ -49,6 +49,14 @@ __device__ __forceinline__ uint32_t mod_mersenne_affine(uint32_t a, uint32_t b, 
   return z >= kMersenne ? z - kMersenne : z;
 }
 
+// (x + y) mod p for x, y < p. Along a stride Δ of coordinates the affine hash advances by a
+// constant, (a(i + Δ) + b) mod p = ((a i + b) mod p + (a Δ mod p)) mod p, so a loop over
+// i, i + Δ, i + 2Δ, ... needs one multiply per row to start and one add per step after.
+__device__ __forceinline__ uint32_t add_mod_mersenne(uint32_t x, uint32_t y) {
+  const uint32_t s = x + y;  // < 2^32
+  return s >= kMersenne ? s - kMersenne : s;
+}
+
 // x mod c for x < 2^31: q = floor(x * magic / 2^shift) is floor(x / c) exactly.
 __device__ __forceinline__ uint32_t mod_c(uint32_t x, uint32_t c, uint32_t magic, uint32_t shift) {
   const uint32_t q = (uint32_t)(((uint64_t)x * magic) >> shift);
@@ -61,6 +69,9 @@ __device__ __forceinline__ void hash_row(const RowConst& k, uint32_t i, uint32_t
   col = mod_c(mod_mersenne_affine(k.a, k.b, i), k.c, k.magic, k.shift);
   sflip = ((mod_mersenne_affine(k.a2, k.b2, i) & 1u) ^ 1u) << 31;
 }
+
+// Sign-bit mask of a raw sign-hash value: +1 (mask 0) iff the value is odd.
+__device__ __forceinline__ uint32_t sign_flip_of(uint32_t raw2) { return ((raw2 & 1u) ^ 1u) << 31; }
 
 __device__ __forceinline__ void hash_ij(const HashSet& hs, int j, uint32_t i, uint32_t& col, uint32_t& sflip) {
   hash_row(row_const(hs, j), i, col, sflip);

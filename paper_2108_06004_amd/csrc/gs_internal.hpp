@@ -25,10 +25,12 @@ struct SelectCtl {
   uint32_t status;      // 0 ok; nonzero: candidate overflow (must not happen)
   uint32_t tau0;        // pruning bound: a key no larger than the k-th key (when no fallback)
   uint32_t fallback;    // 1: fewer than k coordinates reach tau0, run the unpruned selection
-  uint32_t pad;
+  uint32_t n_surv;      // coordinates queued by the pruned pass for an exact estimate
   double l2sq;          // HEAVYMIX: l2-norm-squared estimate (median of the pairwise row sums)
   double theta;         // HEAVYMIX: heavy threshold l2sq / k
   unsigned long long n_heavy;  // HEAVYMIX: |H|
+  uint32_t n_stage2;    // keys of the digit-1 bucket b1 compacted for the digit-3 pass
+  uint32_t pad2;
 };
 constexpr int kSampleMax = 16384;  // sampled estimates for the pruning bound
 
@@ -58,6 +60,7 @@ struct gs_ctx {
   // scratch (device)
   uint32_t* keys = nullptr;       // [d]
   uint32_t* hist = nullptr;       // [kDigit1Bins], zero between calls
+  uint32_t* hist2 = nullptr;      // [kDigitBins] digit-2 histogram of bucket b1, zero between calls
   gs::SelectCtl* ctl = nullptr;   // [1]
   uint32_t* cand_key = nullptr;   // [cand_cap]
   int32_t* cand_idx = nullptr;    // [cand_cap]

@@ -110,13 +110,23 @@ __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __
   for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
   __syncthreads();
   const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < d; i += stride) {
+  const int64_t i0 = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  uint32_t hb[R], hsg[R], db[R], dsg[R];  // raw hashes of the current i and their per-stride steps
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    hb[j] = mod_mersenne_affine(kr[j].a, kr[j].b, (uint32_t)i0);
+    hsg[j] = mod_mersenne_affine(kr[j].a2, kr[j].b2, (uint32_t)i0);
+    db[j] = mod_mersenne_affine(kr[j].a, 0u, (uint32_t)stride);
+    dsg[j] = mod_mersenne_affine(kr[j].a2, 0u, (uint32_t)stride);
+  }
+  for (int64_t i = i0; i < d; i += stride) {
     float val[R];
 #pragma unroll
     for (int j = 0; j < R; ++j) {
-      uint32_t col, sflip;
-      hash_row(kr[j], (uint32_t)i, col, sflip);
-      val[j] = apply_sign(merged[(int64_t)j * hs.c + col], sflip);
+      const uint32_t col = mod_c(hb[j], kr[j].c, kr[j].magic, kr[j].shift);
+      val[j] = apply_sign(merged[(int64_t)j * hs.c + col], sign_flip_of(hsg[j]));
+      hb[j] = add_mod_mersenne(hb[j], db[j]);
+      hsg[j] = add_mod_mersenne(hsg[j], dsg[j]);
     }
     sort_net<R>(val);
     const float e = median_sorted<R>(val);
@@ -241,22 +251,82 @@ __global__ void __launch_bounds__(kBlock) k_compact(const uint32_t* __restrict__
 // ------------------------------------------------------------------------------------
 // 4. Digits 2 and 3 of the k-th key, then the index cut among equal keys.
 
+constexpr int kSelUnroll = 8;    // candidate loads in flight per thread
+constexpr int kStageBuf = 4096;  // per-block LDS buffer of k_digit2
+
+// 4a. Digit 2 of the keys in bucket b1 (many blocks): the digit-2 histogram (LDS per block,
+// added into hist2) and the bucket's keys compacted into stage2 for the digit-3 pass (an
+// LDS buffer per block, one global atomic per flush).
+__global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ cand_key,
+                                                   SelectCtl* __restrict__ ctl, int64_t cap,
+                                                   uint32_t* __restrict__ hist2, uint32_t* __restrict__ stage2) {
+  __shared__ uint32_t h[kDigitBins];
+  __shared__ uint32_t buf[kStageBuf];
+  __shared__ uint32_t bn, gbase;
+  const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
+  const uint32_t b1 = ctl->b1;
+  const int lane = threadIdx.x & 63;
+  for (int b = threadIdx.x; b < kDigitBins; b += kBlock) h[b] = 0u;
+  if (threadIdx.x == 0) bn = 0u;
+  __syncthreads();
+  const int64_t per = (n + gridDim.x - 1) / gridDim.x;
+  const int64_t lo = (int64_t)blockIdx.x * per, hi = min(n, lo + per);
+  constexpr int V = 4;
+  for (int64_t c0 = lo; c0 < hi; c0 += (int64_t)V * kBlock) {  // block-uniform
+    uint32_t key[V];
+#pragma unroll
+    for (int m = 0; m < V; ++m) {
+      const int64_t t = c0 + (int64_t)m * kBlock + threadIdx.x;
+      key[m] = t < hi ? cand_key[t] : 0u;
+    }
+#pragma unroll
+    for (int m = 0; m < V; ++m) {
+      const int64_t t = c0 + (int64_t)m * kBlock + threadIdx.x;
+      const bool take = t < hi && (key[m] >> 20) == b1;
+      if (take) atomicAdd(&h[(key[m] >> 10) & 1023u], 1u);
+      const uint64_t bal = __ballot(take);
+      uint32_t wbase = 0u;
+      if (lane == 0 && bal) wbase = atomicAdd(&bn, (uint32_t)__popcll(bal));
+      wbase = __shfl(wbase, 0);
+      if (take) buf[wbase + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull))] = key[m];
+    }
+    __syncthreads();
+    const uint32_t nb = bn;  // < kStageBuf / 2 + V * kBlock <= kStageBuf
+    if (nb >= (uint32_t)(kStageBuf / 2) || (c0 + (int64_t)V * kBlock >= hi && nb > 0)) {
+      if (threadIdx.x == 0) gbase = atomicAdd(&ctl->n_stage2, nb);
+      __syncthreads();
+      const uint32_t g0 = gbase;
+      for (uint32_t t = threadIdx.x; t < nb; t += kBlock) stage2[g0 + t] = buf[t];
+      __syncthreads();
+      if (threadIdx.x == 0) bn = 0u;
+    }
+    __syncthreads();
+  }
+  for (int b = threadIdx.x; b < kDigitBins; b += kBlock) {
+    const uint32_t c = h[b];
+    if (c) atomicAdd(&hist2[b], c);
+  }
+}
+
+// 4b. Digits 2 and 3 of the k-th key, then the index cut among equal keys (one block).
 __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restrict__ cand_key,
                                                        const int32_t* __restrict__ cand_idx,
-                                                       SelectCtl* __restrict__ ctl, int64_t cap) {
+                                                       SelectCtl* __restrict__ ctl, int64_t cap,
+                                                       uint32_t* __restrict__ hist2,
+                                                       const uint32_t* __restrict__ stage2) {
   __shared__ uint32_t h[2048];
   __shared__ uint32_t shw[kSelBlock / 64];
   __shared__ uint32_t res[2];
   const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
+  const int64_t n2 = ctl->n_stage2;
   const uint32_t b1 = ctl->b1;
   const uint32_t need1 = ctl->k - ctl->above1;
 
-  // digit 2 (key bits 19..10) among keys in bucket b1, scanned from the top
-  for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
-  __syncthreads();
-  for (int64_t t = threadIdx.x; t < n; t += kSelBlock) {
-    const uint32_t key = cand_key[t];
-    if ((key >> 20) == b1) atomicAdd(&h[(key >> 10) & 1023u], 1u);
+  // digit 2 (key bits 19..10) among keys in bucket b1, scanned from the top (histogram
+  // from k_digit2, cleared here for the next call)
+  for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) {
+    h[b] = hist2[b];
+    hist2[b] = 0u;
   }
   __syncthreads();
   find_bucket(h, kDigitBins, true, need1, shw, res);
@@ -264,12 +334,21 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
   const uint32_t need2 = need1 - res[1];
   __syncthreads();
 
-  // digit 3 (key bits 9..0) among keys with the 22-bit prefix pre2
+  // digit 3 (key bits 9..0) among the bucket's keys with the 22-bit prefix pre2
   for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
   __syncthreads();
-  for (int64_t t = threadIdx.x; t < n; t += kSelBlock) {
-    const uint32_t key = cand_key[t];
-    if ((key >> 10) == pre2) atomicAdd(&h[key & 1023u], 1u);
+  for (int64_t t0 = 0; t0 < n2; t0 += (int64_t)kSelUnroll * kSelBlock) {
+    uint32_t key[kSelUnroll];
+#pragma unroll
+    for (int m = 0; m < kSelUnroll; ++m) {
+      const int64_t t = t0 + (int64_t)m * kSelBlock + threadIdx.x;
+      key[m] = t < n2 ? stage2[t] : 0u;
+    }
+#pragma unroll
+    for (int m = 0; m < kSelUnroll; ++m) {
+      const int64_t t = t0 + (int64_t)m * kSelBlock + threadIdx.x;
+      if (t < n2 && (key[m] >> 10) == pre2) atomicAdd(&h[key[m] & 1023u], 1u);
+    }
   }
   __syncthreads();
   find_bucket(h, kDigitBins, true, need2, shw, res);
@@ -316,6 +395,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
   if (threadIdx.x == 0) {
     ctl->tau = tau;
     ctl->iota = iota;
+    ctl->n_stage2 = 0u;
     if ((uint64_t)ctl->n_cand > (uint64_t)cap) ctl->status = 1u;
   }
 }
@@ -349,8 +429,7 @@ __global__ void __launch_bounds__(kBlock) k_finalize(const uint32_t* __restrict_
 // either way.
 
 template <int R>
-__device__ __forceinline__ uint32_t estimate_key(const RowConst (&kr)[R], const float* __restrict__ merged,
-                                                 uint32_t i) {
+__device__ __forceinline__ float estimate_val(const RowConst (&kr)[R], const float* __restrict__ merged, uint32_t i) {
   float val[R];
 #pragma unroll
   for (int j = 0; j < R; ++j) {
@@ -359,18 +438,31 @@ __device__ __forceinline__ uint32_t estimate_key(const RowConst (&kr)[R], const 
     val[j] = apply_sign(merged[(int64_t)j * kr[j].c + col], sflip);
   }
   sort_net<R>(val);
-  return abs_key(median_sorted<R>(val));
+  return median_sorted<R>(val);
 }
 
 template <int R>
+__device__ __forceinline__ uint32_t estimate_key(const RowConst (&kr)[R], const float* __restrict__ merged,
+                                                 uint32_t i) {
+  return abs_key(estimate_val<R>(kr, merged, i));
+}
+
+// Sampled keys at M evenly spaced coordinates: |est| keys, or (HEAVYMIX) the fill keys
+// rnd >> 1, whose rho-th largest bounds the fill from below.
+template <int R, bool HM>
 __global__ void __launch_bounds__(kBlock) k_sample(HashSet hs, const float* __restrict__ merged, int64_t d, int M,
-                                                   uint32_t* __restrict__ out) {
-  RowConst kr[R];
-#pragma unroll
-  for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
+                                                   const uint32_t* __restrict__ rnd, uint32_t* __restrict__ out) {
   const int s = blockIdx.x * kBlock + threadIdx.x;
   if (s >= M) return;
-  out[s] = estimate_key<R>(kr, merged, (uint32_t)(((int64_t)s * d) / M));
+  const uint32_t i = (uint32_t)(((int64_t)s * d) / M);
+  if constexpr (HM) {
+    out[s] = rnd[i] >> 1;
+  } else {
+    RowConst kr[R];
+#pragma unroll
+    for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
+    out[s] = estimate_key<R>(kr, merged, i);
+  }
 }
 
 // tau0 = the rho-th largest sampled key (three radix digits in one block).
@@ -406,20 +498,29 @@ __global__ void __launch_bounds__(kSelBlock) k_tau0(const uint32_t* __restrict__
     ctl->tau0 = (pre << 10) | res[0];
     ctl->k = k;
     ctl->n_cand = 0u;
+    ctl->n_surv = 0u;
     ctl->fallback = 0u;
     ctl->status = 0u;
   }
 }
 
-// Heavy-cell bitmap: bit e of the flat [r][c] sketch is |merged[e]| >= tau0 (one ballot
-// per 64 cells).
+// Heavy-cell bitmap: bit e of the flat [r][c] sketch is |merged[e]| >= tau0, or (HEAVYMIX,
+// hm = 1) merged[e]^2 >= theta in fp64 (one ballot per 64 cells). A coordinate with
+// est^2 >= theta has ceil(r/2) cells with |cell| >= |est| (see the pruned pass), and the
+// squares of fp32 values are exact in fp64, so those cells pass the same test.
 __global__ void __launch_bounds__(kBlock) k_heavy(const float* __restrict__ merged, int64_t rc,
-                                                  const SelectCtl* __restrict__ ctl, uint32_t* __restrict__ heavy) {
+                                                  const SelectCtl* __restrict__ ctl, uint32_t* __restrict__ heavy,
+                                                  int hm) {
   const uint32_t tau0 = ctl->tau0;
+  const double theta = ctl->theta;
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   for (int64_t base = ((int64_t)blockIdx.x * kBlock + threadIdx.x) & ~63ll; base < rc; base += stride) {
     const int64_t e = base + (threadIdx.x & 63);
-    const bool hv = e < rc && abs_key(merged[e]) >= tau0;
+    bool hv = false;
+    if (e < rc) {
+      const float x = merged[e];
+      hv = hm ? (double)x * (double)x >= theta : abs_key(x) >= tau0;
+    }
     const uint64_t m = __ballot(hv);
     if ((threadIdx.x & 63) == 0) {
       heavy[(base >> 5)] = (uint32_t)m;
@@ -428,23 +529,28 @@ __global__ void __launch_bounds__(kBlock) k_heavy(const float* __restrict__ merg
   }
 }
 
-// The pruned pass: every coordinate checks its r heavy bits (early exit once ceil(r/2)
-// is out of reach); survivors compute their exact estimate and, if it reaches tau0, are
-// appended to the candidate list through an LDS buffer (one global atomic per flush).
-// The output bitmap words are cleared on the way. dynamic LDS: [map words?][buf keys][buf idx]
+// The pruned pass, in two kernels.
+// k_pruned: every coordinate checks its r heavy bits (bitmap in LDS when it fits); the
+// survivors (ceil(r/2) heavy cells; for HEAVYMIX also every coordinate whose fill key
+// rnd[i] >> 1 reaches tau0) are queued -- through an LDS buffer, one global atomic per
+// flush -- and the output bitmap words are cleared on the way.
+// k_survivors: the queued coordinates, with every lane busy, compute their exact estimate
+// and append the candidates (key >= tau0; for HEAVYMIX heavy ones always, key
+// 0x80000000 | bits(|est|), others by their fill key) and count |H|. Splitting keeps the
+// table reads of the few survivors from stalling whole waves of the first pass.
+// dynamic LDS of k_pruned: [map words?][buf indices]
 constexpr int kPruneBlock = 1024;  // 16 waves per CU; the heavy bitmap fills the LDS
 
-template <int R>
-__global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, const float* __restrict__ merged, int64_t d,
-                                                   SelectCtl* __restrict__ ctl, const uint32_t* __restrict__ heavy,
-                                                   int64_t map_words, int map_in_lds, int buf_cap,
-                                                   uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx,
-                                                   int64_t cap, uint32_t* __restrict__ bitmap) {
+template <int R, bool HM>
+__global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, SelectCtl* __restrict__ ctl,
+                                                   const uint32_t* __restrict__ heavy, int64_t map_words,
+                                                   int map_in_lds, int buf_cap, uint32_t* __restrict__ queue,
+                                                   uint32_t* __restrict__ bitmap, const uint32_t* __restrict__ rnd) {
   constexpr int U = 4;  // coordinates per lane per pass: independent hash chains in flight
   extern __shared__ uint32_t sm[];
   __shared__ uint32_t bn, gbase;
   const uint32_t* map = heavy;
-  uint32_t* bkey = sm;
+  uint32_t* buf = sm;
   if (map_in_lds) {
     // map_words is even and the map 8-byte aligned: copy 16 bytes per lane, 8 loads in flight
     const int64_t n4 = map_words / 4;
@@ -461,9 +567,8 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, const float*
     for (; w < n4; w += kPruneBlock) dst[w] = src[w];
     for (int64_t x = 4 * n4 + threadIdx.x; x < map_words; x += kPruneBlock) sm[x] = heavy[x];
     map = sm;
-    bkey = sm + map_words;
+    buf = sm + map_words;
   }
-  int32_t* bidx = reinterpret_cast<int32_t*>(bkey + buf_cap);
   RowConst kr[R];
 #pragma unroll
   for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
@@ -472,38 +577,35 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, const float*
   if (threadIdx.x == 0) bn = 0;
   __syncthreads();
   const int64_t stride = (int64_t)gridDim.x * kPruneBlock * U;
-  for (int64_t base = (int64_t)blockIdx.x * kPruneBlock * U; base < d; base += stride) {  // block-uniform
-    int cnt[U];
+  const int64_t base0 = (int64_t)blockIdx.x * kPruneBlock * U;
+  uint32_t hb[R][U], db[R];  // raw bucket hashes of this lane's U coordinates, per-stride steps
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    db[j] = mod_mersenne_affine(kr[j].a, 0u, (uint32_t)stride);
+#pragma unroll
+    for (int m = 0; m < U; ++m)
+      hb[j][m] = mod_mersenne_affine(kr[j].a, kr[j].b, (uint32_t)(base0 + threadIdx.x + (int64_t)m * kPruneBlock));
+  }
+  for (int64_t base = base0; base < d; base += stride) {  // block-uniform
 #pragma unroll
     for (int m = 0; m < U; ++m) {
       const int64_t i = base + threadIdx.x + (int64_t)m * kPruneBlock;
-      cnt[m] = 0;
+      int cnt = 0;
 #pragma unroll
       for (int j = 0; j < R; ++j) {
-        const uint32_t col = mod_c(mod_mersenne_affine(kr[j].a, kr[j].b, (uint32_t)i), kr[j].c, kr[j].magic,
-                                   kr[j].shift);
+        const uint32_t col = mod_c(hb[j][m], kr[j].c, kr[j].magic, kr[j].shift);
+        hb[j][m] = add_mod_mersenne(hb[j][m], db[j]);
         const int64_t e = (int64_t)j * kr[j].c + col;
-        cnt[m] += (map[e >> 5] >> (e & 31)) & 1u;
+        cnt += (map[e >> 5] >> (e & 31)) & 1u;
       }
-      if (i >= d) cnt[m] = 0;
-    }
-#pragma unroll
-    for (int m = 0; m < U; ++m) {
-      const int64_t i = base + threadIdx.x + (int64_t)m * kPruneBlock;
-      if (cnt[m] >= need) {
-        const uint32_t key = estimate_key<R>(kr, merged, (uint32_t)i);
-        if (key >= tau0) {
-          const uint32_t pos = atomicAdd(&bn, 1u);
-          if (pos < (uint32_t)buf_cap) {
-            bkey[pos] = key;
-            bidx[pos] = (int32_t)i;
-          } else {  // buffer full within this pass (dense candidates): append directly
-            const uint32_t gpos = atomicAdd(&ctl->n_cand, 1u);
-            if ((int64_t)gpos < cap) {
-              cand_key[gpos] = key;
-              cand_idx[gpos] = (int32_t)i;
-            }
-          }
+      bool keep = i < d && cnt >= need;
+      if constexpr (HM) keep = keep || (i < d && (rnd[i] >> 1) >= tau0);
+      if (keep) {
+        const uint32_t pos = atomicAdd(&bn, 1u);
+        if (pos < (uint32_t)buf_cap) {
+          buf[pos] = (uint32_t)i;
+        } else {  // buffer full within this pass (dense survivors): queue directly
+          queue[atomicAdd(&ctl->n_surv, 1u)] = (uint32_t)i;
         }
       }
       if (i < d && (i & 31) == 0) bitmap[i >> 5] = 0u;
@@ -512,20 +614,90 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, const float*
     const uint32_t n = min(bn, (uint32_t)buf_cap);
     const bool last = base + stride >= d;
     if (n >= (uint32_t)(buf_cap / 2) || (last && n > 0)) {
-      if (threadIdx.x == 0) gbase = atomicAdd(&ctl->n_cand, n);
+      if (threadIdx.x == 0) gbase = atomicAdd(&ctl->n_surv, n);
       __syncthreads();
       const uint32_t g0 = gbase;
-      for (uint32_t t = threadIdx.x; t < n; t += kPruneBlock) {
-        const int64_t pos = (int64_t)g0 + t;
-        if (pos < cap) {
-          cand_key[pos] = bkey[t];
-          cand_idx[pos] = bidx[t];
-        }
-      }
+      for (uint32_t t = threadIdx.x; t < n; t += kPruneBlock) queue[g0 + t] = buf[t];
       __syncthreads();
       if (threadIdx.x == 0) bn = 0;
     }
     __syncthreads();
+  }
+}
+
+constexpr int kSurvBuf = 2048;  // per-block LDS candidate buffer of k_survivors
+
+template <int R, bool HM>
+__global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* __restrict__ merged,
+                                                      SelectCtl* __restrict__ ctl, const uint32_t* __restrict__ queue,
+                                                      uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx,
+                                                      int64_t cap, const uint32_t* __restrict__ rnd) {
+  __shared__ uint32_t bkey[kSurvBuf];
+  __shared__ int32_t bidx[kSurvBuf];
+  __shared__ uint32_t bn, gbase, nheavy;
+  RowConst kr[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
+  const uint32_t tau0 = ctl->tau0;
+  const double theta = HM ? ctl->theta : 0.0;
+  const int64_t n = ctl->n_surv;
+  const int lane = threadIdx.x & 63;
+  if (threadIdx.x == 0) {
+    bn = 0u;
+    nheavy = 0u;
+  }
+  __syncthreads();
+  uint32_t mine = 0;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t0 = (int64_t)blockIdx.x * kBlock; t0 < n; t0 += stride) {  // block-uniform trip count
+    const int64_t t = t0 + threadIdx.x;
+    bool cand = false;
+    uint32_t key = 0u, i = 0u;
+    if (t < n) {
+      i = queue[t];
+      const float e = estimate_val<R>(kr, merged, i);
+      if constexpr (HM) {
+        const bool hv = (double)e * (double)e >= theta;
+        key = hv ? (0x80000000u | abs_key(e)) : (rnd[i] >> 1);
+        cand = hv || key >= tau0;
+        mine += hv ? 1u : 0u;
+      } else {
+        key = abs_key(e);
+        cand = key >= tau0;
+      }
+    }
+    // block-local append (one LDS atomic per wave); at most kBlock per pass, so the buffer,
+    // flushed whenever it is half full, never overflows
+    const uint64_t bal = __ballot(cand);
+    uint32_t wbase = 0u;
+    if (lane == 0 && bal) wbase = atomicAdd(&bn, (uint32_t)__popcll(bal));
+    wbase = __shfl(wbase, 0);
+    if (cand) {
+      const uint32_t pos = wbase + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
+      bkey[pos] = key;
+      bidx[pos] = (int32_t)i;
+    }
+    __syncthreads();
+    const uint32_t nb = bn;
+    if (nb >= (uint32_t)(kSurvBuf / 2) || (t0 + stride >= n && nb > 0)) {
+      if (threadIdx.x == 0) gbase = atomicAdd(&ctl->n_cand, nb);
+      __syncthreads();
+      const int64_t g0 = gbase;
+      for (uint32_t u = threadIdx.x; u < nb; u += kBlock) {
+        if (g0 + u < cap) {
+          cand_key[g0 + u] = bkey[u];
+          cand_idx[g0 + u] = bidx[u];
+        }
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) bn = 0u;
+    }
+    __syncthreads();
+  }
+  if constexpr (HM) {
+    if (mine) atomicAdd(&nheavy, mine);
+    __syncthreads();
+    if (threadIdx.x == 0 && nheavy) atomicAdd(&ctl->n_heavy, (unsigned long long)nheavy);
   }
 }
 
@@ -687,10 +859,13 @@ __global__ void k_theta(const double* __restrict__ rows, int r, int64_t k, Selec
 
 // Estimate + HEAVYMIX key + digit-1 histogram + |H|.
 template <int R>
+// gated: act only when the pruned pass raised the fallback flag; count_heavy: add |H| to
+// ctl->n_heavy (off after a pruned pass, which already counted it).
 __global__ void __launch_bounds__(kBlock) k_unsketch_hm(HashSet hs, const float* __restrict__ merged, int64_t d,
                                                         const uint32_t* __restrict__ rnd, float* __restrict__ est,
                                                         uint32_t* __restrict__ keys, uint32_t* __restrict__ hist,
-                                                        SelectCtl* __restrict__ ctl) {
+                                                        SelectCtl* __restrict__ ctl, int gated, int count_heavy) {
+  if (gated && ctl->fallback == 0u) return;
   __shared__ uint32_t h[kDigit1Bins];
   __shared__ uint32_t nh;
   for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
@@ -702,13 +877,23 @@ __global__ void __launch_bounds__(kBlock) k_unsketch_hm(HashSet hs, const float*
   __syncthreads();
   uint32_t mine = 0;
   const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < d; i += stride) {
+  const int64_t i0 = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+  uint32_t hb[R], hsg[R], db[R], dsg[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    hb[j] = mod_mersenne_affine(kr[j].a, kr[j].b, (uint32_t)i0);
+    hsg[j] = mod_mersenne_affine(kr[j].a2, kr[j].b2, (uint32_t)i0);
+    db[j] = mod_mersenne_affine(kr[j].a, 0u, (uint32_t)stride);
+    dsg[j] = mod_mersenne_affine(kr[j].a2, 0u, (uint32_t)stride);
+  }
+  for (int64_t i = i0; i < d; i += stride) {
     float val[R];
 #pragma unroll
     for (int j = 0; j < R; ++j) {
-      uint32_t col, sflip;
-      hash_row(kr[j], (uint32_t)i, col, sflip);
-      val[j] = apply_sign(merged[(int64_t)j * hs.c + col], sflip);
+      const uint32_t col = mod_c(hb[j], kr[j].c, kr[j].magic, kr[j].shift);
+      val[j] = apply_sign(merged[(int64_t)j * hs.c + col], sign_flip_of(hsg[j]));
+      hb[j] = add_mod_mersenne(hb[j], db[j]);
+      hsg[j] = add_mod_mersenne(hsg[j], dsg[j]);
     }
     sort_net<R>(val);
     const float e = median_sorted<R>(val);
@@ -726,7 +911,7 @@ __global__ void __launch_bounds__(kBlock) k_unsketch_hm(HashSet hs, const float*
     const uint32_t n = h[b];
     if (n) atomicAdd(&hist[b], n);
   }
-  if (threadIdx.x == 0 && nh) atomicAdd(&ctl->n_heavy, (unsigned long long)nh);
+  if (count_heavy && threadIdx.x == 0 && nh) atomicAdd(&ctl->n_heavy, (unsigned long long)nh);
 }
 
 __global__ void k_hm_out(const SelectCtl* __restrict__ ctl, int64_t* __restrict__ n_heavy, double* __restrict__ l2sq) {
@@ -741,25 +926,26 @@ void launch_unsketch_r(gs_ctx* x, hipStream_t s, const float* merged, float* est
                      x->d, est, x->keys, x->hist, gate);
 }
 
-template <int R>
-void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k) {
+template <int R, bool HM>
+void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, const uint32_t* rnd) {
   const int M = (int)(x->d < kSampleMax ? x->d : kSampleMax);
   const double mk = (double)M * (double)k / (double)x->d;
   // expected sampled keys above the k-th key: mk (sd ~ sqrt(mk)); the margin is ~8 sd
   double rho_d = std::ceil(1.2 * mk + 5.0 * std::sqrt(mk) + 8.0);
   if (rho_d > M) rho_d = M;
   if (rho_d < 1) rho_d = 1;
-  hipLaunchKernelGGL(k_sample<R>, dim3((M + kBlock - 1) / kBlock), dim3(kBlock), 0, s, x->hs, merged, x->d, M,
-                     x->sample_keys);
+  hipLaunchKernelGGL((k_sample<R, HM>), dim3((M + kBlock - 1) / kBlock), dim3(kBlock), 0, s, x->hs, merged, x->d, M,
+                     rnd, x->sample_keys);
   hipLaunchKernelGGL(k_tau0, dim3(1), dim3(kSelBlock), 0, s, x->sample_keys, M, (uint32_t)rho_d, x->ctl, (uint32_t)k);
   const int64_t rc = (int64_t)x->r * x->c;
   hipLaunchKernelGGL(k_heavy, dim3(grid_for(rc, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, merged, rc, x->ctl,
-                     x->heavy);
+                     x->heavy, HM ? 1 : 0);
   // with the bitmap in LDS one block fits a CU: launch one per CU so the map is loaded once
   const int pgrid = grid_for(x->d, 4 * kPruneBlock, x->prune_map_in_lds ? x->num_cus : 2 * x->num_cus);
-  hipLaunchKernelGGL(k_pruned<R>, dim3(pgrid), dim3(kPruneBlock), x->prune_lds, s, x->hs,
-                     merged, x->d, x->ctl, x->heavy, x->prune_map_words, x->prune_map_in_lds, x->prune_buf_cap,
-                     x->cand_key, x->cand_idx, x->cand_cap, x->bitmap);
+  hipLaunchKernelGGL((k_pruned<R, HM>), dim3(pgrid), dim3(kPruneBlock), x->prune_lds, s, x->hs, x->d, x->ctl,
+                     x->heavy, x->prune_map_words, x->prune_map_in_lds, x->prune_buf_cap, x->keys, x->bitmap, rnd);
+  hipLaunchKernelGGL((k_survivors<R, HM>), dim3(x->num_cus), dim3(kBlock), 0, s, x->hs, merged, x->ctl, x->keys,
+                     x->cand_key, x->cand_idx, x->cand_cap, rnd);
   hipLaunchKernelGGL(k_cand_hist, dim3(grid_for(4 * k, kBlock, x->num_cus)), dim3(kBlock), 0, s, x->cand_key, x->ctl,
                      x->cand_cap, x->hist);
   hipLaunchKernelGGL(k_select1p, dim3(1), dim3(kSelBlock), 0, s, x->hist, x->ctl);
@@ -767,8 +953,12 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k) {
 
 template <int R>
 hipError_t allow_prune_lds(size_t bytes) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pruned<R>), hipFuncAttributeMaxDynamicSharedMemorySize,
-                             (int)bytes);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pruned<R, false>),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e == hipSuccess)
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pruned<R, true>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  return e;
 }
 
 // select1 -> compact -> select2 -> finalize -> emit over the keys in x->keys (digit-1
@@ -784,7 +974,10 @@ hipError_t launch_select_tail(gs_ctx* x, hipStream_t s, int64_t k, int gated, in
     hipLaunchKernelGGL(k_compact, dim3((unsigned)grid), dim3(kBlock), 0, s, x->keys, x->d, x->ctl, x->cand_key,
                        x->cand_idx, x->cand_cap, x->bitmap, per_block, gated);
   }
-  hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap);
+  hipLaunchKernelGGL(k_digit2, dim3(x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->ctl, x->cand_cap, x->hist2,
+                     x->keys);
+  hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap,
+                     x->hist2, x->keys);
   hipLaunchKernelGGL(k_finalize, dim3(4 * x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl,
                      x->cand_cap, x->bitmap);
   const int64_t words = (x->d + 31) / 32;
@@ -807,16 +1000,16 @@ hipError_t prepare_prune(gs_ctx* x) {
   const int64_t words = (rc + 63) / 64 * 2;
   const int64_t lds_max = 160 * 1024 - 256;
   x->prune_map_words = words;
-  int64_t buf = (lds_max - words * 4) / 8;
-  if (buf > 4096) buf = 4096;
-  if (buf >= 256) {
+  int64_t buf = (lds_max - words * 4) / 4;
+  if (buf > 8192) buf = 8192;
+  if (buf >= 512) {
     x->prune_map_in_lds = 1;
     x->prune_buf_cap = (int)buf;
-    x->prune_lds = (size_t)(words * 4 + buf * 8);
+    x->prune_lds = (size_t)(words * 4 + buf * 4);
   } else {
     x->prune_map_in_lds = 0;
-    x->prune_buf_cap = 4096;
-    x->prune_lds = 4096 * 8;
+    x->prune_buf_cap = 8192;
+    x->prune_lds = 8192 * 4;
   }
   switch (x->r) {
 #define GS_R_CASE(RR) \
@@ -837,7 +1030,7 @@ hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, i
   switch (x->r) {
 #define GS_R_CASE(RR) \
   case RR:                                            \
-    if (prune) launch_prune_r<RR>(x, s, merged, k);  \
+    if (prune) launch_prune_r<RR, false>(x, s, merged, k, nullptr);  \
     launch_unsketch_r<RR>(x, s, merged, est, gate);  \
     break;
     GS_R_CASE(1) GS_R_CASE(2) GS_R_CASE(3) GS_R_CASE(4) GS_R_CASE(5) GS_R_CASE(6) GS_R_CASE(7) GS_R_CASE(8)
@@ -867,11 +1060,15 @@ hipError_t launch_heavymix_topk(gs_ctx* x, hipStream_t s, const float* merged, i
     first = false;
   }
   hipLaunchKernelGGL(k_theta, dim3(1), dim3(64), 0, s, in, x->r, k, x->ctl);
+  // With an estimate vector requested every coordinate is estimated; otherwise the pruned
+  // pass runs and the full one only acts if the pruned candidates fell short of k.
+  const bool prune = (est == nullptr);
   switch (x->r) {
 #define GS_R_CASE(RR)                                                                                              \
   case RR:                                                                                                         \
+    if (prune) launch_prune_r<RR, true>(x, s, merged, k, rnd);                                                     \
     hipLaunchKernelGGL(k_unsketch_hm<RR>, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->hs, \
-                       merged, x->d, rnd, est, x->keys, x->hist, x->ctl);                                          \
+                       merged, x->d, rnd, est, x->keys, x->hist, x->ctl, prune ? 1 : 0, prune ? 0 : 1);            \
     break;
     GS_R_CASE(1) GS_R_CASE(2) GS_R_CASE(3) GS_R_CASE(4) GS_R_CASE(5) GS_R_CASE(6) GS_R_CASE(7) GS_R_CASE(8)
     GS_R_CASE(9) GS_R_CASE(10) GS_R_CASE(11) GS_R_CASE(12) GS_R_CASE(13) GS_R_CASE(14) GS_R_CASE(15) GS_R_CASE(16)
@@ -879,7 +1076,7 @@ hipError_t launch_heavymix_topk(gs_ctx* x, hipStream_t s, const float* merged, i
     default: return hipErrorInvalidValue;
   }
   if (n_heavy || l2sq) hipLaunchKernelGGL(k_hm_out, dim3(1), dim3(64), 0, s, x->ctl, n_heavy, l2sq);
-  return launch_select_tail(x, s, k, 0, idx);
+  return launch_select_tail(x, s, k, prune ? 1 : 0, idx);
 }
 
 int64_t l2_pad(int64_t c) {

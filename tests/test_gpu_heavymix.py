@@ -63,6 +63,13 @@ def check_identical_sketch(ctx, merged_h, hp, d, k, rnd, label):
     assert l2 == ref["l2sq"], f"{label}: l2sq {l2!r} vs oracle {ref['l2sq']!r}"
     assert nh == ref["n_heavy"], f"{label}: |H| {nh} vs oracle {ref['n_heavy']}"
     assert np.array_equal(idx, ref["idx"]), f"{label}: selection differs ({np.setxor1d(idx, ref['idx']).size} indices)"
+    # without an estimate vector the pruned pass runs (heavy-cell bitmap, sampled fill bound,
+    # unpruned fallback when its candidates fall short of k): the same selection and |H|
+    idx_p = torch.empty(k, dtype=torch.int32, device=DEV)
+    nh_p = torch.empty(1, dtype=torch.int64, device=DEV)
+    ctx.heavymix_topk(to_dev(merged_h), k, rnd_dev(rnd), idx_p, n_heavy=nh_p)
+    assert np.array_equal(host(idx_p), ref["idx"]), f"{label}: pruned HEAVYMIX selection differs"
+    assert int(host(nh_p)[0]) == ref["n_heavy"], f"{label}: pruned |H|"
     # the other selection path on the same context still works after a HEAVYMIX call
     idx_t = torch.empty(k, dtype=torch.int32, device=DEV)
     ctx.unsketch_topk(to_dev(merged_h), k, idx_t)
@@ -173,6 +180,8 @@ EDGE = [
     (65_536, 16, 3000, 655, "spiky"),   # maximum r, even
     (50_000, 5, 1000, 333, "zero"),     # l2sq = 0: every coordinate heavy
     (50_000, 5, 1000, 333, "equal"),    # all draws equal: the fill is the lowest indices
+    (20_000, 5, 300, 20_000, "normal"),  # k = d > the sample: the pruned fill bound admits fewer
+    (50_000, 3, 400, 45_000, "spiky"),   # than k coordinates, so the unpruned pass takes over
 ]
 
 

@@ -333,6 +333,19 @@ def test_all_zero_gradients_every_key_ties():
     dv.close()
 
 
+def test_all_zero_large_dense_survivors():
+    # every cell and coordinate ties at 0: the pruned pass keeps all 2M coordinates (its LDS
+    # queue overflows into direct appends) and the digit-2 pass flushes its per-block buffer
+    # many times before the lowest k indices are selected
+    d, P, r, c, k = 2_000_000, 2, 5, 20_000, 1000
+    hp = synth.hash_params(synth.BASE_SEED + 8, r)
+    dv = Dev(d, P, r, c, k, hp)
+    z = np.zeros((P, d), np.float32)
+    chain_check(dv, z, z.copy(), z.copy(), k, 0.9, label="all-zero 2M")
+    assert np.array_equal(host(dv.idx), np.arange(k, dtype=np.int32))
+    dv.close()
+
+
 def test_single_huge_coordinate():
     d, P, r, c, k = 200_000, 4, 5, 2000, 10
     hp = synth.hash_params(synth.BASE_SEED + 6, r)
