@@ -59,6 +59,8 @@ def _load():
         "ora_heavy_count": (i64, [i64, i64, vp, f64]),
         "ora_row_sq_sum": (f64, [i64, vp]),
         "ora_heavymix": (ctypes.c_int, [i64, i32, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "ora_sketch_momentum_step": (ctypes.c_int, [i32, i64, i32, i64, i64, f32, i32, vp, vp, vp, vp, vp, vp, vp,
+                                                    vp, vp, vp, vp]),
         "ora_step": (ctypes.c_int, [i32, i64, i32, i64, i64, f32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                     vp, vp, vp]),
     }
@@ -239,6 +241,26 @@ def heavymix(merged: np.ndarray, hp: dict, d: int, k: int, rnd: np.ndarray) -> d
     _check(_load().ora_heavymix(d, r, c, k, _p(a), _p(b), _p(a2), _p(b2), _p(merged), _p(rnd), _p(est), _p(idx),
                                 ctypes.addressof(nh), ctypes.addressof(l2)), "heavymix")
     return {"idx": idx, "n_heavy": int(nh.value), "l2sq": float(l2.value), "est": est}
+
+
+def sketch_momentum_step(g, U, E, hp: dict, k: int, rho: float = 0.9, reset_momentum: bool = True,
+                         want_est: bool = True) -> dict:
+    """Momentum and error kept in the sketch (one step): U, E ([r][c] fp32) are updated in
+    place. Returns {"merged", "idx" (ascending), "values" (the estimates at idx), "est"}."""
+    g = _f32(g)
+    P, d = g.shape
+    a, b, a2, b2 = _hp(hp)
+    r, c = U.shape
+    assert U.dtype == np.float32 and E.dtype == np.float32 and U.flags.c_contiguous and E.flags.c_contiguous
+    assert E.shape == (r, c) and a.size == r
+    merged = np.empty((r, c), dtype=np.float32)
+    est = np.empty(d, dtype=np.float32) if want_est else None
+    idx = np.empty(k, dtype=np.int32)
+    values = np.empty(k, dtype=np.float32)
+    _check(_load().ora_sketch_momentum_step(P, d, r, c, k, rho, int(bool(reset_momentum)), _p(a), _p(b), _p(a2),
+                                            _p(b2), _p(g), _p(U), _p(E), _p(merged), _p(est), _p(idx), _p(values)),
+           "sketch_momentum_step")
+    return {"merged": merged, "idx": idx, "values": values, "est": est}
 
 
 def step(g, u, v, hp: dict, c: int, k: int, rho: float = 0.9, reset_momentum: bool = True,

@@ -30,6 +30,7 @@
  *   Top_k         the k largest |estimate|, ties to the lower index, returned ascending
  *   HEAVYMIX      as printed, with a fixed pairwise order for the row sums of squares and
  *                 the random fill taken from caller-supplied draws (see ora_heavymix)
+ *   sketch state  momentum and error kept in the merged sketch (see ora_sketch_momentum_step)
  *   reset         v (and u when reset_momentum) zeroed at Top_k on every worker
  *
  * Build: gcc -O2 -ffp-contract=off -std=c11 (no -ffast-math). On x86-64 float arithmetic
@@ -425,6 +426,62 @@ int ora_heavymix(int64_t d, int32_t r, int64_t c, int64_t k, const uint32_t* ha,
   free(heavy);
   free(light);
   return rc;
+}
+
+/* ---------------------------------------------------------------------------------- */
+/* Momentum and error accumulation kept in the sketch (the sketch is linear, so both can be
+ * carried inside it: Sec. II, sketching paragraph, after FetchSGD). One step:
+ *   S = tree-order merge of the P workers' sketches of g          (Alg. 1 sketch + reduction)
+ *   U <- fl(fl(rho * U) + S),  E <- fl(E + U)                       (per cell, fp32, no FMA)
+ *   est = median unsketch of E;  Top_k = the k largest |est|, ties to the lower index
+ *   values: Delta_i = est_i for i in Top_k (no per-worker vectors hold exact values)
+ *   E <- fl(E - D) on every cell D touches, where D = S(Delta) is the sketch of the sparse
+ *        selection, each touched cell summed in fp64 and rounded once to fp32
+ *   U <- 0 on those cells when reset_momentum (momentum masking)
+ * U and E are [r][c], updated in place; merged ([r][c]) receives S; est ([d]) may be NULL. */
+
+int ora_sketch_momentum_step(int32_t P, int64_t d, int32_t r, int64_t c, int64_t k, float rho,
+                             int32_t reset_momentum, const uint32_t* ha, const uint32_t* hb, const uint32_t* sa,
+                             const uint32_t* sb, const float* g, float* U, float* E, float* merged, float* est,
+                             int32_t* idx, float* values) {
+  const int64_t rc = (int64_t)r * c;
+  float* tb = (float*)malloc((size_t)P * (size_t)rc * sizeof(float));
+  float* es = est ? est : (float*)malloc((size_t)d * sizeof(float));
+  double* acc = (double*)calloc((size_t)rc, sizeof(double));
+  unsigned char* touched = (unsigned char*)calloc((size_t)rc, 1);
+  int rc_ = (!tb || !es || !acc || !touched) ? 1 : 0;
+  if (!rc_) rc_ = ora_sketch(P, d, r, c, ha, hb, sa, sb, g, tb);
+  if (!rc_) rc_ = ora_merge(P, rc, tb, merged);
+  if (!rc_) {
+    for (int64_t e = 0; e < rc; ++e) {
+      float m = rho * U[e];
+      U[e] = m + merged[e];
+      E[e] = E[e] + U[e];
+    }
+    rc_ = ora_unsketch(d, r, c, ha, hb, sa, sb, E, es);
+  }
+  if (!rc_) rc_ = ora_topk(d, k, es, idx, NULL);
+  if (!rc_) {
+    for (int64_t t = 0; t < k; ++t) {
+      const int64_t i = idx[t];
+      values[t] = es[i];
+      for (int32_t j = 0; j < r; ++j) {
+        const int64_t cell = (int64_t)j * c + ora_bucket(ha[j], hb[j], c, i);
+        acc[cell] += (double)ora_sign(sa[j], sb[j], i) * (double)es[i];
+        touched[cell] = 1;
+      }
+    }
+    for (int64_t e = 0; e < rc; ++e) {
+      if (!touched[e]) continue;
+      E[e] = E[e] - (float)acc[e];
+      if (reset_momentum) U[e] = 0.0f;
+    }
+  }
+  free(tb);
+  if (!est) free(es);
+  free(acc);
+  free(touched);
+  return rc_;
 }
 
 /* ---------------------------------------------------------------------------------- */

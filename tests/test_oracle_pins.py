@@ -598,3 +598,93 @@ def test_heavymix_fill_is_uniform_over_the_non_heavy_set():
     chi2 = float(np.sum((counts[light] - expect) ** 2 / (expect * (1 - p))))
     dof = light.size - 1
     assert abs(chi2 - dof) < 6 * np.sqrt(2 * dof), (chi2, dof)
+
+
+# ---------------------------------------------------------------------------------------
+# Momentum and error kept in the sketch (the sketch is linear: Sec. II, sketching paragraph)
+
+def _collision_free_hash(d, c, r, seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(200):
+        hp = _hp(rng, r)
+        if all(len(set(oracle.buckets(int(hp["a"][j]), int(hp["b"][j]), c, range(d)))) == d for j in range(r)):
+            return hp
+    raise AssertionError("no collision-free hash found")
+
+
+def test_sketch_momentum_equals_vector_space_when_collision_free_and_exact():
+    # With no two coordinates sharing a cell and every operation exact (small integer
+    # gradients, rho = 0.5), the sketch of the summed vector-space state is the sketch-space
+    # state: the same selections and values on every step, and the reset at Top_k in vector
+    # space is the subtraction plus momentum mask in sketch space.
+    d, P, r, c, k = 300, 3, 3, 1 << 20, 17
+    hp = _collision_free_hash(d, c, r, 61)
+    rng = np.random.default_rng(62)
+    u = np.zeros((P, d), np.float32)
+    v = np.zeros((P, d), np.float32)
+    U = np.zeros((r, c), np.float32)
+    E = np.zeros((r, c), np.float32)
+    for t in range(5):
+        g = rng.integers(-8, 9, size=(P, d)).astype(np.float32)
+        vec = oracle.step(g, u, v, hp, c, k, rho=0.5, want_tables=False, want_est=False)
+        sk = oracle.sketch_momentum_step(g, U, E, hp, k, rho=0.5)
+        assert np.array_equal(sk["idx"], vec["idx"]), t
+        assert np.array_equal(sk["values"], vec["values"]), t
+        # the state itself: E and U are the sketches of sum_q v and sum_q u
+        assert np.array_equal(E, oracle.sketch(v.sum(axis=0, keepdims=True), hp, c)[0]), t
+        assert np.array_equal(U, oracle.sketch(u.sum(axis=0, keepdims=True), hp, c)[0]), t
+
+
+def test_sketch_momentum_k_equals_d_clears_the_state():
+    d, P, r, c = 64, 2, 3, 1 << 16
+    hp = _collision_free_hash(d, c, r, 63)
+    g = np.random.default_rng(64).standard_normal((P, d)).astype(np.float32)
+    U = np.zeros((r, c), np.float32)
+    E = np.zeros((r, c), np.float32)
+    res = oracle.sketch_momentum_step(g, U, E, hp, d, rho=0.9)
+    assert res["idx"].tolist() == list(range(d))
+    assert not E.any() and not U.any()
+
+
+def test_sketch_momentum_without_reset_keeps_momentum_and_composes():
+    rng = np.random.default_rng(65)
+    d, P, r, c, k = 3000, 4, 5, 400, 30
+    hp = _hp(rng, r)
+    U0 = rng.standard_normal((r, c)).astype(np.float32)
+    E0 = rng.standard_normal((r, c)).astype(np.float32)
+    g = rng.standard_normal((P, d)).astype(np.float32)
+    U, E = U0.copy(), E0.copy()
+    res = oracle.sketch_momentum_step(g, U, E, hp, k, rho=0.9, reset_momentum=False)
+    S = oracle.merge(oracle.sketch(g, hp, c))
+    assert np.array_equal(res["merged"], S)
+    want_U = (np.float32(0.9) * U0).astype(np.float32) + S
+    assert np.array_equal(U, want_U)
+    E1 = E0 + want_U
+    est = oracle.unsketch(E1, hp, d)
+    idx, _ = oracle.topk(est, k)
+    assert np.array_equal(res["idx"], idx) and np.array_equal(res["values"], est[idx])
+    # untouched cells keep E1; the others moved by the selection's sketch
+    touched = np.zeros((r, c), bool)
+    for j in range(r):
+        touched[j, oracle.buckets(int(hp["a"][j]), int(hp["b"][j]), c, idx)] = True
+    assert np.array_equal(E[~touched], E1[~touched])
+    assert not np.array_equal(E[touched], E1[touched])
+
+
+def test_sketch_momentum_subtracts_the_selection_sketch_worked_example():
+    # One cell (r = c = 1), two coordinates with sign +1, g = (1, 2), rho = 0, k = 2 = d:
+    # U = S = 1 + 2 = 3, E = 3; both estimates are 3; the selection's sketch is 3 + 3 = 6,
+    # so E becomes 3 - 6 = -3 (a cell shared by selected coordinates is over-corrected, not
+    # zeroed), and U is masked to 0.
+    rng = np.random.default_rng(66)
+    for _ in range(1000):
+        hp = _hp(rng, 1)
+        if oracle.signs(int(hp["a2"][0]), int(hp["b2"][0]), [0, 1]).tolist() == [1, 1]:
+            break
+    else:
+        raise AssertionError("no all-positive sign hash found")
+    U = np.zeros((1, 1), np.float32)
+    E = np.zeros((1, 1), np.float32)
+    res = oracle.sketch_momentum_step(np.array([[1.0, 2.0]], np.float32), U, E, hp, 2, rho=0.0)
+    assert res["merged"][0, 0] == 3.0 and res["values"].tolist() == [3.0, 3.0]
+    assert E[0, 0] == -3.0 and U[0, 0] == 0.0
