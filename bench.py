@@ -127,6 +127,9 @@ def main():
     ap.add_argument("--selection", choices=("topk", "heavymix"), default="topk",
                     help="topk: deterministic top-k by |estimate| (gs_step); heavymix: HEAVYMIX as printed with a "
                          "seeded random fill (gs_step_heavymix)")
+    ap.add_argument("--state", choices=("vector", "sketch"), default="vector",
+                    help="vector: per-worker u, v d-vectors (gs_step / gs_step_heavymix); sketch: momentum and error "
+                         "kept in the merged sketch (gs_step_sketch_momentum; deterministic top-k)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="before warm-up, run one plain device copy of the gradient buffer (P*d*4 bytes read and "
                          "written) to calibrate rocprofv3 FETCH_SIZE / WRITE_SIZE counters")
@@ -155,7 +158,16 @@ def main():
     idx = torch.empty(w.k, dtype=torch.int32, device=dev)
     vals = torch.empty(w.k, dtype=torch.float32, device=dev)
     ctx = gs.GsContext(w.d, w.P, w.r, w.c, w.k, hp, rho=w.rho)
-    if args.selection == "heavymix":
+    if args.state == "sketch":
+        if args.selection != "topk":
+            print("--state sketch uses the deterministic top-k selection", file=sys.stderr)
+            sys.exit(2)
+        U_s = torch.zeros((w.r, w.c), dtype=torch.float32, device=dev)
+        E_s = torch.zeros_like(U_s)
+
+        def run_step(s_):
+            ctx.step_sketch_momentum(g_dev[s_ % nb], U_s, E_s, w.k, merged, idx, vals)
+    elif args.selection == "heavymix":
         # one set of fill draws per gradient batch (fresh draws each step in real use)
         rnd_dev = [torch.from_numpy(synth.fill_draws(w, t).view(np.int32)).to(dev) for t in range(nb)]
 
@@ -245,7 +257,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "d": w.d, "P": w.P, "r": w.r, "c": w.c, "k": w.k,
-                   "selection": args.selection, "gradients": w.note},
+                   "selection": args.selection, "state": args.state, "gradients": w.note},
         "coords_per_s_per_worker": w.d / t,
         "algorithmic_bytes_per_step": B,
         "achieved_gbs": B / t / 1e9,

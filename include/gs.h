@@ -147,6 +147,21 @@ gs_status gs_heavymix_topk(gs_ctx* ctx, void* stream, const float* merged, int64
 gs_status gs_step_heavymix(gs_ctx* ctx, void* stream, const float* g, float* u, float* v, int64_t k,
                            const uint32_t* rnd, float* merged, int32_t* idx, float* values, int64_t* n_heavy);
 
+/* One step with momentum and error accumulation kept in the merged sketch instead of in
+ * per-worker d-vectors (the sketch is linear, so both can be carried inside it: Sec. II,
+ * sketching paragraph). With S the tree-order merge of the P workers' sketches of g:
+ *   U <- fl(fl(rho U) + S), E <- fl(E + U)                      per cell, fp32, no FMA
+ *   idx = the k largest |estimate of E|, ties to the lower index, ascending
+ *   values[t] = the estimate of E at idx[t] (taken before the correction below)
+ *   E <- fl(E - D) on every cell that D touches, with D the sketch of the selection (the
+ *        values at idx, signed and bucketed like any sketch), each cell summed in double
+ *        precision and rounded once; U <- 0 on those cells when reset_momentum is set.
+ * g: [P][d] input. U, E: [r][c] state, updated in place (zero before the first step).
+ * merged: [r][c] output (S). idx: [k] output, values: [k] output. 1 <= k <= k_max.
+ * Uses the context's per-worker sketch scratch, so calls on one context must not overlap. */
+gs_status gs_step_sketch_momentum(gs_ctx* ctx, void* stream, const float* g, float* U, float* E, int64_t k,
+                                  float* merged, int32_t* idx, float* values);
+
 /* Stage timing for benchmarks and profiling. Runs exactly the kernels of gs_step, records a
  * HIP event on `stream` before the first stage and after each stage, synchronizes the stream
  * and writes the stage durations in milliseconds to the HOST array stage_ms[GS_NUM_STAGES]:

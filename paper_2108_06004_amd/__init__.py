@@ -23,8 +23,8 @@ GS_OK, GS_ERR_INVALID_ARG, GS_ERR_OUT_OF_MEMORY, GS_ERR_DEVICE, GS_ERR_UNSUPPORT
 GS_MAX_WORKERS = 64
 GS_MAX_ROWS = 16
 EXPORTED = ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
-            "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_profiled",
-            "gs_status_string", "gs_last_error")
+            "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_sketch_momentum",
+            "gs_step_profiled", "gs_status_string", "gs_last_error")
 GS_NUM_STAGES = 5
 STAGES = ("accumulate", "sketch", "merge", "select", "gather_reset")
 
@@ -78,8 +78,10 @@ def load_library():
     lib.gs_step_profiled.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp, vp]
     lib.gs_heavymix_topk.argtypes = [vp, vp, vp, i64, vp, vp, vp, vp, vp]
     lib.gs_step_heavymix.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp]
+    lib.gs_step_sketch_momentum.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp]
     for name in ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
-                 "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_profiled"):
+                 "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_sketch_momentum",
+                 "gs_step_profiled"):
         getattr(lib, name).restype = st
     lib.gs_status_string.argtypes = [st]
     lib.gs_status_string.restype = ctypes.c_char_p
@@ -186,6 +188,13 @@ def gs_step_heavymix(ctx: int, g, u, v, k: int, rnd, merged, idx, values, n_heav
                                            _ptr(n_heavy, name="n_heavy")), ctx, "gs_step_heavymix")
 
 
+def gs_step_sketch_momentum(ctx: int, g, U, E, k: int, merged, idx, values, stream=None) -> None:
+    _check(load_library().gs_step_sketch_momentum(ctx, _stream(stream), _ptr(g, name="g"), _ptr(U, name="U"),
+                                                  _ptr(E, name="E"), k, _ptr(merged, name="merged"),
+                                                  _ptr(idx, name="idx"), _ptr(values, name="values")),
+           ctx, "gs_step_sketch_momentum")
+
+
 def gs_step_profiled(ctx: int, g, u, v, k: int, merged, idx, values, stream=None) -> dict:
     """gs_step with per-stage HIP-event timing (blocks until done); returns stage -> ms."""
     ms = (ctypes.c_float * GS_NUM_STAGES)()
@@ -289,6 +298,16 @@ class GsContext:
         gs_step_heavymix(self.handle, self._f32(g, n, "g"), self._f32(u, n, "u"), self._f32(v, n, "v"), k, rnd,
                          self._f32(merged, self.r * self.c, "merged"), idx, self._f32(values, k, "values"), n_heavy,
                          stream)
+
+    def step_sketch_momentum(self, g, U, E, k, merged, idx, values, stream=None):
+        """Momentum and error kept in the sketch: U, E are [r][c] fp32 state tensors."""
+        import torch
+
+        rc = self.r * self.c
+        _ptr(idx, torch.int32, k, "idx")
+        gs_step_sketch_momentum(self.handle, self._f32(g, self.P * self.d, "g"), self._f32(U, rc, "U"),
+                                self._f32(E, rc, "E"), k, self._f32(merged, rc, "merged"), idx,
+                                self._f32(values, k, "values"), stream)
 
     def step_profiled(self, g, u, v, k, merged, idx, values, stream=None) -> dict:
         import torch

@@ -301,6 +301,28 @@ gs_status gs_step_heavymix(gs_ctx* x, void* stream, const float* g, float* u, fl
   return device_status(x, e, "gs_step_heavymix");
 }
 
+gs_status gs_step_sketch_momentum(gs_ctx* x, void* stream, const float* g, float* U, float* E, int64_t k,
+                                  float* merged, int32_t* idx, float* values) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!g || !U || !E || !merged || !idx || !values)
+    return fail(x, GS_ERR_INVALID_ARG, "gs_step_sketch_momentum: NULL array");
+  if (k < 1 || k > x->k_max)
+    return fail(x, GS_ERR_INVALID_ARG, "gs_step_sketch_momentum: k must satisfy 1 <= k <= k_max");
+  hipStream_t s = as_stream(stream);
+  hipError_t e;
+  if (x->use_pull) {
+    e = gs::launch_interleave(x, s, g);
+    if (e == hipSuccess) e = gs::launch_pull(x, s);
+    if (e == hipSuccess) e = gs::launch_merge_partials(x, s, merged, nullptr);
+  } else {
+    e = gs::launch_sketch_acc(x, s, g);
+    if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
+  }
+  if (e == hipSuccess) e = gs::launch_sketch_state(x, s, merged, U, E, k, idx, values);
+  return device_status(x, e, "gs_step_sketch_momentum");
+}
+
 gs_status gs_step_profiled(gs_ctx* x, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
                            int32_t* idx, float* values, float* stage_ms) {
   if (!x) return GS_ERR_INVALID_ARG;

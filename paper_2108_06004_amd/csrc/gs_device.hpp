@@ -128,6 +128,21 @@ __device__ __forceinline__ float median_sorted(const float (&v)[R]) {
   }
 }
 
+// The estimate of coordinate i from a merged sketch (Alg. 2, query): the median over rows
+// of s_j(i) * S[j][h_j(i)].
+template <int R>
+__device__ __forceinline__ float estimate_val(const RowConst (&kr)[R], const float* __restrict__ merged, uint32_t i) {
+  float val[R];
+#pragma unroll
+  for (int j = 0; j < R; ++j) {
+    uint32_t col, sflip;
+    hash_row(kr[j], i, col, sflip);
+    val[j] = apply_sign(merged[(int64_t)j * kr[j].c + col], sflip);
+  }
+  sort_net<R>(val);
+  return median_sorted<R>(val);
+}
+
 // |x| as an order-preserving uint32 key (non-negative floats order like their bits).
 __device__ __forceinline__ uint32_t abs_key(float x) { return __float_as_uint(x) & 0x7fffffffu; }
 

@@ -131,11 +131,29 @@ __global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int6
 // Per step: accumulation that also writes the worker-interleaved copy of v.
 // One lane handles 4 consecutive coordinates of every worker (float4 per worker row).
 
+// Rows 4t .. 4t+3 of vI from the P workers' values vv[q][m] of coordinate 4t + m.
+template <int P>
+__device__ __forceinline__ void write_vi_rows(float* __restrict__ vI, int64_t t, const float (&vv)[P][4]) {
+  constexpr int PP = (P + 3) & ~3;
+  f4* dst = reinterpret_cast<f4*>(vI + (4 * t) * PP);
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+#pragma unroll
+    for (int q0 = 0; q0 < PP; q0 += 4) {
+      f4 x;
+      x.x = q0 + 0 < P ? vv[q0 + 0 < P ? q0 + 0 : 0][m] : 0.f;
+      x.y = q0 + 1 < P ? vv[q0 + 1 < P ? q0 + 1 : 0][m] : 0.f;
+      x.z = q0 + 2 < P ? vv[q0 + 2 < P ? q0 + 2 : 0][m] : 0.f;
+      x.w = q0 + 3 < P ? vv[q0 + 3 < P ? q0 + 3 : 0][m] : 0.f;
+      dst[(m * PP + q0) / 4] = x;
+    }
+  }
+}
+
 template <int P>
 __global__ void __launch_bounds__(kBlock) k_accumulate_vi(const float* __restrict__ g, float* __restrict__ u,
                                                           float* __restrict__ v, float* __restrict__ vI, int64_t d,
                                                           float rho) {
-  constexpr int PP = (P + 3) & ~3;  // vI row length
   const int64_t n4 = d / 4;
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n4; t += stride) {
@@ -155,19 +173,27 @@ __global__ void __launch_bounds__(kBlock) k_accumulate_vi(const float* __restric
       vv[q][2] = w.z;
       vv[q][3] = w.w;
     }
-    f4* dst = reinterpret_cast<f4*>(vI + (4 * t) * PP);
+    write_vi_rows<P>(vI, t, vv);
+  }
+}
+
+// Interleave only (the sketch of a given [P][d] array, e.g. the gradients).
+template <int P>
+__global__ void __launch_bounds__(kBlock) k_interleave4(const float* __restrict__ src, float* __restrict__ vI,
+                                                        int64_t d) {
+  const int64_t n4 = d / 4;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n4; t += stride) {
+    float vv[P][4];
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-#pragma unroll
-      for (int q0 = 0; q0 < PP; q0 += 4) {
-        f4 x;
-        x.x = q0 + 0 < P ? vv[q0 + 0 < P ? q0 + 0 : 0][m] : 0.f;
-        x.y = q0 + 1 < P ? vv[q0 + 1 < P ? q0 + 1 : 0][m] : 0.f;
-        x.z = q0 + 2 < P ? vv[q0 + 2 < P ? q0 + 2 : 0][m] : 0.f;
-        x.w = q0 + 3 < P ? vv[q0 + 3 < P ? q0 + 3 : 0][m] : 0.f;
-        dst[(m * PP + q0) / 4] = x;
-      }
+    for (int q = 0; q < P; ++q) {
+      const f4 w = __builtin_nontemporal_load(reinterpret_cast<const f4*>(src) + q * n4 + t);
+      vv[q][0] = w.x;
+      vv[q][1] = w.y;
+      vv[q][2] = w.z;
+      vv[q][3] = w.w;
     }
+    write_vi_rows<P>(vI, t, vv);
   }
 }
 
@@ -466,6 +492,18 @@ hipError_t launch_accumulate_vi(const gs_ctx* x, hipStream_t s, const float* g, 
 }
 
 hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v) {
+  if ((x->d % 4 == 0) && ((uintptr_t)v % 16 == 0) && x->P <= 16) {
+    const dim3 grid(grid_for(x->d / 4, kBlock, 64 * x->num_cus)), block(kBlock);
+    switch (x->P) {
+#define GS_IL_CASE(PP) \
+  case PP: hipLaunchKernelGGL(k_interleave4<PP>, grid, block, 0, s, v, x->vI, x->d); return hipGetLastError();
+      GS_IL_CASE(1) GS_IL_CASE(2) GS_IL_CASE(3) GS_IL_CASE(4) GS_IL_CASE(5) GS_IL_CASE(6) GS_IL_CASE(7) GS_IL_CASE(8)
+      GS_IL_CASE(9) GS_IL_CASE(10) GS_IL_CASE(11) GS_IL_CASE(12) GS_IL_CASE(13) GS_IL_CASE(14) GS_IL_CASE(15)
+      GS_IL_CASE(16)
+#undef GS_IL_CASE
+      default: break;
+    }
+  }
   const int64_t n = (int64_t)x->P * x->d;
   hipLaunchKernelGGL(k_accumulate_vi_any, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, nullptr,
                      nullptr, const_cast<float*>(v), x->vI, x->d, x->P, x->plan.PP, x->rho, 0);

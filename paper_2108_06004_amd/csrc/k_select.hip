@@ -429,19 +429,6 @@ __global__ void __launch_bounds__(kBlock) k_finalize(const uint32_t* __restrict_
 // either way.
 
 template <int R>
-__device__ __forceinline__ float estimate_val(const RowConst (&kr)[R], const float* __restrict__ merged, uint32_t i) {
-  float val[R];
-#pragma unroll
-  for (int j = 0; j < R; ++j) {
-    uint32_t col, sflip;
-    hash_row(kr[j], i, col, sflip);
-    val[j] = apply_sign(merged[(int64_t)j * kr[j].c + col], sflip);
-  }
-  sort_net<R>(val);
-  return median_sorted<R>(val);
-}
-
-template <int R>
 __device__ __forceinline__ uint32_t estimate_key(const RowConst (&kr)[R], const float* __restrict__ merged,
                                                  uint32_t i) {
   return abs_key(estimate_val<R>(kr, merged, i));
