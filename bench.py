@@ -12,7 +12,8 @@ Prints one JSON line with
   roofline     the dominant stage's algorithmic bytes / its mean duration (HIP events on
                the stream the kernels run on) against MI355X's 8 TB/s HBM peak
   cpu_baseline the plain CPU oracle (single thread) timed on a bounded sample
-Algorithmic bytes per step: B = 20*P*d + 8*P*r*c + 8*r*c + 12*P*k + 8*k.
+Algorithmic bytes per step: B = 20*P*d + 8*P*r*c + 8*r*c + 12*P*k + 8*k (vector state); with
+--state sketch (momentum and error kept in the sketch) B = 4*P*d + 8*P*r*c + 28*r*c + 8*k.
 """
 from __future__ import annotations
 
@@ -239,7 +240,12 @@ def main():
     copy_gbs = 2 * src.numel() * 4 / (c0.elapsed_time(c1) / ncopy * 1e-3) / 1e9
     del dst
 
-    B = 20 * w.P * w.d + 8 * w.P * w.r * w.c + 8 * w.r * w.c + 12 * w.P * w.k + 8 * w.k
+    if args.state == "sketch":
+        # read g; write and read the P tables; merged written; U, E read and written; E read
+        # again for the estimates; idx and values written
+        B = 4 * w.P * w.d + 8 * w.P * w.r * w.c + 4 * w.r * w.c + 16 * w.r * w.c + 4 * w.r * w.c + 8 * w.k
+    else:
+        B = 20 * w.P * w.d + 8 * w.P * w.r * w.c + 8 * w.r * w.c + 12 * w.P * w.k + 8 * w.k
     t = ms * 1e-3
     out = {
         "metric": METRIC,
