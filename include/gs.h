@@ -76,7 +76,12 @@ typedef struct gs_config {
 typedef struct gs_ctx gs_ctx; /* opaque: a copy of the config plus device scratch */
 
 /* Validate `cfg`, copy it, and allocate the device scratch on the current HIP device.
- * This is the only call that allocates. On success *out receives the context. */
+ * This is the only call that allocates. On success *out receives the context.
+ * The sketch runs as a gather into LDS tiles from per-tile coordinate lists built here;
+ * when those lists cannot be built (more than 40,960 tiles) it runs as fp64 device
+ * atomics instead. Setting the environment variable GS_SKETCH_PATH=atomic before the call
+ * selects the atomic form for any shape (a diagnostic override; results agree within the
+ * table tolerance). */
 gs_status gs_create(const gs_config* cfg, gs_ctx** out);
 
 /* Free the context's scratch (after synchronizing the device). NULL is accepted. */

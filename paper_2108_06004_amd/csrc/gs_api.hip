@@ -2,6 +2,7 @@
 // its device scratch, and the kernel sequence of each call.
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -168,6 +169,11 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   }
   x->plan = gs::make_pull_plan(x->d, x->P, x->r, x->c, x->num_cus);
   x->use_pull = (int64_t)x->plan.T * (int64_t)sizeof(uint32_t) <= gs::kMaxFillLds;
+  {
+    // diagnostic override: GS_SKETCH_PATH=atomic selects the fp64-atomic sketch for any plan
+    const char* path = std::getenv("GS_SKETCH_PATH");
+    if (path && std::strcmp(path, "atomic") == 0) x->use_pull = false;
+  }
   if (x->use_pull) {
     chk(alloc(&x->list, (int64_t)x->r * x->d));
     chk(alloc(&x->tile_off, (int64_t)x->plan.T + 1));

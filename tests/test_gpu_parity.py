@@ -346,6 +346,22 @@ def test_all_zero_large_dense_survivors():
     dv.close()
 
 
+@pytest.mark.parametrize("d,P,r,c,k", [(10_007, 3, 5, 211, 300), (65_536, 8, 4, 4096, 655), (3001, 17, 5, 97, 60)])
+def test_atomic_sketch_path(monkeypatch, d, P, r, c, k):
+    # the fp64-atomic sketch (used when the tile lists cannot be built) through every entry
+    # point, the fused step included
+    monkeypatch.setenv("GS_SKETCH_PATH", "atomic")
+    hp = synth.hash_params(synth.BASE_SEED + 19 * d + P, r)
+    rng = np.random.default_rng(d + P)
+    dv = Dev(d, P, r, c, k, hp, 0.9)
+    u = rng.standard_normal((P, d)).astype(np.float32)
+    v = rng.standard_normal((P, d)).astype(np.float32)
+    for t in range(2):
+        g = rng.laplace(0, 1e-2, (P, d)).astype(np.float32)
+        u, v = chain_check(dv, g, u, v, k, 0.9, label=f"atomic d={d} P={P} r={r} c={c} k={k} t={t}")
+    dv.close()
+
+
 def test_single_huge_coordinate():
     d, P, r, c, k = 200_000, 4, 5, 2000, 10
     hp = synth.hash_params(synth.BASE_SEED + 6, r)

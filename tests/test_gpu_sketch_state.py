@@ -136,3 +136,17 @@ def test_sketch_state_rejects_invalid_arguments():
         gs.gs_step_sketch_momentum(ctx.handle, g, U, U.clone(), w.k + 1, U.clone(), idx, vals)
     assert e.value.status == gs.GS_ERR_INVALID_ARG
     ctx.close()
+
+
+def test_sketch_state_atomic_sketch_path(monkeypatch):
+    monkeypatch.setenv("GS_SKETCH_PATH", "atomic")
+    d, P, r, c, k = 20_000, 4, 5, 700, 150
+    hp = synth.hash_params(synth.BASE_SEED + 77, r)
+    rng = np.random.default_rng(77)
+    ctx = gs.GsContext(d, P, r, c, k, hp, rho=0.9)
+    U = np.zeros((r, c), np.float32)
+    E = np.zeros((r, c), np.float32)
+    for t in range(3):
+        g = rng.standard_normal((P, d)).astype(np.float32)
+        U, E = state_step(ctx, g, U, E, hp, k, 0.9, True, f"atomic sketch state t={t}")
+    ctx.close()
