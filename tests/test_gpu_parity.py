@@ -423,3 +423,46 @@ def test_invalid_arguments_are_rejected_on_device_calls():
         gs.gs_gather_reset(dv.ctx.handle, dv.idx, 0, dv.est, dv.est, dv.values)
     assert e.value.status == gs.GS_ERR_INVALID_ARG
     dv.close()
+
+
+def test_two_contexts_and_a_side_stream():
+    # two live contexts of different shapes, calls interleaved, one of them on a side stream:
+    # each result equals the same call made alone on a fresh context
+    wa = synth.WORKLOADS["t3planted-d65536-P4"]
+    wb = synth.WORKLOADS["laplace20-d270000-P4"]
+    ga, gb = synth.gradients(wa, 0), synth.gradients(wb, 0)
+
+    def alone(w, g):
+        dv = Dev(w.d, w.P, w.r, w.c, w.k, synth.hash_params(w), w.rho)
+        u = torch.zeros((w.P, w.d), dtype=torch.float32, device=DEV)
+        v = torch.zeros_like(u)
+        dv.ctx.step(to_dev(g), u, v, w.k, dv.merged, dv.idx, dv.values)
+        out = (host(dv.merged).copy(), host(dv.idx).copy(), host(dv.values).copy(), host(u), host(v))
+        dv.close()
+        return out
+
+    ref_a, ref_b = alone(wa, ga), alone(wb, gb)
+    da = Dev(wa.d, wa.P, wa.r, wa.c, wa.k, synth.hash_params(wa), wa.rho)
+    db = Dev(wb.d, wb.P, wb.r, wb.c, wb.k, synth.hash_params(wb), wb.rho)
+    side = torch.cuda.Stream()
+    ua = torch.zeros((wa.P, wa.d), dtype=torch.float32, device=DEV)
+    va = torch.zeros_like(ua)
+    ub = torch.zeros((wb.P, wb.d), dtype=torch.float32, device=DEV)
+    vb = torch.zeros_like(ub)
+    ga_d, gb_d = to_dev(ga), to_dev(gb)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(side):
+        db.ctx.step(gb_d, ub, vb, wb.k, db.merged, db.idx, db.values, stream=side)
+    da.ctx.step(ga_d, ua, va, wa.k, da.merged, da.idx, da.values)
+    side.synchronize()
+    torch.cuda.synchronize()
+    got_a = (host(da.merged), host(da.idx), host(da.values), host(ua), host(va))
+    got_b = (host(db.merged), host(db.idx), host(db.values), host(ub), host(vb))
+    assert_tol(got_a[0], ref_a[0], "context A merged")
+    assert np.array_equal(got_a[1], ref_a[1]) and np.array_equal(got_a[2], ref_a[2])
+    assert np.array_equal(got_a[3], ref_a[3]) and np.array_equal(got_a[4], ref_a[4])
+    assert_tol(got_b[0], ref_b[0], "context B merged")
+    assert np.array_equal(got_b[1], ref_b[1]) and np.array_equal(got_b[2], ref_b[2])
+    assert np.array_equal(got_b[3], ref_b[3]) and np.array_equal(got_b[4], ref_b[4])
+    da.close()
+    db.close()
