@@ -46,7 +46,7 @@ hipError_t alloc(T** p, int64_t count) {
 
 void free_scratch(gs_ctx* x) {
   void* ptrs[] = {x->keys, x->hist, x->hist2, x->ctl, x->cand_key, x->cand_idx, x->bitmap, x->blockcnt, x->acc64,
-                  x->list, x->tile_off, x->vI, x->partial, x->sample_keys, x->heavy, x->l2buf};
+                  x->list, x->tile_off, x->vI, x->partial, x->sample_keys, x->heavy, x->l2buf, x->coarse};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   x->keys = nullptr;
@@ -65,6 +65,7 @@ void free_scratch(gs_ctx* x) {
   x->sample_keys = nullptr;
   x->heavy = nullptr;
   x->l2buf = nullptr;
+  x->coarse = nullptr;
 }
 
 bool valid_ab(const uint32_t* a, const uint32_t* b, int r) {

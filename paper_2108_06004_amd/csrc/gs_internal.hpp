@@ -70,7 +70,10 @@ struct gs_ctx {
   uint32_t* sample_keys = nullptr;  // [kSampleMax]
   uint32_t* heavy = nullptr;        // [ceil(r*c/64)*2] heavy-cell bitmap
   int64_t prune_map_words = 0;      // words of the heavy bitmap
-  int prune_map_in_lds = 0;         // 1: the pruned pass keeps the bitmap in LDS
+  int prune_map_in_lds = 0;         // 1: the pruned pass keeps a bitmap in LDS (fine, or coarse below)
+  int prune_coarse_log2 = 0;        // > 0: LDS holds the coarse map, one bit per 2^this cells
+  uint32_t* coarse = nullptr;       // coarse heavy-cell map (bit = OR of its cells' heavy bits)
+  int64_t prune_coarse_words = 0;
   int prune_buf_cap = 0;            // LDS candidate buffer entries of the pruned pass
   size_t prune_lds = 0;             // dynamic LDS bytes of the pruned pass
   int64_t emit_blocks = 0;

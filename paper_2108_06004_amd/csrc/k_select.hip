@@ -516,6 +516,26 @@ __global__ void __launch_bounds__(kBlock) k_heavy(const float* __restrict__ merg
   }
 }
 
+// Coarse heavy-cell map: coarse word w covers fine words [w*G, w*G + G) (G = 2^log2g <= 32);
+// each fine word contributes 32/G bits, bit q set when any of its cells q*G .. q*G+G-1 is.
+__global__ void __launch_bounds__(kBlock) k_coarse(const uint32_t* __restrict__ fine, int64_t fine_words,
+                                                   int log2g, uint32_t* __restrict__ coarse, int64_t coarse_words) {
+  const int G = 1 << log2g;
+  const int per = 32 / G;  // coarse bits from one fine word
+  const uint32_t mask = G == 32 ? 0xffffffffu : ((1u << G) - 1u);
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t w = (int64_t)blockIdx.x * kBlock + threadIdx.x; w < coarse_words; w += stride) {
+    uint32_t out = 0u;
+    for (int f = 0; f < G; ++f) {
+      const int64_t fw = w * G + f;
+      const uint32_t x = fw < fine_words ? fine[fw] : 0u;
+      for (int q = 0; q < per; ++q)
+        if ((x >> (q * G)) & mask) out |= 1u << (f * per + q);
+    }
+    coarse[w] = out;
+  }
+}
+
 // The pruned pass, in two kernels.
 // k_pruned: every coordinate checks its r heavy bits (bitmap in LDS when it fits); the
 // survivors (ceil(r/2) heavy cells; for HEAVYMIX also every coordinate whose fill key
@@ -528,20 +548,25 @@ __global__ void __launch_bounds__(kBlock) k_heavy(const float* __restrict__ merg
 // dynamic LDS of k_pruned: [map words?][buf indices]
 constexpr int kPruneBlock = 1024;  // 16 waves per CU; the heavy bitmap fills the LDS
 
-template <int R, bool HM>
+// coarse_log2 > 0: `lmap` is the coarse map (one bit per 2^coarse_log2 cells, set when any
+// of them is heavy), kept in LDS; a set coarse bit is confirmed in the fine map `heavy` in
+// global memory, so the count is the same as with the fine map alone.
+template <int R, bool HM, bool COARSE>
 __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, SelectCtl* __restrict__ ctl,
-                                                   const uint32_t* __restrict__ heavy, int64_t map_words,
-                                                   int map_in_lds, int buf_cap, uint32_t* __restrict__ queue,
-                                                   uint32_t* __restrict__ bitmap, const uint32_t* __restrict__ rnd) {
+                                                   const uint32_t* __restrict__ heavy,
+                                                   const uint32_t* __restrict__ lmap, int64_t map_words,
+                                                   int map_in_lds, int coarse_log2, int buf_cap,
+                                                   uint32_t* __restrict__ queue, uint32_t* __restrict__ bitmap,
+                                                   const uint32_t* __restrict__ rnd) {
   constexpr int U = 4;  // coordinates per lane per pass: independent hash chains in flight
   extern __shared__ uint32_t sm[];
   __shared__ uint32_t bn, gbase;
-  const uint32_t* map = heavy;
+  const uint32_t* map = lmap;
   uint32_t* buf = sm;
   if (map_in_lds) {
     // map_words is even and the map 8-byte aligned: copy 16 bytes per lane, 8 loads in flight
     const int64_t n4 = map_words / 4;
-    const uint4* src = reinterpret_cast<const uint4*>(heavy);
+    const uint4* src = reinterpret_cast<const uint4*>(lmap);
     uint4* dst = reinterpret_cast<uint4*>(sm);
     int64_t w = threadIdx.x;
     for (; w + 7 * kPruneBlock < n4; w += 8 * kPruneBlock) {
@@ -552,7 +577,7 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
       for (int m = 0; m < 8; ++m) dst[w + m * kPruneBlock] = t[m];
     }
     for (; w < n4; w += kPruneBlock) dst[w] = src[w];
-    for (int64_t x = 4 * n4 + threadIdx.x; x < map_words; x += kPruneBlock) sm[x] = heavy[x];
+    for (int64_t x = 4 * n4 + threadIdx.x; x < map_words; x += kPruneBlock) sm[x] = lmap[x];
     map = sm;
     buf = sm + map_words;
   }
@@ -583,7 +608,12 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
         const uint32_t col = mod_c(hb[j][m], kr[j].c, kr[j].magic, kr[j].shift);
         hb[j][m] = add_mod_mersenne(hb[j][m], db[j]);
         const int64_t e = (int64_t)j * kr[j].c + col;
-        cnt += (map[e >> 5] >> (e & 31)) & 1u;
+        if constexpr (!COARSE) {
+          cnt += (map[e >> 5] >> (e & 31)) & 1u;
+        } else {
+          const int64_t cb = e >> coarse_log2;
+          if ((map[cb >> 5] >> (cb & 31)) & 1u) cnt += (heavy[e >> 5] >> (e & 31)) & 1u;
+        }
       }
       bool keep = i < d && cnt >= need;
       if constexpr (HM) keep = keep || (i < d && (rnd[i] >> 1) >= tau0);
@@ -929,8 +959,17 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
                      x->heavy, HM ? 1 : 0);
   // with the bitmap in LDS one block fits a CU: launch one per CU so the map is loaded once
   const int pgrid = grid_for(x->d, 4 * kPruneBlock, x->prune_map_in_lds ? x->num_cus : 2 * x->num_cus);
-  hipLaunchKernelGGL((k_pruned<R, HM>), dim3(pgrid), dim3(kPruneBlock), x->prune_lds, s, x->hs, x->d, x->ctl,
-                     x->heavy, x->prune_map_words, x->prune_map_in_lds, x->prune_buf_cap, x->keys, x->bitmap, rnd);
+  if (x->prune_coarse_log2 > 0)
+    hipLaunchKernelGGL(k_coarse, dim3(grid_for(x->prune_coarse_words, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s,
+                       x->heavy, (rc + 63) / 64 * 2, x->prune_coarse_log2, x->coarse, x->prune_coarse_words);
+  if (x->prune_coarse_log2 > 0)
+    hipLaunchKernelGGL((k_pruned<R, HM, true>), dim3(pgrid), dim3(kPruneBlock), x->prune_lds, s, x->hs, x->d,
+                       x->ctl, x->heavy, x->coarse, x->prune_map_words, x->prune_map_in_lds, x->prune_coarse_log2,
+                       x->prune_buf_cap, x->keys, x->bitmap, rnd);
+  else
+    hipLaunchKernelGGL((k_pruned<R, HM, false>), dim3(pgrid), dim3(kPruneBlock), x->prune_lds, s, x->hs, x->d,
+                       x->ctl, x->heavy, x->heavy, x->prune_map_words, x->prune_map_in_lds, 0, x->prune_buf_cap,
+                       x->keys, x->bitmap, rnd);
   hipLaunchKernelGGL((k_survivors<R, HM>), dim3(x->num_cus), dim3(kBlock), 0, s, x->hs, merged, x->ctl, x->keys,
                      x->cand_key, x->cand_idx, x->cand_cap, rnd);
   hipLaunchKernelGGL(k_cand_hist, dim3(grid_for(4 * k, kBlock, x->num_cus)), dim3(kBlock), 0, s, x->cand_key, x->ctl,
@@ -940,12 +979,15 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
 
 template <int R>
 hipError_t allow_prune_lds(size_t bytes) {
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pruned<R, false>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-  if (e == hipSuccess)
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pruned<R, true>),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-  return e;
+  const void* fns[] = {reinterpret_cast<const void*>(&k_pruned<R, false, false>),
+                       reinterpret_cast<const void*>(&k_pruned<R, true, false>),
+                       reinterpret_cast<const void*>(&k_pruned<R, false, true>),
+                       reinterpret_cast<const void*>(&k_pruned<R, true, true>)};
+  for (const void* f : fns) {
+    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // select1 -> compact -> select2 -> finalize -> emit over the keys in x->keys (digit-1
@@ -986,15 +1028,32 @@ hipError_t prepare_prune(gs_ctx* x) {
   const int64_t rc = (int64_t)x->r * x->c;
   const int64_t words = (rc + 63) / 64 * 2;
   const int64_t lds_max = 160 * 1024 - 256;
-  x->prune_map_words = words;
-  int64_t buf = (lds_max - words * 4) / 4;
+  // the fine map in LDS if it fits beside a 512-entry queue buffer; else the coarsest-needed
+  // coarse map (2 .. 32 cells per bit); else the fine map from global memory
+  int64_t map_words = words;
+  int log2g = 0;
+  while ((lds_max - map_words * 4) / 4 < 512 && log2g < 5) {
+    ++log2g;
+    map_words = (rc + (32ll << log2g) - 1) / (32ll << log2g);
+    map_words += map_words & 1;
+  }
+  int64_t buf = (lds_max - map_words * 4) / 4;
   if (buf > 8192) buf = 8192;
   if (buf >= 512) {
     x->prune_map_in_lds = 1;
+    x->prune_coarse_log2 = log2g;
+    x->prune_map_words = map_words;
     x->prune_buf_cap = (int)buf;
-    x->prune_lds = (size_t)(words * 4 + buf * 4);
+    x->prune_lds = (size_t)(map_words * 4 + buf * 4);
+    if (log2g > 0) {
+      x->prune_coarse_words = map_words;
+      const hipError_t e = hipMalloc(reinterpret_cast<void**>(&x->coarse), (size_t)map_words * sizeof(uint32_t));
+      if (e != hipSuccess) return e;
+    }
   } else {
     x->prune_map_in_lds = 0;
+    x->prune_coarse_log2 = 0;
+    x->prune_map_words = words;
     x->prune_buf_cap = 8192;
     x->prune_lds = 8192 * 4;
   }

@@ -307,6 +307,8 @@ EDGE = [
     (65_536, 2, 16, 4096, 655), # maximum r
     (20_000, 2, 3, 500, 19_999),  # k near d: the sampled pruning bound admits fewer than k
     (50_000, 3, 5, 300, 40_000),  # coordinates, so the unpruned selection takes over
+    (100_003, 1, 5, 2_000_003, 50),  # 10M cells: the pruned pass keeps a coarse map in LDS
+    (30_000, 1, 16, 3_000_000, 40),  # 48M cells: even the coarsest map exceeds LDS (global map)
 ]
 
 
