@@ -1,19 +1,24 @@
-// k_select.hip -- HEAVYMIX estimate and deterministic top-k selection (Alg. 2).
+// k_select.hip -- HEAVYMIX estimate and selection (Alg. 2): the deterministic top-k and
+// HEAVYMIX as printed.
 //
 // Estimate: est_i = median over rows of s_j(i) * S[j][h_j(i)] (register sorting network).
-// Selection: the k largest |est_i|, ties toward the lower index, output ascending. Keys are
-// the bit patterns of |est_i| (non-negative floats order like unsigned integers). The k-th
-// key is found by a most-significant-digit radix select entirely on the device (no host
-// synchronisation inside the call):
-//   1. unsketch: keys + histogram of digit 1 (key bits 31..20) in LDS, flushed to global;
-//   2. select1 (one block): the digit-1 bucket b1 holding the k-th key;
-//   3. compact: every key with digit 1 >= b1 is appended to a candidate list (wave ballot,
-//      one atomic per wave); the output bitmap is cleared on the way;
-//   4. select2 (one block): digits 2 and 3 over the candidates give the k-th key tau and how
-//      many keys equal to tau are taken; if not all of them, three index digits find the
-//      largest index iota taken among them (lowest indices win);
-//   5. finalize: candidates with key > tau, or key == tau and index <= iota, set their bit;
-//   6. emit: the bitmap is turned into ascending indices (per-block popcounts, then a
+// Selection: the k largest keys, ties toward the lower index, output ascending. For the
+// top-k the keys are the bit patterns of |est_i| (non-negative floats order like unsigned
+// integers); for HEAVYMIX, heavy coordinates get 0x80000000 | bits(|est_i|) and the others
+// their fill draw. The k-th key is found by a most-significant-digit radix select entirely
+// on the device (no host synchronisation inside the call):
+//   1. candidates: every key whose digit 1 (bits 31..20) is at least that of the k-th key,
+//      either from the pruned pass (sampled bound, heavy-cell bitmap, survivor estimates;
+//      k_sample .. k_survivors, then k_cand_hist / k_select1p) or from the full estimate
+//      (k_unsketch / k_unsketch_hm, k_select1, k_compact), which also runs whenever the
+//      pruned candidates fall short of k;
+//   2. k_digit2 (many blocks): digit 2 (bits 19..10) of the keys in the k-th key's digit-1
+//      bucket, and that bucket compacted;
+//   3. k_select2 (one block): digit 3 (bits 9..0) gives the k-th key tau and how many keys
+//      equal to tau are taken; if not all of them, three index digits find the largest
+//      index iota taken among them (lowest indices win);
+//   4. k_finalize: candidates with key > tau, or key == tau and index <= iota, set their bit;
+//   5. emit: the bitmap is turned into ascending indices (per-block popcounts, then a
 //      block-local scan offset by the preceding blocks' totals).
 #include <cmath>
 
@@ -96,7 +101,7 @@ __device__ void find_bucket(const uint32_t* h, int nbins, bool descending, uint3
 }
 
 // ------------------------------------------------------------------------------------
-// 1. Estimate (HEAVYMIX query) + keys + digit-1 histogram.
+// Step 1, full path: estimate (HEAVYMIX query) + keys + digit-1 histogram.
 
 template <int R>
 __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __restrict__ merged, int64_t d,
@@ -143,8 +148,8 @@ __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __
 }
 
 // ------------------------------------------------------------------------------------
-// 2. Digit-1 bucket of the k-th key. Clears the histogram for the next call and the
-// candidate counter for the compaction pass.
+// Step 1, full path: digit-1 bucket of the k-th key. Clears the histogram for the next
+// call and the candidate counter for the compaction pass.
 
 __global__ void __launch_bounds__(kSelBlock) k_select1(uint32_t* __restrict__ hist, SelectCtl* __restrict__ ctl,
                                                        uint32_t k, int gated) {
@@ -168,7 +173,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select1(uint32_t* __restrict__ hi
 }
 
 // ------------------------------------------------------------------------------------
-// 3. Candidate compaction (digit 1 >= b1) and bitmap clearing.
+// Step 1, full path: candidate compaction (digit 1 >= b1) and bitmap clearing.
 
 // Each block scans a contiguous range of keys and collects its candidates in an LDS buffer
 // (one LDS atomic per wave), flushing it to the global list with a single global atomic
@@ -249,14 +254,14 @@ __global__ void __launch_bounds__(kBlock) k_compact(const uint32_t* __restrict__
 }
 
 // ------------------------------------------------------------------------------------
-// 4. Digits 2 and 3 of the k-th key, then the index cut among equal keys.
+// Steps 2 and 3: digits 2 and 3 of the k-th key, then the index cut among equal keys.
 
 constexpr int kSelUnroll = 8;    // candidate loads in flight per thread
 constexpr int kStageBuf = 4096;  // per-block LDS buffer of k_digit2
 
-// 4a. Digit 2 of the keys in bucket b1 (many blocks): the digit-2 histogram (LDS per block,
-// added into hist2) and the bucket's keys compacted into stage2 for the digit-3 pass (an
-// LDS buffer per block, one global atomic per flush).
+// Step 2: digit 2 of the keys in bucket b1 (many blocks): the digit-2 histogram (LDS per
+// block, added into hist2) and the bucket's keys compacted into stage2 for the digit-3
+// pass (an LDS buffer per block, one global atomic per flush).
 __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ cand_key,
                                                    SelectCtl* __restrict__ ctl, int64_t cap,
                                                    uint32_t* __restrict__ hist2, uint32_t* __restrict__ stage2) {
@@ -308,7 +313,7 @@ __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ 
   }
 }
 
-// 4b. Digits 2 and 3 of the k-th key, then the index cut among equal keys (one block).
+// Step 3: the digit-2 bucket from the histogram, digit 3 and the index cut (one block).
 __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restrict__ cand_key,
                                                        const int32_t* __restrict__ cand_idx,
                                                        SelectCtl* __restrict__ ctl, int64_t cap,
@@ -401,7 +406,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
 }
 
 // ------------------------------------------------------------------------------------
-// 5. Mark the selected candidates.
+// Step 4: mark the selected candidates.
 
 __global__ void __launch_bounds__(kBlock) k_finalize(const uint32_t* __restrict__ cand_key,
                                                      const int32_t* __restrict__ cand_idx,
@@ -760,7 +765,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select1p(uint32_t* __restrict__ h
 }
 
 // ------------------------------------------------------------------------------------
-// 6. Bitmap -> ascending index list.
+// Step 5: bitmap -> ascending index list.
 
 __global__ void __launch_bounds__(kSelBlock) k_emit_count(const uint32_t* __restrict__ bitmap, int64_t words,
                                                           uint32_t* __restrict__ blockcnt) {
