@@ -167,6 +167,13 @@ gs_status gs_step_heavymix(gs_ctx* ctx, void* stream, const float* g, float* u, 
 gs_status gs_step_sketch_momentum(gs_ctx* ctx, void* stream, const float* g, float* U, float* E, int64_t k,
                                   float* merged, int32_t* idx, float* values);
 
+/* The weight update (Alg. 1, last step): w <- w - lr * G~, with G~ zero outside the
+ * selection: for t < k, w[idx[t]] = fl(w[idx[t]] - fl(lr * values[t])) (no fused
+ * multiply-add). idx: [k] distinct coordinates in [0, d) (e.g. from gs_step). values: [k].
+ * w: [d] parameters, updated in place. lr finite. 1 <= k <= k_max. */
+gs_status gs_apply_update(gs_ctx* ctx, void* stream, const int32_t* idx, const float* values, int64_t k, float lr,
+                          float* w);
+
 /* Stage timing for benchmarks and profiling. Runs exactly the kernels of gs_step, records a
  * HIP event on `stream` before the first stage and after each stage, synchronizes the stream
  * and writes the stage durations in milliseconds to the HOST array stage_ms[GS_NUM_STAGES]:

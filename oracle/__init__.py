@@ -59,6 +59,9 @@ def _load():
         "ora_heavy_count": (i64, [i64, i64, vp, f64]),
         "ora_row_sq_sum": (f64, [i64, vp]),
         "ora_heavymix": (ctypes.c_int, [i64, i32, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+        "ora_apply_update": (ctypes.c_int, [i64, i64, vp, vp, f32, vp]),
+        "ora_sketch_state_update": (ctypes.c_int, [i64, i32, i64, i64, f32, i32, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                   vp, vp]),
         "ora_sketch_momentum_step": (ctypes.c_int, [i32, i64, i32, i64, i64, f32, i32, vp, vp, vp, vp, vp, vp, vp,
                                                     vp, vp, vp, vp]),
         "ora_step": (ctypes.c_int, [i32, i64, i32, i64, i64, f32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp,
@@ -261,6 +264,29 @@ def sketch_momentum_step(g, U, E, hp: dict, k: int, rho: float = 0.9, reset_mome
                                             _p(b2), _p(g), _p(U), _p(E), _p(merged), _p(est), _p(idx), _p(values)),
            "sketch_momentum_step")
     return {"merged": merged, "idx": idx, "values": values, "est": est}
+
+
+def apply_update(w: np.ndarray, idx, values, lr: float) -> None:
+    """w[idx] -= lr * values (fp32, each operation rounded), in place."""
+    assert w.dtype == np.float32 and w.flags.c_contiguous
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    values = _f32(values)
+    _check(_load().ora_apply_update(w.size, idx.size, _p(idx), _p(values), lr, _p(w)), "apply_update")
+
+
+def sketch_state_update(merged, U, E, hp: dict, d: int, k: int, rho: float = 0.9,
+                        reset_momentum: bool = True) -> dict:
+    """The sketch-space step after the merge, from a given merged sketch S ([r][c])."""
+    merged = _f32(merged)
+    a, b, a2, b2 = _hp(hp)
+    r, c = merged.shape
+    assert U.shape == E.shape == (r, c) and U.flags.c_contiguous and E.flags.c_contiguous
+    idx = np.empty(k, dtype=np.int32)
+    values = np.empty(k, dtype=np.float32)
+    _check(_load().ora_sketch_state_update(d, r, c, k, rho, int(bool(reset_momentum)), _p(a), _p(b), _p(a2), _p(b2),
+                                           _p(merged), _p(U), _p(E), None, _p(idx), _p(values)),
+           "sketch_state_update")
+    return {"idx": idx, "values": values}
 
 
 def step(g, u, v, hp: dict, c: int, k: int, rho: float = 0.9, reset_momentum: bool = True,

@@ -429,6 +429,20 @@ int ora_heavymix(int64_t d, int32_t r, int64_t c, int64_t k, const uint32_t* ha,
 }
 
 /* ---------------------------------------------------------------------------------- */
+/* The weight update (Alg. 1, last step): w <- w - eta * G~, where G~ is zero outside Top_k
+ * and holds the selected values there: w[idx[t]] = fl(w[idx[t]] - fl(eta * values[t])). */
+
+int ora_apply_update(int64_t d, int64_t k, const int32_t* idx, const float* values, float lr, float* w) {
+  for (int64_t t = 0; t < k; ++t) {
+    const int64_t i = idx[t];
+    if (i < 0 || i >= d) return 1;
+    const float step = lr * values[t];
+    w[i] = w[i] - step;
+  }
+  return 0;
+}
+
+/* ---------------------------------------------------------------------------------- */
 /* Momentum and error accumulation kept in the sketch (the sketch is linear, so both can be
  * carried inside it: Sec. II, sketching paragraph, after FetchSGD). One step:
  *   S = tree-order merge of the P workers' sketches of g          (Alg. 1 sketch + reduction)
@@ -438,20 +452,17 @@ int ora_heavymix(int64_t d, int32_t r, int64_t c, int64_t k, const uint32_t* ha,
  *   E <- fl(E - D) on every cell D touches, where D = S(Delta) is the sketch of the sparse
  *        selection, each touched cell summed in fp64 and rounded once to fp32
  *   U <- 0 on those cells when reset_momentum (momentum masking)
- * U and E are [r][c], updated in place; merged ([r][c]) receives S; est ([d]) may be NULL. */
+ * U and E are [r][c], updated in place; merged ([r][c]) receives S; est ([d]) may be NULL.
+ * ora_sketch_state_update is the part after the merge, from a given S. */
 
-int ora_sketch_momentum_step(int32_t P, int64_t d, int32_t r, int64_t c, int64_t k, float rho,
-                             int32_t reset_momentum, const uint32_t* ha, const uint32_t* hb, const uint32_t* sa,
-                             const uint32_t* sb, const float* g, float* U, float* E, float* merged, float* est,
-                             int32_t* idx, float* values) {
+int ora_sketch_state_update(int64_t d, int32_t r, int64_t c, int64_t k, float rho, int32_t reset_momentum,
+                            const uint32_t* ha, const uint32_t* hb, const uint32_t* sa, const uint32_t* sb,
+                            const float* merged, float* U, float* E, float* est, int32_t* idx, float* values) {
   const int64_t rc = (int64_t)r * c;
-  float* tb = (float*)malloc((size_t)P * (size_t)rc * sizeof(float));
   float* es = est ? est : (float*)malloc((size_t)d * sizeof(float));
   double* acc = (double*)calloc((size_t)rc, sizeof(double));
   unsigned char* touched = (unsigned char*)calloc((size_t)rc, 1);
-  int rc_ = (!tb || !es || !acc || !touched) ? 1 : 0;
-  if (!rc_) rc_ = ora_sketch(P, d, r, c, ha, hb, sa, sb, g, tb);
-  if (!rc_) rc_ = ora_merge(P, rc, tb, merged);
+  int rc_ = (!es || !acc || !touched) ? 1 : 0;
   if (!rc_) {
     for (int64_t e = 0; e < rc; ++e) {
       float m = rho * U[e];
@@ -477,10 +488,24 @@ int ora_sketch_momentum_step(int32_t P, int64_t d, int32_t r, int64_t c, int64_t
       if (reset_momentum) U[e] = 0.0f;
     }
   }
-  free(tb);
   if (!est) free(es);
   free(acc);
   free(touched);
+  return rc_;
+}
+
+int ora_sketch_momentum_step(int32_t P, int64_t d, int32_t r, int64_t c, int64_t k, float rho,
+                             int32_t reset_momentum, const uint32_t* ha, const uint32_t* hb, const uint32_t* sa,
+                             const uint32_t* sb, const float* g, float* U, float* E, float* merged, float* est,
+                             int32_t* idx, float* values) {
+  const int64_t rc = (int64_t)r * c;
+  float* tb = (float*)malloc((size_t)P * (size_t)rc * sizeof(float));
+  int rc_ = tb ? 0 : 1;
+  if (!rc_) rc_ = ora_sketch(P, d, r, c, ha, hb, sa, sb, g, tb);
+  if (!rc_) rc_ = ora_merge(P, rc, tb, merged);
+  if (!rc_) rc_ = ora_sketch_state_update(d, r, c, k, rho, reset_momentum, ha, hb, sa, sb, merged, U, E, est, idx,
+                                          values);
+  free(tb);
   return rc_;
 }
 

@@ -24,7 +24,7 @@ GS_MAX_WORKERS = 64
 GS_MAX_ROWS = 16
 EXPORTED = ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
             "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_sketch_momentum",
-            "gs_step_profiled", "gs_status_string", "gs_last_error")
+            "gs_apply_update", "gs_step_profiled", "gs_status_string", "gs_last_error")
 GS_NUM_STAGES = 5
 STAGES = ("accumulate", "sketch", "merge", "select", "gather_reset")
 
@@ -79,9 +79,10 @@ def load_library():
     lib.gs_heavymix_topk.argtypes = [vp, vp, vp, i64, vp, vp, vp, vp, vp]
     lib.gs_step_heavymix.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp]
     lib.gs_step_sketch_momentum.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp]
+    lib.gs_apply_update.argtypes = [vp, vp, vp, vp, i64, ctypes.c_float, vp]
     for name in ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
                  "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_sketch_momentum",
-                 "gs_step_profiled"):
+                 "gs_apply_update", "gs_step_profiled"):
         getattr(lib, name).restype = st
     lib.gs_status_string.argtypes = [st]
     lib.gs_status_string.restype = ctypes.c_char_p
@@ -193,6 +194,11 @@ def gs_step_sketch_momentum(ctx: int, g, U, E, k: int, merged, idx, values, stre
                                                   _ptr(E, name="E"), k, _ptr(merged, name="merged"),
                                                   _ptr(idx, name="idx"), _ptr(values, name="values")),
            ctx, "gs_step_sketch_momentum")
+
+
+def gs_apply_update(ctx: int, idx, values, k: int, lr: float, w, stream=None) -> None:
+    _check(load_library().gs_apply_update(ctx, _stream(stream), _ptr(idx, name="idx"), _ptr(values, name="values"),
+                                          k, lr, _ptr(w, name="w")), ctx, "gs_apply_update")
 
 
 def gs_step_profiled(ctx: int, g, u, v, k: int, merged, idx, values, stream=None) -> dict:
@@ -308,6 +314,16 @@ class GsContext:
         gs_step_sketch_momentum(self.handle, self._f32(g, self.P * self.d, "g"), self._f32(U, rc, "U"),
                                 self._f32(E, rc, "E"), k, self._f32(merged, rc, "merged"), idx,
                                 self._f32(values, k, "values"), stream)
+
+    def apply_update(self, idx, values, k, lr, w, stream=None):
+        """w[idx] -= lr * values (fp32, no fused multiply-add); w: [d] fp32 parameters."""
+        import torch
+
+        _ptr(idx, torch.int32, None, "idx")
+        if idx.numel() < k or values.numel() < k:
+            raise ValueError("idx and values need at least k elements")
+        _ptr(values, torch.float32, None, "values")
+        gs_apply_update(self.handle, idx, values, k, lr, self._f32(w, self.d, "w"), stream)
 
     def step_profiled(self, g, u, v, k, merged, idx, values, stream=None) -> dict:
         import torch

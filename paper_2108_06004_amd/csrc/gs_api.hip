@@ -330,6 +330,16 @@ gs_status gs_step_sketch_momentum(gs_ctx* x, void* stream, const float* g, float
   return device_status(x, e, "gs_step_sketch_momentum");
 }
 
+gs_status gs_apply_update(gs_ctx* x, void* stream, const int32_t* idx, const float* values, int64_t k, float lr,
+                          float* w) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!idx || !values || !w) return fail(x, GS_ERR_INVALID_ARG, "gs_apply_update: NULL array");
+  if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_apply_update: k must satisfy 1 <= k <= k_max");
+  if (!std::isfinite(lr)) return fail(x, GS_ERR_INVALID_ARG, "gs_apply_update: lr must be finite");
+  return device_status(x, gs::launch_apply_update(x, as_stream(stream), idx, values, k, lr, w), "gs_apply_update");
+}
+
 gs_status gs_step_profiled(gs_ctx* x, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
                            int32_t* idx, float* values, float* stage_ms) {
   if (!x) return GS_ERR_INVALID_ARG;

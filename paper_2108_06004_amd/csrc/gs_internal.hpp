@@ -104,6 +104,8 @@ hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, i
 hipError_t launch_heavymix_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, const uint32_t* rnd,
                                 float* est, int32_t* idx, int64_t* n_heavy, double* l2sq);
 int64_t l2_pad(int64_t c);
+hipError_t launch_apply_update(const gs_ctx* x, hipStream_t s, const int32_t* idx, const float* values, int64_t k,
+                               float lr, float* w);
 hipError_t launch_sketch_state(gs_ctx* x, hipStream_t s, const float* merged, float* U, float* E, int64_t k,
                                int32_t* idx, float* values);
 hipError_t launch_gather_reset(const gs_ctx* x, hipStream_t s, const int32_t* idx, int64_t k, float* u, float* v,

@@ -183,6 +183,19 @@ __global__ void __launch_bounds__(kBlock) k_gather_reset_dyn(const int32_t* __re
   }
 }
 
+// Weight update of the selected coordinates (Alg. 1, last step): w[idx[t]] -= lr * values[t],
+// the product and the difference each rounded (no fused multiply-add).
+__global__ void __launch_bounds__(kBlock) k_apply_update(const int32_t* __restrict__ idx,
+                                                         const float* __restrict__ values, int64_t k, float lr,
+                                                         float* __restrict__ w) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < k; t += stride) {
+    const int64_t i = idx[t];
+    const float step = lr * values[t];
+    w[i] = w[i] - step;
+  }
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------------------------
@@ -273,6 +286,13 @@ hipError_t launch_gather_reset(const gs_ctx* x, hipStream_t s, const int32_t* id
 #undef GS_GATHER_CASE
     default: hipLaunchKernelGGL(k_gather_reset_dyn, grid, block, 0, s, idx, k, u, v, values, x->d, ru, x->P); break;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_apply_update(const gs_ctx* x, hipStream_t s, const int32_t* idx, const float* values, int64_t k,
+                               float lr, float* w) {
+  hipLaunchKernelGGL(k_apply_update, dim3(grid_for(k, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, idx, values, k, lr,
+                     w);
   return hipGetLastError();
 }
 

@@ -1,0 +1,86 @@
+"""The training integration on the GPU: the weight update against the oracle, and
+convergence of a noisy quadratic with the paper's warm-up schedule (needs an MI355X)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+gs = pytest.importorskip("paper_2108_06004_amd")
+from paper_2108_06004_amd.train import DensitySchedule, GlobalSketchSGD  # noqa: E402
+
+DEV = "cuda:0"
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def test_apply_update_matches_oracle():
+    d, k = 100_003, 5_000
+    hp = synth.hash_params(synth.BASE_SEED + 91, 3)
+    ctx = gs.GsContext(d, 2, 3, 1000, k, hp)
+    rng = np.random.default_rng(91)
+    w = rng.standard_normal(d).astype(np.float32)
+    idx = np.sort(rng.choice(d, k, replace=False)).astype(np.int32)
+    vals = rng.standard_normal(k).astype(np.float32)
+    w_d = torch.from_numpy(w.copy()).to(DEV)
+    ctx.apply_update(torch.from_numpy(idx).to(DEV), torch.from_numpy(vals).to(DEV), k, 0.037, w_d)
+    oracle.apply_update(w, idx, vals, 0.037)
+    assert np.array_equal(host(w_d), w)
+    ctx.close()
+
+
+def run_quadratic(opt, wstar, P, d, steps, noise, epoch_len, rng):
+    w = torch.zeros(d, dtype=torch.float32, device=DEV)
+    loss0 = 0.5 * float(torch.sum((w - wstar) ** 2))
+    for t in range(steps):
+        g = ((w - wstar).unsqueeze(0) +
+             torch.from_numpy((noise * rng.standard_normal((P, d))).astype(np.float32)).to(DEV)).contiguous()
+        w_before = host(w).copy()
+        info = opt.step(g, w, epoch=t // epoch_len)
+        k = info["k"]
+        # the update touched exactly the selection, by fl(w - fl(lr/P * value))
+        want = w_before.copy()
+        oracle.apply_update(want, host(opt.idx)[:k], host(opt.values)[:k], info["lr"] / P)
+        assert np.array_equal(host(w), want), t
+    return 0.5 * float(torch.sum((w - wstar) ** 2)) / loss0
+
+
+@pytest.mark.parametrize("selection,state", [("topk", "vector"), ("heavymix", "vector"), ("topk", "sketch")])
+def test_sparse_optimum_converges(selection, state):
+    # f(w) = |w - w*|^2 / 2 with 200 nonzero coordinates in w* (the gradients have heavy
+    # hitters, which the sketch recovers), noise N(0, 0.01^2) per worker, density 0.4%
+    d, P, r, c = 65_536, 4, 5, 8192
+    hp = synth.hash_params(synth.BASE_SEED + 90, r)
+    rng = np.random.default_rng(92)
+    wstar = np.zeros(d, np.float32)
+    wstar[rng.choice(d, 200, replace=False)] = 3 * rng.standard_normal(200).astype(np.float32)
+    opt = GlobalSketchSGD(d, P, r, c, hp, DensitySchedule(0.004, 0.1), rho=0.5, selection=selection, state=state,
+                          seed=6)
+    rel = run_quadratic(opt, torch.from_numpy(wstar).to(DEV), P, d, 40, 0.01, 1000, rng)
+    print(f"{selection}/{state}: loss {rel:.4f} of the initial", flush=True)
+    assert rel < 0.01
+    opt.close()
+
+
+@pytest.mark.parametrize("selection", ["topk", "heavymix"])
+def test_noisy_quadratic_converges_with_warmup(selection):
+    # a dense optimum (no heavy hitters): only the vector-space state, whose values are exact,
+    # descends here; the sketch-space state applies sketch estimates and needs heavy hitters
+    # f(w) = |w - w*|^2 / 2, each worker's gradient (w - w*) plus N(0, 0.1^2) noise; warm-up
+    # densities 0.25, 0.0725, 0.015, 0.004 for 10 steps each, then 0.001 (Sec. IV)
+    d, P, r, c = 65_536, 4, 5, 8192
+    hp = synth.hash_params(synth.BASE_SEED + 90, r)
+    sched = DensitySchedule(0.001, 0.1, [(0.25, 0.1), (0.0725, 0.03), (0.015, 0.01), (0.004, 0.01)])
+    opt = GlobalSketchSGD(d, P, r, c, hp, sched, rho=0.5, selection=selection, seed=5)
+    rng = np.random.default_rng(90)
+    wstar = torch.from_numpy(rng.standard_normal(d).astype(np.float32)).to(DEV)
+    rel = run_quadratic(opt, wstar, P, d, 40, 0.1, 10, rng)
+    print(f"{selection}/vector with warm-up: loss {rel:.3f} of the initial", flush=True)
+    assert rel < 0.3
+    opt.close()

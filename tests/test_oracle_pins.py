@@ -688,3 +688,37 @@ def test_sketch_momentum_subtracts_the_selection_sketch_worked_example():
     res = oracle.sketch_momentum_step(np.array([[1.0, 2.0]], np.float32), U, E, hp, 2, rho=0.0)
     assert res["merged"][0, 0] == 3.0 and res["values"].tolist() == [3.0, 3.0]
     assert E[0, 0] == -3.0 and U[0, 0] == 0.0
+
+
+# ---------------------------------------------------------------------------------------
+# Weight update (Alg. 1, last step)
+
+def test_apply_update_closed_forms():
+    d = 1000
+    idx = np.array([3, 17, 999], np.int32)
+    vals = np.array([0.5, -2.0, 3.25], np.float32)
+    w = np.zeros(d, np.float32)
+    oracle.apply_update(w, idx, vals, 1.0)  # eta = 1 from zero: w = -G~ exactly
+    want = np.zeros(d, np.float32)
+    want[idx] = -vals
+    assert np.array_equal(w, want)
+    w2 = np.full(d, 1.0, np.float32)
+    oracle.apply_update(w2, idx, vals, 0.25)  # dyadic: exact
+    want2 = np.full(d, 1.0, np.float32)
+    want2[idx] = [1.0 - 0.125, 1.5, 1.0 - 0.8125]
+    assert np.array_equal(w2, want2)
+
+
+def test_apply_update_rounds_the_product_then_the_difference():
+    # fl(w - fl(eta * x)) differs from a fused multiply-subtract on some inputs
+    rng = np.random.default_rng(71)
+    d = 100_000
+    w = rng.standard_normal(d).astype(np.float32)
+    x = rng.standard_normal(d).astype(np.float32)
+    idx = np.arange(d, dtype=np.int32)
+    w1 = w.copy()
+    oracle.apply_update(w1, idx, x, 0.1)
+    two_step = (w - (np.float32(0.1) * x).astype(np.float32)).astype(np.float32)
+    assert np.array_equal(w1, two_step)
+    fused = (w.astype(np.float64) - np.float64(np.float32(0.1)) * x.astype(np.float64)).astype(np.float32)
+    assert np.count_nonzero(fused != w1) > 100
