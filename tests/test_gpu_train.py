@@ -84,3 +84,17 @@ def test_noisy_quadratic_converges_with_warmup(selection):
     print(f"{selection}/vector with warm-up: loss {rel:.3f} of the initial", flush=True)
     assert rel < 0.3
     opt.close()
+
+
+def test_apply_update_rejects_invalid_arguments():
+    hp = synth.hash_params(synth.BASE_SEED + 93, 3)
+    ctx = gs.GsContext(1000, 2, 3, 100, 10, hp)
+    idx = torch.arange(10, dtype=torch.int32, device=DEV)
+    vals = torch.ones(10, dtype=torch.float32, device=DEV)
+    w = torch.zeros(1000, dtype=torch.float32, device=DEV)
+    for k, lr in ((11, 0.1), (0, 0.1), (10, float("nan")), (10, float("inf"))):
+        with pytest.raises(gs.GsError) as e:
+            gs.gs_apply_update(ctx.handle, idx, vals, k, lr, w)
+        assert e.value.status == gs.GS_ERR_INVALID_ARG
+    assert not host(w).any()
+    ctx.close()
