@@ -9,8 +9,9 @@ Prints one JSON line with
   value        gradient coordinates per second, P*d / (mean time per step over the timed steps);
                the median and minimum step times are reported beside it
   copy_frac    algorithmic GB/s as a fraction of a plain device copy timed in the same run
-  roofline     the dominant stage's algorithmic bytes / its mean duration (HIP events on
-               the stream the kernels run on) against MI355X's 8 TB/s HBM peak
+  roofline     the dominant stage's algorithmic bytes / its mean duration (HIP events the
+               library records between the stages of the timed steps, on the stream the
+               kernels run on) against MI355X's 8 TB/s HBM peak
   cpu_baseline the plain CPU oracle (single thread) timed on a bounded sample
 Algorithmic bytes per step: B = 20*P*d + 8*P*r*c + 8*r*c + 12*P*k + 8*k (vector state); with
 --state sketch (momentum and error kept in the sketch) B = 4*P*d + 8*P*r*c + 28*r*c + 8*k.
@@ -35,9 +36,17 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "gradient coords/sec per full sketch+unsketch+top-k step; % of HBM peak"
 
 
-def stage_bytes(w) -> dict:
+def stage_bytes(w, state: str = "vector") -> dict:
     """Algorithmic bytes each stage must move (not what an implementation happens to move)."""
     P, d, r, c, k = w.P, w.d, w.r, w.c, w.k
+    if state == "sketch":
+        return {
+            "interleave": 0,                      # implementation only (g is read by the sketch)
+            "sketch": 4 * P * d + 4 * P * r * c,  # read g, write the P tables
+            "merge": 4 * P * r * c + 4 * r * c,   # read the P tables, write the merged one
+            "select": 4 * r * c + 16 * r * c + 4 * r * c + 4 * k,  # read S; U, E read+written; E read
+            "state_update": 8 * k,                # values and the correction of touched cells
+        }
     return {
         "accumulate": 20 * P * d,            # read g, u, v; write u, v
         "sketch": 4 * P * d + 4 * P * r * c, # read v, write the P tables (v is not re-read once fused)
@@ -85,8 +94,8 @@ def measured_traffic(w, stage: str):
     if not m or m.group(1) != kernel_source_digest():
         return None
     table = {name.strip(): float(val) for name, val in re.findall(r"traffic: (.+?) \| ([0-9.]+)", text)}
-    names = stage_kernels(w)[stage]
-    if not all(n in table for n in names):
+    names = stage_kernels(w).get(stage)
+    if not names or not all(n in table for n in names):
         return None
     return sum(table[n] for n in names)
 
@@ -124,7 +133,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="laplace53-d25.6M-P8")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile-steps", type=int, default=None, help="steps of the per-stage timing pass")
+    ap.add_argument("--profile-steps", type=int, default=None,
+                    help="timed steps that also record stage events (default: all; 0: none)")
     ap.add_argument("--selection", choices=("topk", "heavymix"), default="topk",
                     help="topk: deterministic top-k by |estimate| (gs_step); heavymix: HEAVYMIX as printed with a "
                          "seeded random fill (gs_step_heavymix)")
@@ -190,10 +200,15 @@ def main():
         run_step(s)
     torch.cuda.synchronize()
 
-    log(f"[bench] timing {args.steps} steps")
+    # the timed region: stage events are recorded by the library inside the timed steps (on
+    # the stream the kernels run on, without synchronizing), step events by torch around them
+    nprof = min(args.steps, args.profile_steps if args.profile_steps is not None else args.steps)
+    log(f"[bench] timing {args.steps} steps (stage events in the first {nprof})")
     stream = torch.cuda.current_stream()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
+    if nprof > 0:
+        ctx.timing_start(nprof)
     wall0 = time.perf_counter()
     ev[0].record(stream)
     for s in range(args.steps):
@@ -205,23 +220,15 @@ def main():
     per_step = sorted(ev[s].elapsed_time(ev[s + 1]) for s in range(args.steps))
     ms_median = per_step[len(per_step) // 2] if len(per_step) % 2 else \
         0.5 * (per_step[len(per_step) // 2 - 1] + per_step[len(per_step) // 2])
-
-    # per-stage timing pass: the same kernels, events between stages on the same stream (always
-    # the deterministic selection's step: the first three stages are the same kernels either way)
-    nprof = args.profile_steps if args.profile_steps is not None else args.steps
-    log(f"[bench] per-stage timing over {nprof} steps")
-    acc = {st: 0.0 for st in gs.STAGES}
-    for s in range(nprof):
-        st_ms = ctx.step_profiled(g_dev[s % nb], u, v, w.k, merged, idx, vals)
-        for key in acc:
-            acc[key] += st_ms[key]
-    stage_ms = {key: val / max(nprof, 1) for key, val in acc.items()}
-    sb = stage_bytes(w)
-    # the fused design folds the sketch into the accumulate stage
-    if stage_ms["sketch"] == 0.0:
-        sb["accumulate"] += sb.pop("sketch") - 4 * w.P * w.d
-        stage_ms.pop("sketch")
-    dom = max(stage_ms, key=lambda s_: stage_ms[s_])
+    if nprof > 0:
+        stage_ms, n_timed = ctx.timing_stop()
+    else:
+        stage_ms, n_timed = {st: 0.0 for st in gs.STAGES}, 0
+    if args.state == "sketch":  # stages of the sketch-space step
+        stage_ms = {"interleave": stage_ms["accumulate"], "sketch": stage_ms["sketch"], "merge": stage_ms["merge"],
+                    "select": stage_ms["select"], "state_update": stage_ms["gather_reset"]}
+    sb = stage_bytes(w, args.state)
+    dom = max(stage_ms, key=lambda s_: stage_ms[s_]) if n_timed else "sketch"
     achieved = sb[dom] / (stage_ms[dom] * 1e-3) / 1e9 if stage_ms[dom] > 0 else 0.0
     ctx.close()
 
@@ -272,8 +279,8 @@ def main():
         "copy_frac": B / t / 1e9 / copy_gbs,
         "wall_s_timed": wall,
         "stage_ms": stage_ms,
-        "stage_ms_from": "gs_step_profiled (deterministic top-k selection)",
-        "roofline": {"bound": "hbm", "kernel": " + ".join(stage_kernels(w)[dom]), "stage": dom,
+        "stage_ms_from": f"HIP events recorded between the stages of the first {n_timed} timed steps",
+        "roofline": {"bound": "hbm", "kernel": " + ".join(stage_kernels(w).get(dom, [dom])), "stage": dom,
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(w, dom), "traffic_unit": "bytes per launch",
                      "bytes_per_launch": sb[dom], "mean_ms": stage_ms[dom]},

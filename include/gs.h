@@ -184,6 +184,19 @@ gs_status gs_apply_update(gs_ctx* ctx, void* stream, const int32_t* idx, const f
 gs_status gs_step_profiled(gs_ctx* ctx, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
                            int32_t* idx, float* values, float* stage_ms);
 
+/* Stage timing over ordinary steps (for benchmarks). gs_timing_start allocates
+ * max_steps * (GS_NUM_STAGES + 1) HIP events; while it is active, each of the next max_steps
+ * calls of gs_step, gs_step_heavymix or gs_step_sketch_momentum records one event on its
+ * stream before its first stage and one after each stage, without synchronizing (stages as
+ * for gs_step_profiled; for gs_step_sketch_momentum [0] is the gradient interleave and [4]
+ * the estimate correction of the sketch-space state). gs_timing_stop synchronizes, writes the
+ * mean stage durations in milliseconds to the HOST array stage_ms[GS_NUM_STAGES] (may be
+ * NULL) and the number of timed steps to *n_steps (may be NULL), and frees the events.
+ * 1 <= max_steps <= 2^20; starting while active, or stopping while not, is
+ * GS_ERR_INVALID_ARG. The calls of one context must come from one host thread. */
+gs_status gs_timing_start(gs_ctx* ctx, int32_t max_steps);
+gs_status gs_timing_stop(gs_ctx* ctx, float* stage_ms, int32_t* n_steps);
+
 /* Static description of a status code. */
 const char* gs_status_string(gs_status status);
 

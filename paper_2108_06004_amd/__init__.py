@@ -24,7 +24,8 @@ GS_MAX_WORKERS = 64
 GS_MAX_ROWS = 16
 EXPORTED = ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
             "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_sketch_momentum",
-            "gs_apply_update", "gs_step_profiled", "gs_status_string", "gs_last_error")
+            "gs_apply_update", "gs_step_profiled", "gs_timing_start", "gs_timing_stop", "gs_status_string",
+            "gs_last_error")
 GS_NUM_STAGES = 5
 STAGES = ("accumulate", "sketch", "merge", "select", "gather_reset")
 
@@ -80,9 +81,11 @@ def load_library():
     lib.gs_step_heavymix.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp, vp, vp]
     lib.gs_step_sketch_momentum.argtypes = [vp, vp, vp, vp, vp, i64, vp, vp, vp]
     lib.gs_apply_update.argtypes = [vp, vp, vp, vp, i64, ctypes.c_float, vp]
+    lib.gs_timing_start.argtypes = [vp, ctypes.c_int32]
+    lib.gs_timing_stop.argtypes = [vp, vp, vp]
     for name in ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
                  "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_sketch_momentum",
-                 "gs_apply_update", "gs_step_profiled"):
+                 "gs_apply_update", "gs_step_profiled", "gs_timing_start", "gs_timing_stop"):
         getattr(lib, name).restype = st
     lib.gs_status_string.argtypes = [st]
     lib.gs_status_string.restype = ctypes.c_char_p
@@ -324,6 +327,17 @@ class GsContext:
             raise ValueError("idx and values need at least k elements")
         _ptr(values, torch.float32, None, "values")
         gs_apply_update(self.handle, idx, values, k, lr, self._f32(w, self.d, "w"), stream)
+
+    def timing_start(self, max_steps: int) -> None:
+        """Record stage events inside the next max_steps fused steps (no synchronization)."""
+        _check(load_library().gs_timing_start(self.handle, max_steps), self.handle, "gs_timing_start")
+
+    def timing_stop(self) -> tuple[dict, int]:
+        """(stage -> mean ms over the timed steps, number of timed steps); synchronizes."""
+        ms = (ctypes.c_float * GS_NUM_STAGES)()
+        n = ctypes.c_int32(0)
+        _check(load_library().gs_timing_stop(self.handle, ms, ctypes.byref(n)), self.handle, "gs_timing_stop")
+        return dict(zip(STAGES, [float(x) for x in ms])), int(n.value)
 
     def step_profiled(self, g, u, v, k, merged, idx, values, stream=None) -> dict:
         import torch

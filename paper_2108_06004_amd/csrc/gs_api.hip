@@ -78,6 +78,14 @@ hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 }  // namespace
 
+namespace gs {
+void stage_mark(gs_ctx* x, hipStream_t s, int t) {
+  if (!x->timing || x->t_step >= x->t_max) return;
+  (void)hipEventRecord(x->t_events[(int64_t)x->t_step * kStageMarks + t], s);
+  if (t == kStageMarks - 1) ++x->t_step;
+}
+}  // namespace gs
+
 extern "C" {
 
 const char* gs_status_string(gs_status st) {
@@ -204,6 +212,11 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
 gs_status gs_destroy(gs_ctx* x) {
   if (!x) return GS_OK;
   hipError_t e = hipDeviceSynchronize();
+  if (x->t_events) {
+    for (int64_t t = 0; t < (int64_t)x->t_max * gs::kStageMarks; ++t) (void)hipEventDestroy(x->t_events[t]);
+    delete[] x->t_events;
+    x->t_events = nullptr;
+  }
   free_scratch(x);
   delete x;
   return e == hipSuccess ? GS_OK : GS_ERR_DEVICE;
@@ -256,18 +269,25 @@ gs_status gs_gather_reset(gs_ctx* x, void* stream, const int32_t* idx, int64_t k
   return device_status(x, gs::launch_gather_reset(x, as_stream(stream), idx, k, u, v, values), "gs_gather_reset");
 }
 
-// accumulate + sketch + merge of the fused step (tables kept in context scratch)
+// accumulate + sketch + merge of the fused step (tables kept in context scratch), with the
+// timing marks 0..3 when stage timing is active
 static hipError_t launch_sketch_phase(gs_ctx* x, hipStream_t s, const float* g, float* u, float* v, float* merged) {
   hipError_t e;
+  gs::stage_mark(x, s, 0);
   if (x->use_pull) {
     e = gs::launch_accumulate_vi(x, s, g, u, v);
+    gs::stage_mark(x, s, 1);
     if (e == hipSuccess) e = gs::launch_pull(x, s);
+    gs::stage_mark(x, s, 2);
     if (e == hipSuccess) e = gs::launch_merge_partials(x, s, merged, nullptr);
   } else {
     e = gs::launch_accumulate(x, s, g, u, v);
+    gs::stage_mark(x, s, 1);
     if (e == hipSuccess) e = gs::launch_sketch_acc(x, s, v);
+    gs::stage_mark(x, s, 2);
     if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
   }
+  gs::stage_mark(x, s, 3);
   return e;
 }
 
@@ -280,7 +300,9 @@ gs_status gs_step(gs_ctx* x, void* stream, const float* g, float* u, float* v, i
   hipStream_t s = as_stream(stream);
   hipError_t e = launch_sketch_phase(x, s, g, u, v, merged);
   if (e == hipSuccess) e = gs::launch_unsketch_topk(x, s, merged, k, nullptr, idx);
+  gs::stage_mark(x, s, 4);
   if (e == hipSuccess) e = gs::launch_gather_reset(x, s, idx, k, u, v, values);
+  gs::stage_mark(x, s, 5);
   return device_status(x, e, "gs_step");
 }
 
@@ -304,7 +326,9 @@ gs_status gs_step_heavymix(gs_ctx* x, void* stream, const float* g, float* u, fl
   hipStream_t s = as_stream(stream);
   hipError_t e = launch_sketch_phase(x, s, g, u, v, merged);
   if (e == hipSuccess) e = gs::launch_heavymix_topk(x, s, merged, k, rnd, nullptr, idx, n_heavy, nullptr);
+  gs::stage_mark(x, s, 4);
   if (e == hipSuccess) e = gs::launch_gather_reset(x, s, idx, k, u, v, values);
+  gs::stage_mark(x, s, 5);
   return device_status(x, e, "gs_step_heavymix");
 }
 
@@ -318,15 +342,21 @@ gs_status gs_step_sketch_momentum(gs_ctx* x, void* stream, const float* g, float
     return fail(x, GS_ERR_INVALID_ARG, "gs_step_sketch_momentum: k must satisfy 1 <= k <= k_max");
   hipStream_t s = as_stream(stream);
   hipError_t e;
+  gs::stage_mark(x, s, 0);
   if (x->use_pull) {
     e = gs::launch_interleave(x, s, g);
+    gs::stage_mark(x, s, 1);
     if (e == hipSuccess) e = gs::launch_pull(x, s);
+    gs::stage_mark(x, s, 2);
     if (e == hipSuccess) e = gs::launch_merge_partials(x, s, merged, nullptr);
   } else {
+    gs::stage_mark(x, s, 1);
     e = gs::launch_sketch_acc(x, s, g);
+    gs::stage_mark(x, s, 2);
     if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
   }
-  if (e == hipSuccess) e = gs::launch_sketch_state(x, s, merged, U, E, k, idx, values);
+  gs::stage_mark(x, s, 3);
+  if (e == hipSuccess) e = gs::launch_sketch_state(x, s, merged, U, E, k, idx, values);  // marks 4 and 5
   return device_status(x, e, "gs_step_sketch_momentum");
 }
 
@@ -338,6 +368,58 @@ gs_status gs_apply_update(gs_ctx* x, void* stream, const int32_t* idx, const flo
   if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_apply_update: k must satisfy 1 <= k <= k_max");
   if (!std::isfinite(lr)) return fail(x, GS_ERR_INVALID_ARG, "gs_apply_update: lr must be finite");
   return device_status(x, gs::launch_apply_update(x, as_stream(stream), idx, values, k, lr, w), "gs_apply_update");
+}
+
+gs_status gs_timing_start(gs_ctx* x, int32_t max_steps) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (x->timing) return fail(x, GS_ERR_INVALID_ARG, "gs_timing_start: timing already active");
+  if (max_steps < 1 || max_steps > (1 << 20)) return fail(x, GS_ERR_INVALID_ARG, "gs_timing_start: bad max_steps");
+  const int64_t n = (int64_t)max_steps * gs::kStageMarks;
+  hipEvent_t* ev = new (std::nothrow) hipEvent_t[n]();
+  if (!ev) return fail(x, GS_ERR_OUT_OF_MEMORY, "gs_timing_start: host allocation failed");
+  hipError_t e = hipSuccess;
+  int64_t made = 0;
+  for (; made < n && e == hipSuccess; ++made) e = hipEventCreate(&ev[made]);
+  if (e != hipSuccess) {
+    for (int64_t t = 0; t < made; ++t)
+      if (ev[t]) (void)hipEventDestroy(ev[t]);
+    delete[] ev;
+    return device_status(x, e, "gs_timing_start");
+  }
+  x->t_events = ev;
+  x->t_max = max_steps;
+  x->t_step = 0;
+  x->timing = true;
+  return GS_OK;
+}
+
+gs_status gs_timing_stop(gs_ctx* x, float* stage_ms, int32_t* n_steps) {
+  if (!x) return GS_ERR_INVALID_ARG;
+  x->last_error.clear();
+  if (!x->timing) return fail(x, GS_ERR_INVALID_ARG, "gs_timing_stop: timing not active");
+  const int32_t steps = x->t_step;
+  hipError_t e = hipSuccess;
+  double acc[GS_NUM_STAGES] = {0.0, 0.0, 0.0, 0.0, 0.0};
+  for (int32_t st = 0; st < steps && e == hipSuccess; ++st) {
+    hipEvent_t* m = x->t_events + (int64_t)st * gs::kStageMarks;
+    e = hipEventSynchronize(m[gs::kStageMarks - 1]);
+    for (int t = 0; t < GS_NUM_STAGES && e == hipSuccess; ++t) {
+      float ms = 0.f;
+      e = hipEventElapsedTime(&ms, m[t], m[t + 1]);
+      acc[t] += ms;
+    }
+  }
+  for (int64_t t = 0; t < (int64_t)x->t_max * gs::kStageMarks; ++t) (void)hipEventDestroy(x->t_events[t]);
+  delete[] x->t_events;
+  x->t_events = nullptr;
+  x->timing = false;
+  x->t_max = x->t_step = 0;
+  if (e != hipSuccess) return device_status(x, e, "gs_timing_stop");
+  if (stage_ms)
+    for (int t = 0; t < GS_NUM_STAGES; ++t) stage_ms[t] = steps ? (float)(acc[t] / steps) : 0.f;
+  if (n_steps) *n_steps = steps;
+  return GS_OK;
 }
 
 gs_status gs_step_profiled(gs_ctx* x, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,

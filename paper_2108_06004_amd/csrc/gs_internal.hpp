@@ -89,10 +89,20 @@ struct gs_ctx {
   double* l2buf = nullptr;        // [2][l2_half]
   int64_t l2_half = 0;            // r * max(1, npad / 2048) with npad = next power of two >= c
 
+  // stage timing of the fused steps (gs_timing_start / gs_timing_stop): events recorded on
+  // the step's stream before the first stage and after each stage, for up to t_max steps
+  bool timing = false;
+  int32_t t_max = 0, t_step = 0;
+  hipEvent_t* t_events = nullptr;  // [t_max][GS_STAGE_MARKS]
+
   std::string last_error;
 };
 
 namespace gs {
+constexpr int kStageMarks = 6;  // events per timed step: before stage 0, after stages 0..4
+// Record timing mark t (0..5) of the current step on `s` when timing is active; mark 5
+// completes the step.
+void stage_mark(gs_ctx* x, hipStream_t s, int t);
 // Launchers (each enqueues on `s` and returns hipGetLastError()).
 hipError_t launch_accumulate(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v);
 hipError_t launch_fill_zero(hipStream_t s, float* p, int64_t n);

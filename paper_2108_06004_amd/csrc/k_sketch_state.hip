@@ -103,6 +103,7 @@ hipError_t launch_sketch_state(gs_ctx* x, hipStream_t s, const float* merged, fl
   hipLaunchKernelGGL(k_sketch_mom, dim3(grid_for(rc, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, merged, U, E, rc,
                      x->rho);
   hipError_t e = launch_unsketch_topk(x, s, E, k, nullptr, idx);
+  stage_mark(x, s, 4);
   if (e != hipSuccess) return e;
   const dim3 gk(grid_for(k, kBlock, 4 * x->num_cus)), block(kBlock);
   switch (x->r) {
@@ -121,6 +122,7 @@ hipError_t launch_sketch_state(gs_ctx* x, hipStream_t s, const float* merged, fl
   hipLaunchKernelGGL(k_sub_clear, gp, block, 0, s, x->hs, idx, n_pairs, acc, claim);
   hipLaunchKernelGGL(k_sub_add, gp, block, 0, s, x->hs, idx, n_pairs, values, acc);
   hipLaunchKernelGGL(k_sub_apply, gp, block, 0, s, x->hs, idx, n_pairs, acc, claim, U, E, x->reset_momentum);
+  stage_mark(x, s, 5);
   return hipGetLastError();
 }
 

@@ -468,3 +468,39 @@ def test_two_contexts_and_a_side_stream():
     assert np.array_equal(got_b[3], ref_b[3]) and np.array_equal(got_b[4], ref_b[4])
     da.close()
     db.close()
+
+
+def test_stage_timing_over_ordinary_steps():
+    w = synth.WORKLOADS["laplace20-d270000-P4"]
+    hp = synth.hash_params(w)
+    dv = Dev(w.d, w.P, w.r, w.c, w.k, hp, w.rho)
+    g = to_dev(synth.gradients(w, 0))
+    u = torch.zeros((w.P, w.d), dtype=torch.float32, device=DEV)
+    v = torch.zeros_like(u)
+    with pytest.raises(gs.GsError):
+        dv.ctx.timing_stop()  # not active
+    dv.ctx.timing_start(3)
+    with pytest.raises(gs.GsError):
+        dv.ctx.timing_start(3)  # already active
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(3):
+        dv.ctx.step(g, u, v, w.k, dv.merged, dv.idx, dv.values)
+    e1.record()
+    for _ in range(2):  # beyond max_steps: not recorded
+        dv.ctx.step(g, u, v, w.k, dv.merged, dv.idx, dv.values)
+    stages, n = dv.ctx.timing_stop()
+    torch.cuda.synchronize()
+    assert n == 3 and set(stages) == set(gs.STAGES)
+    assert all(ms > 0 for ms in stages.values())
+    total = e0.elapsed_time(e1) / 3
+    assert 0.5 * total < sum(stages.values()) <= 1.05 * total
+    # the sketch-space and HEAVYMIX steps record their stages too
+    U = torch.zeros((w.r, w.c), dtype=torch.float32, device=DEV)
+    E = torch.zeros_like(U)
+    dv.ctx.timing_start(2)
+    for _ in range(2):
+        dv.ctx.step_sketch_momentum(g, U, E, w.k, dv.merged, dv.idx, dv.values)
+    stages, n = dv.ctx.timing_stop()
+    assert n == 2 and all(ms > 0 for ms in stages.values())
+    dv.close()
