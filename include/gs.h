@@ -177,8 +177,8 @@ gs_status gs_apply_update(gs_ctx* ctx, void* stream, const int32_t* idx, const f
 /* Stage timing for benchmarks and profiling. Runs exactly the kernels of gs_step, records a
  * HIP event on `stream` before the first stage and after each stage, synchronizes the stream
  * and writes the stage durations in milliseconds to the HOST array stage_ms[GS_NUM_STAGES]:
- *   [0] accumulate   [1] sketch (0 when fused into [0])   [2] merge
- *   [3] estimate + top-k selection                        [4] gather + reset
+ *   [0] accumulate   [1] sketch   [2] merge   [3] estimate + top-k selection
+ *   [4] gather + reset
  * Unlike gs_step this call blocks until the step has finished. */
 #define GS_NUM_STAGES 5
 gs_status gs_step_profiled(gs_ctx* ctx, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
