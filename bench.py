@@ -70,10 +70,11 @@ def kernel_source_digest() -> str:
     return h.hexdigest()
 
 
-def stage_kernels(w) -> dict:
+def stage_kernels(w, layout: str = "interleaved") -> dict:
     """The kernels each stage of the fused step launches (names as rocprofv3 reports them)."""
+    acc = [f"k_accumulate_il<{w.P // 4}>"] if layout == "interleaved" else [f"k_accumulate_vi<{w.P}>"]
     return {
-        "accumulate": [f"k_accumulate_vi<{w.P}>"],
+        "accumulate": acc,
         "sketch": [f"k_pull<{w.P}, 4>"],
         "merge": [f"k_merge_partials<{w.P}>"],
         "select": [f"k_sample<{w.r}, false>", "k_tau0", "k_heavy", f"k_pruned<{w.r}, false, false>",
@@ -83,10 +84,10 @@ def stage_kernels(w) -> dict:
     }
 
 
-def measured_traffic(w, stage: str):
+def measured_traffic(w, stage: str, layout: str = "interleaved"):
     """HBM-side bytes per launch of `stage` from the committed counter summary, or None when
-    there is none for this workload or the kernels changed since it was taken."""
-    path = os.path.join(ROOT, "profiles", f"traffic_gs_step_{w.name}.md")
+    there is none for this workload and state layout or the kernels changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_gs_step_{w.name}_{layout}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -94,7 +95,7 @@ def measured_traffic(w, stage: str):
     if not m or m.group(1) != kernel_source_digest():
         return None
     table = {name.strip(): float(val) for name, val in re.findall(r"traffic: (.+?) \| ([0-9.]+)", text)}
-    names = stage_kernels(w).get(stage)
+    names = stage_kernels(w, layout).get(stage)
     if not names or not all(n in table for n in names):
         return None
     return sum(table[n] for n in names)
@@ -141,6 +142,11 @@ def main():
     ap.add_argument("--state", choices=("vector", "sketch"), default="vector",
                     help="vector: per-worker u, v d-vectors (gs_step / gs_step_heavymix); sketch: momentum and error "
                          "kept in the merged sketch (gs_step_sketch_momentum; deterministic top-k)")
+    ap.add_argument("--state-layout", choices=("interleaved", "worker_major"), default="interleaved",
+                    help="layout of the per-worker state u, v: interleaved [d][P] rows (the sketch gathers them "
+                         "directly) or worker-major [P][d] (the accumulation also writes an interleaved copy)")
+    ap.add_argument("--compare-layout", action=argparse.BooleanOptionalAction, default=True,
+                    help="also time the same steps with the other state layout (reported under other_layout)")
     ap.add_argument("--calibration-copy", action="store_true",
                     help="before warm-up, run one plain device copy of the gradient buffer (P*d*4 bytes read and "
                          "written) to calibrate rocprofv3 FETCH_SIZE / WRITE_SIZE counters")
@@ -163,12 +169,13 @@ def main():
     nb = min(2, w.steps)
     g_host = [synth.gradients(w, t) for t in range(nb)]
     g_dev = [torch.from_numpy(x).to(dev) for x in g_host]
-    u = torch.zeros((w.P, w.d), dtype=torch.float32, device=dev)
-    v = torch.zeros_like(u)
     merged = torch.empty((w.r, w.c), dtype=torch.float32, device=dev)
     idx = torch.empty(w.k, dtype=torch.int32, device=dev)
     vals = torch.empty(w.k, dtype=torch.float32, device=dev)
-    ctx = gs.GsContext(w.d, w.P, w.r, w.c, w.k, hp, rho=w.rho)
+    layout = args.state_layout if args.state == "vector" else "worker_major"
+    ctx = gs.GsContext(w.d, w.P, w.r, w.c, w.k, hp, rho=w.rho, state_layout=layout)
+    u = torch.zeros(ctx.state_shape, dtype=torch.float32, device=dev)
+    v = torch.zeros_like(u)
     if args.state == "sketch":
         if args.selection != "topk":
             print("--state sketch uses the deterministic top-k selection", file=sys.stderr)
@@ -231,6 +238,27 @@ def main():
     dom = max(stage_ms, key=lambda s_: stage_ms[s_]) if n_timed else "sketch"
     achieved = sb[dom] / (stage_ms[dom] * 1e-3) / 1e9 if stage_ms[dom] > 0 else 0.0
     ctx.close()
+    del u, v
+
+    other_ms = None
+    if args.compare_layout and args.state == "vector" and args.selection == "topk":
+        other = "worker_major" if layout == "interleaved" else "interleaved"
+        log(f"[bench] timing {args.steps} steps with the {other} state layout")
+        ctx2 = gs.GsContext(w.d, w.P, w.r, w.c, w.k, hp, rho=w.rho, state_layout=other)
+        u2 = torch.zeros(ctx2.state_shape, dtype=torch.float32, device=dev)
+        v2 = torch.zeros_like(u2)
+        for s in range(args.warmup):
+            ctx2.step(g_dev[s % nb], u2, v2, w.k, merged, idx, vals)
+        o0, o1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        o0.record(stream)
+        for s in range(args.steps):
+            ctx2.step(g_dev[s % nb], u2, v2, w.k, merged, idx, vals)
+        o1.record(stream)
+        torch.cuda.synchronize()
+        other_ms = {"state_layout": other, "ms_per_step": o0.elapsed_time(o1) / args.steps}
+        ctx2.close()
+        del u2, v2
 
     # device copy bandwidth in the same run (read + write of one P*d fp32 buffer)
     src = g_dev[0]
@@ -270,7 +298,9 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "d": w.d, "P": w.P, "r": w.r, "c": w.c, "k": w.k,
-                   "selection": args.selection, "state": args.state, "gradients": w.note},
+                   "selection": args.selection, "state": args.state, "state_layout": layout,
+                   "gradients": w.note},
+        "other_layout": other_ms,
         "coords_per_s_per_worker": w.d / t,
         "algorithmic_bytes_per_step": B,
         "achieved_gbs": B / t / 1e9,
@@ -280,9 +310,9 @@ def main():
         "wall_s_timed": wall,
         "stage_ms": stage_ms,
         "stage_ms_from": f"HIP events recorded between the stages of the first {n_timed} timed steps",
-        "roofline": {"bound": "hbm", "kernel": " + ".join(stage_kernels(w).get(dom, [dom])), "stage": dom,
+        "roofline": {"bound": "hbm", "kernel": " + ".join(stage_kernels(w, layout).get(dom, [dom])), "stage": dom,
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": measured_traffic(w, dom), "traffic_unit": "bytes per launch",
+                     "traffic": measured_traffic(w, dom, layout), "traffic_unit": "bytes per launch",
                      "bytes_per_launch": sb[dom], "mean_ms": stage_ms[dom]},
         "cpu_baseline": None,
     }

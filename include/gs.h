@@ -8,7 +8,9 @@
  * coordinates are recovered from the summed sketch, and their exact values are fetched
  * and removed from the error accumulators (HEAVYMIX, Alg. 2).
  *
- * One GPU holds all P workers: per-worker arrays are stacked row-major as [P][d].
+ * One GPU holds all P workers. The gradients are stacked row-major as [P][d]; the workers'
+ * momentum and error state (u, v) is stacked either the same way or worker-interleaved,
+ * as chosen by gs_config.state_layout (see there).
  *
  * Conventions shared by every call
  *   - Array arguments are DEVICE pointers to memory owned by the caller (for example
@@ -47,6 +49,17 @@ typedef enum gs_status {
 #define GS_MAX_ROWS 16
 #define GS_MERSENNE_P 2147483647u /* 2^31 - 1 */
 
+/* Layouts of the per-worker state arrays u and v (gs_config.state_layout).
+ *   GS_STATE_WORKER_MAJOR  [P][d]: element (q, i) at q*d + i (the default, 0).
+ *   GS_STATE_INTERLEAVED   [d][GS_STATE_STRIDE(P)]: element (q, i) at i*GS_STATE_STRIDE(P) + q,
+ *                          rows padded to a multiple of 4 floats (16 bytes). The padding
+ *                          entries (q >= P) are never written and never affect a result.
+ * The interleaved form keeps the P values of a coordinate in one 16-byte-aligned row, which
+ * is what the sketch gathers, so the step needs no interleaved copy of v. */
+#define GS_STATE_WORKER_MAJOR 0
+#define GS_STATE_INTERLEAVED 1
+#define GS_STATE_STRIDE(P) ((((P) + 3) / 4) * 4)
+
 /*
  * Problem description (Alg. 1 inputs: k, P; the Count Sketch of Sec. III-A).
  *   d        coordinates per worker, 1 <= d <= p - 1 (so every index is a valid hash input)
@@ -58,6 +71,10 @@ typedef enum gs_status {
  *   hash_a, hash_b  HOST arrays [r]: bucket hash h_j(i) = ((a_j*i + b_j) mod p) mod c
  *   sign_a, sign_b  HOST arrays [r]: sign s_j(i) = +1 if ((a_j*i + b_j) mod p) is odd, else -1
  *                   with 1 <= a < p and 0 <= b < p for all four; copied by gs_create.
+ *   state_layout    GS_STATE_WORKER_MAJOR (0) or GS_STATE_INTERLEAVED: the layout of u and v
+ *                   in every call that takes them (gs_accumulate, gs_sketch's v,
+ *                   gs_gather_reset, gs_step, gs_step_heavymix, gs_step_profiled). Other
+ *                   values are GS_ERR_INVALID_ARG.
  */
 typedef struct gs_config {
   int64_t d;
@@ -71,6 +88,7 @@ typedef struct gs_config {
   const uint32_t* hash_b;
   const uint32_t* sign_a;
   const uint32_t* sign_b;
+  int32_t state_layout;
 } gs_config;
 
 typedef struct gs_ctx gs_ctx; /* opaque: a copy of the config plus device scratch */
@@ -91,13 +109,13 @@ gs_status gs_destroy(gs_ctx* ctx);
  * error accumulation carried along with the sketch; Alg. 1 starts from a zero state).
  * For every worker q and coordinate i, in IEEE fp32 with each operation rounded:
  *     u[q][i] = rho * u[q][i] + g[q][i];   v[q][i] = v[q][i] + u[q][i].
- * g: [P][d] input. u, v: [P][d], updated in place. */
+ * g: [P][d] input. u, v: state layout (see gs_config), updated in place. */
 gs_status gs_accumulate(gs_ctx* ctx, void* stream, const float* g, float* u, float* v);
 
 /* Count Sketch of every worker's accumulator (Sec. III-A; Alg. 1 sketch step):
  *     tables[q][j][col] = sum over i with h_j(i) == col of s_j(i) * v[q][i].
- * v: [P][d] input. tables: [P][r][c] output (overwritten; fp32 cell sums whose rounding
- * depends on the summation order). */
+ * v: state layout input. tables: [P][r][c] output (overwritten; each cell is the sum
+ * accumulated in double precision and rounded once to fp32). */
 gs_status gs_sketch(gs_ctx* ctx, void* stream, const float* v, float* tables);
 
 /* Sum of the P worker sketches in the binomial-tree order of Alg. 1 (in each round the
@@ -117,13 +135,14 @@ gs_status gs_unsketch_topk(gs_ctx* ctx, void* stream, const float* merged, int64
  * For t < k, with i = idx[t]: values[t] = tree-order sum over q of v[q][i] (the merge
  * order above); then v[q][i] = 0 for every q, and u[q][i] = 0 too when reset_momentum.
  * idx: [k] distinct coordinates in [0, d) (e.g. the output of gs_unsketch_topk).
- * u, v: [P][d], updated in place. values: [k] output. 1 <= k <= k_max. */
+ * u, v: state layout, updated in place. values: [k] output. 1 <= k <= k_max. */
 gs_status gs_gather_reset(gs_ctx* ctx, void* stream, const int32_t* idx, int64_t k, float* u, float* v,
                           float* values);
 
 /* One whole step: accumulate, sketch, merge, estimate + top-k, exact values + reset, with
  * the per-worker tables kept in context scratch. Equivalent to the five calls above.
- * g: [P][d] input. u, v: [P][d] in place. merged: [r][c] output. idx, values: [k] outputs. */
+ * g: [P][d] input. u, v: state layout, in place. merged: [r][c] output. idx, values: [k]
+ * outputs. */
 gs_status gs_step(gs_ctx* ctx, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
                   int32_t* idx, float* values);
 

@@ -28,6 +28,14 @@ EXPORTED = ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge",
             "gs_last_error")
 GS_NUM_STAGES = 5
 STAGES = ("accumulate", "sketch", "merge", "select", "gather_reset")
+# layouts of the per-worker state u, v (gs_config.state_layout)
+GS_STATE_WORKER_MAJOR, GS_STATE_INTERLEAVED = 0, 1
+STATE_LAYOUTS = {"worker_major": GS_STATE_WORKER_MAJOR, "interleaved": GS_STATE_INTERLEAVED}
+
+
+def state_stride(P: int) -> int:
+    """Row length of the interleaved state: P rounded up to a multiple of 4."""
+    return (P + 3) // 4 * 4
 
 
 class GsLibraryMissing(RuntimeError):
@@ -53,6 +61,7 @@ class gs_config(ctypes.Structure):
         ("hash_b", ctypes.POINTER(ctypes.c_uint32)),
         ("sign_a", ctypes.POINTER(ctypes.c_uint32)),
         ("sign_b", ctypes.POINTER(ctypes.c_uint32)),
+        ("state_layout", ctypes.c_int32),
     ]
 
 
@@ -130,14 +139,15 @@ def _stream(stream):
 
 
 def gs_create(d: int, P: int, r: int, c: int, k_max: int, hash_a, hash_b, sign_a, sign_b, rho: float = 0.9,
-              reset_momentum: bool = True) -> int:
+              reset_momentum: bool = True, state_layout: int = GS_STATE_WORKER_MAJOR) -> int:
     """Create a context on the current device; returns the opaque handle (an int)."""
     lib = load_library()
     arrs = [np.ascontiguousarray(a, dtype=np.uint32) for a in (hash_a, hash_b, sign_a, sign_b)]
     if any(a.size != r for a in arrs):
         raise ValueError("hash parameter arrays must have r entries")
     u32p = ctypes.POINTER(ctypes.c_uint32)
-    cfg = gs_config(d, P, r, c, k_max, rho, int(bool(reset_momentum)), *(a.ctypes.data_as(u32p) for a in arrs))
+    cfg = gs_config(d, P, r, c, k_max, rho, int(bool(reset_momentum)), *(a.ctypes.data_as(u32p) for a in arrs),
+                    int(state_layout))
     out = ctypes.c_void_p()
     _check(lib.gs_create(ctypes.byref(cfg), ctypes.byref(out)), None, "gs_create")
     return out.value
@@ -217,10 +227,41 @@ class GsContext:
     """A context plus shape/dtype checks on every call."""
 
     def __init__(self, d: int, P: int, r: int, c: int, k_max: int, hash_params: dict, rho: float = 0.9,
-                 reset_momentum: bool = True):
+                 reset_momentum: bool = True, state_layout: str = "worker_major"):
+        if state_layout not in STATE_LAYOUTS:
+            raise ValueError(f"state_layout must be one of {sorted(STATE_LAYOUTS)}")
         self.d, self.P, self.r, self.c, self.k_max = d, P, r, c, k_max
+        self.state_layout = state_layout
         self.handle = gs_create(d, P, r, c, k_max, hash_params["a"], hash_params["b"], hash_params["a2"],
-                                hash_params["b2"], rho, reset_momentum)
+                                hash_params["b2"], rho, reset_momentum, STATE_LAYOUTS[state_layout])
+
+    @property
+    def state_shape(self) -> tuple:
+        """Shape of u and v: (P, d) worker-major, or (d, P rounded up to 4) interleaved."""
+        if self.state_layout == "interleaved":
+            return (self.d, state_stride(self.P))
+        return (self.P, self.d)
+
+    def state_numel(self) -> int:
+        a, b = self.state_shape
+        return a * b
+
+    def to_state(self, x):
+        """A [P][d] tensor (worker rows) rearranged into this context's state layout (a new
+        tensor; interleaved padding is zero)."""
+        import torch
+
+        if self.state_layout == "worker_major":
+            return x.reshape(self.P, self.d).contiguous().clone()
+        out = torch.zeros(self.state_shape, dtype=x.dtype, device=x.device)
+        out[:, :self.P] = x.reshape(self.P, self.d).t()
+        return out
+
+    def from_state(self, t):
+        """The [P][d] view of a state tensor in this context's layout (a copy for interleaved)."""
+        if self.state_layout == "worker_major":
+            return t.reshape(self.P, self.d)
+        return t.reshape(self.state_shape)[:, :self.P].t().contiguous()
 
     def close(self):
         if self.handle:
@@ -240,12 +281,13 @@ class GsContext:
         return t
 
     def accumulate(self, g, u, v, stream=None):
-        n = self.P * self.d
-        gs_accumulate(self.handle, self._f32(g, n, "g"), self._f32(u, n, "u"), self._f32(v, n, "v"), stream)
+        ns = self.state_numel()
+        gs_accumulate(self.handle, self._f32(g, self.P * self.d, "g"), self._f32(u, ns, "u"), self._f32(v, ns, "v"),
+                      stream)
 
     def sketch(self, v, tables, stream=None):
-        gs_sketch(self.handle, self._f32(v, self.P * self.d, "v"), self._f32(tables, self.P * self.r * self.c,
-                                                                             "tables"), stream)
+        gs_sketch(self.handle, self._f32(v, self.state_numel(), "v"),
+                  self._f32(tables, self.P * self.r * self.c, "tables"), stream)
 
     def merge(self, tables, merged, stream=None):
         gs_merge(self.handle, self._f32(tables, self.P * self.r * self.c, "tables"),
@@ -263,16 +305,16 @@ class GsContext:
         import torch
 
         _ptr(idx, torch.int32, k, "idx")
-        n = self.P * self.d
-        gs_gather_reset(self.handle, idx, k, self._f32(u, n, "u"), self._f32(v, n, "v"),
+        ns = self.state_numel()
+        gs_gather_reset(self.handle, idx, k, self._f32(u, ns, "u"), self._f32(v, ns, "v"),
                         self._f32(values, k, "values"), stream)
 
     def step(self, g, u, v, k, merged, idx, values, stream=None):
         import torch
 
-        n = self.P * self.d
+        n, ns = self.P * self.d, self.state_numel()
         _ptr(idx, torch.int32, k, "idx")
-        gs_step(self.handle, self._f32(g, n, "g"), self._f32(u, n, "u"), self._f32(v, n, "v"), k,
+        gs_step(self.handle, self._f32(g, n, "g"), self._f32(u, ns, "u"), self._f32(v, ns, "v"), k,
                 self._f32(merged, self.r * self.c, "merged"), idx, self._f32(values, k, "values"), stream)
 
     def heavymix_topk(self, merged, k, rnd, idx, est=None, n_heavy=None, l2sq=None, stream=None):
@@ -297,14 +339,14 @@ class GsContext:
     def step_heavymix(self, g, u, v, k, rnd, merged, idx, values, n_heavy=None, stream=None):
         import torch
 
-        n = self.P * self.d
+        n, ns = self.P * self.d, self.state_numel()
         _ptr(idx, torch.int32, k, "idx")
         if rnd.dtype not in (torch.int32, torch.uint32):
             raise TypeError("rnd must hold 32-bit draws (int32 or uint32)")
         _ptr(rnd, None, self.d, "rnd")
         if n_heavy is not None:
             _ptr(n_heavy, torch.int64, 1, "n_heavy")
-        gs_step_heavymix(self.handle, self._f32(g, n, "g"), self._f32(u, n, "u"), self._f32(v, n, "v"), k, rnd,
+        gs_step_heavymix(self.handle, self._f32(g, n, "g"), self._f32(u, ns, "u"), self._f32(v, ns, "v"), k, rnd,
                          self._f32(merged, self.r * self.c, "merged"), idx, self._f32(values, k, "values"), n_heavy,
                          stream)
 
@@ -342,8 +384,8 @@ class GsContext:
     def step_profiled(self, g, u, v, k, merged, idx, values, stream=None) -> dict:
         import torch
 
-        n = self.P * self.d
+        n, ns = self.P * self.d, self.state_numel()
         _ptr(idx, torch.int32, k, "idx")
-        return gs_step_profiled(self.handle, self._f32(g, n, "g"), self._f32(u, n, "u"), self._f32(v, n, "v"), k,
+        return gs_step_profiled(self.handle, self._f32(g, n, "g"), self._f32(u, ns, "u"), self._f32(v, ns, "v"), k,
                                 self._f32(merged, self.r * self.c, "merged"), idx, self._f32(values, k, "values"),
                                 stream)

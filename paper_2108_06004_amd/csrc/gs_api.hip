@@ -120,6 +120,8 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   if (!valid_ab(cfg->hash_a, cfg->hash_b, cfg->r) || !valid_ab(cfg->sign_a, cfg->sign_b, cfg->r))
     return bad("hash parameters must satisfy 1 <= a < p and 0 <= b < p");
   if ((int64_t)cfg->P * cfg->r * cfg->c > (int64_t)1 << 40) return bad("P*r*c too large");
+  if (cfg->state_layout != GS_STATE_WORKER_MAJOR && cfg->state_layout != GS_STATE_INTERLEAVED)
+    return bad("state_layout must be GS_STATE_WORKER_MAJOR or GS_STATE_INTERLEAVED");
 
   gs_ctx* x = new (std::nothrow) gs_ctx();
   if (!x) {
@@ -133,6 +135,8 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   x->r = cfg->r;
   x->rho = cfg->rho;
   x->reset_momentum = cfg->reset_momentum ? 1 : 0;
+  x->state_layout = cfg->state_layout;
+  x->state_stride = GS_STATE_STRIDE(cfg->P);
   x->hs.r = cfg->r;
   for (int j = 0; j < cfg->r; ++j) {
     x->hs.row[j].a = cfg->hash_a[j];
@@ -236,11 +240,15 @@ gs_status gs_sketch(gs_ctx* x, void* stream, const float* v, float* tables) {
   hipStream_t s = as_stream(stream);
   hipError_t e;
   if (x->use_pull) {
-    e = gs::launch_interleave(x, s, v);
-    if (e == hipSuccess) e = gs::launch_pull(x, s);
+    const float* rows = x->vI;
+    if (x->state_layout == GS_STATE_INTERLEAVED)
+      rows = gs::pull_rows_of_state(x, s, v, &e);
+    else
+      e = gs::launch_interleave(x, s, v);
+    if (e == hipSuccess) e = gs::launch_pull(x, s, rows);
     if (e == hipSuccess) e = gs::launch_merge_partials(x, s, nullptr, tables);
   } else {
-    e = gs::launch_sketch(x, s, v, tables);
+    e = gs::launch_sketch(x, s, v, gs::state_view(x), tables);
   }
   return device_status(x, e, "gs_sketch");
 }
@@ -269,27 +277,44 @@ gs_status gs_gather_reset(gs_ctx* x, void* stream, const int32_t* idx, int64_t k
   return device_status(x, gs::launch_gather_reset(x, as_stream(stream), idx, k, u, v, values), "gs_gather_reset");
 }
 
-// accumulate + sketch + merge of the fused step (tables kept in context scratch), with the
-// timing marks 0..3 when stage timing is active
-static hipError_t launch_sketch_phase(gs_ctx* x, hipStream_t s, const float* g, float* u, float* v, float* merged) {
+}  // extern "C"
+
+// accumulate + sketch + merge of the fused step (tables kept in context scratch); mark(t)
+// is called before stage 0 (t = 0) and after stages 0..2 (t = 1..3)
+template <class Mark>
+static hipError_t launch_sketch_phase(gs_ctx* x, hipStream_t s, const float* g, float* u, float* v, float* merged,
+                                      Mark mark) {
   hipError_t e;
-  gs::stage_mark(x, s, 0);
+  mark(0);
   if (x->use_pull) {
-    e = gs::launch_accumulate_vi(x, s, g, u, v);
-    gs::stage_mark(x, s, 1);
-    if (e == hipSuccess) e = gs::launch_pull(x, s);
-    gs::stage_mark(x, s, 2);
+    const float* rows = x->vI;
+    if (x->state_layout == GS_STATE_INTERLEAVED) {
+      // the caller's v rows are what the pull gathers: no interleaved copy
+      e = gs::launch_accumulate(x, s, g, u, v);
+      if (e == hipSuccess) rows = gs::pull_rows_of_state(x, s, v, &e);
+    } else {
+      e = gs::launch_accumulate_vi(x, s, g, u, v);
+    }
+    mark(1);
+    if (e == hipSuccess) e = gs::launch_pull(x, s, rows);
+    mark(2);
     if (e == hipSuccess) e = gs::launch_merge_partials(x, s, merged, nullptr);
   } else {
     e = gs::launch_accumulate(x, s, g, u, v);
-    gs::stage_mark(x, s, 1);
-    if (e == hipSuccess) e = gs::launch_sketch_acc(x, s, v);
-    gs::stage_mark(x, s, 2);
+    mark(1);
+    if (e == hipSuccess) e = gs::launch_sketch_acc(x, s, v, gs::state_view(x));
+    mark(2);
     if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
   }
-  gs::stage_mark(x, s, 3);
+  mark(3);
   return e;
 }
+
+static hipError_t launch_sketch_phase(gs_ctx* x, hipStream_t s, const float* g, float* u, float* v, float* merged) {
+  return launch_sketch_phase(x, s, g, u, v, merged, [x, s](int t) { gs::stage_mark(x, s, t); });
+}
+
+extern "C" {
 
 gs_status gs_step(gs_ctx* x, void* stream, const float* g, float* u, float* v, int64_t k, float* merged,
                   int32_t* idx, float* values) {
@@ -346,12 +371,12 @@ gs_status gs_step_sketch_momentum(gs_ctx* x, void* stream, const float* g, float
   if (x->use_pull) {
     e = gs::launch_interleave(x, s, g);
     gs::stage_mark(x, s, 1);
-    if (e == hipSuccess) e = gs::launch_pull(x, s);
+    if (e == hipSuccess) e = gs::launch_pull(x, s, x->vI);
     gs::stage_mark(x, s, 2);
     if (e == hipSuccess) e = gs::launch_merge_partials(x, s, merged, nullptr);
   } else {
     gs::stage_mark(x, s, 1);
-    e = gs::launch_sketch_acc(x, s, g);
+    e = gs::launch_sketch_acc(x, s, g, gs::worker_major_view(x));
     gs::stage_mark(x, s, 2);
     if (e == hipSuccess) e = gs::launch_merge_acc(x, s, merged);
   }
@@ -433,17 +458,16 @@ gs_status gs_step_profiled(gs_ctx* x, void* stream, const float* g, float* u, fl
   hipEvent_t ev[GS_NUM_STAGES + 1] = {};
   hipError_t e = hipSuccess;
   for (int t = 0; t <= GS_NUM_STAGES && e == hipSuccess; ++t) e = hipEventCreate(&ev[t]);
-  if (e == hipSuccess) e = hipEventRecord(ev[0], s);
-  if (e == hipSuccess) e = x->use_pull ? gs::launch_accumulate_vi(x, s, g, u, v) : gs::launch_accumulate(x, s, g, u, v);
-  if (e == hipSuccess) e = hipEventRecord(ev[1], s);
-  if (e == hipSuccess) e = x->use_pull ? gs::launch_pull(x, s) : gs::launch_sketch_acc(x, s, v);
-  if (e == hipSuccess) e = hipEventRecord(ev[2], s);
-  if (e == hipSuccess) e = x->use_pull ? gs::launch_merge_partials(x, s, merged, nullptr) : gs::launch_merge_acc(x, s, merged);
-  if (e == hipSuccess) e = hipEventRecord(ev[3], s);
+  hipError_t erec = hipSuccess;
+  auto mark = [&](int t) {
+    if (erec == hipSuccess) erec = hipEventRecord(ev[t], s);
+  };
+  if (e == hipSuccess) e = launch_sketch_phase(x, s, g, u, v, merged, mark);
   if (e == hipSuccess) e = gs::launch_unsketch_topk(x, s, merged, k, nullptr, idx);
-  if (e == hipSuccess) e = hipEventRecord(ev[4], s);
+  mark(4);
   if (e == hipSuccess) e = gs::launch_gather_reset(x, s, idx, k, u, v, values);
-  if (e == hipSuccess) e = hipEventRecord(ev[5], s);
+  mark(5);
+  if (e == hipSuccess) e = erec;
   if (e == hipSuccess) e = hipEventSynchronize(ev[5]);
   for (int t = 0; t < GS_NUM_STAGES && e == hipSuccess; ++t) e = hipEventElapsedTime(&stage_ms[t], ev[t], ev[t + 1]);
   for (int t = 0; t <= GS_NUM_STAGES; ++t)

@@ -6,6 +6,7 @@
 
 #include <string>
 
+#include "../../include/gs.h"
 #include "gs_device.hpp"
 
 // Top-k selection works on 32-bit keys (the bits of |estimate|) in three radix digits.
@@ -45,6 +46,13 @@ struct PullPlan {
   int64_t chunk;          // coordinates per build chunk
 };
 constexpr int64_t kMaxFillLds = 160 * 1024;  // LDS of the list-fill kernel holds T cursors
+
+// Where element (worker q, coordinate i) of a per-worker array lives: q*qs + i*is.
+// [P][d] (worker-major) is {d, 1}; the interleaved state [d][PP] is {1, PP}.
+struct StateView {
+  int64_t qs, is;
+  __host__ __device__ int64_t at(int q, int64_t i) const { return (int64_t)q * qs + i * is; }
+};
 constexpr int kTilesPerCu = 1;               // resident pull workgroups per CU (LDS-limited)
 }  // namespace gs
 
@@ -54,6 +62,8 @@ struct gs_ctx {
   int32_t P = 0, r = 0;
   float rho = 0.f;
   int32_t reset_momentum = 1;
+  int32_t state_layout = 0;   // GS_STATE_WORKER_MAJOR or GS_STATE_INTERLEAVED (u and v)
+  int32_t state_stride = 0;   // row length of the interleaved state: P rounded up to a multiple of 4
   gs::HashSet hs{};
   int num_cus = 256;
 
@@ -99,6 +109,12 @@ struct gs_ctx {
 };
 
 namespace gs {
+// The view of the caller's u and v (per the context's state layout), and of a [P][d] array.
+inline StateView state_view(const gs_ctx* x) {
+  return x->state_layout == GS_STATE_INTERLEAVED ? StateView{1, x->state_stride} : StateView{x->d, 1};
+}
+inline StateView worker_major_view(const gs_ctx* x) { return StateView{x->d, 1}; }
+
 constexpr int kStageMarks = 6;  // events per timed step: before stage 0, after stages 0..4
 // Record timing mark t (0..5) of the current step on `s` when timing is active; mark 5
 // completes the step.
@@ -106,8 +122,8 @@ void stage_mark(gs_ctx* x, hipStream_t s, int t);
 // Launchers (each enqueues on `s` and returns hipGetLastError()).
 hipError_t launch_accumulate(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v);
 hipError_t launch_fill_zero(hipStream_t s, float* p, int64_t n);
-hipError_t launch_sketch_acc(const gs_ctx* x, hipStream_t s, const float* v);
-hipError_t launch_sketch(const gs_ctx* x, hipStream_t s, const float* v, float* tables);
+hipError_t launch_sketch_acc(const gs_ctx* x, hipStream_t s, const float* v, StateView sv);
+hipError_t launch_sketch(const gs_ctx* x, hipStream_t s, const float* v, StateView sv, float* tables);
 hipError_t launch_merge_acc(const gs_ctx* x, hipStream_t s, float* merged);
 hipError_t launch_merge(const gs_ctx* x, hipStream_t s, const float* tables, float* merged);
 hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, float* est, int32_t* idx);
@@ -126,6 +142,11 @@ PullPlan make_pull_plan(int64_t d, int32_t P, int32_t r, int64_t c, int num_cus)
 hipError_t build_pull_lists(gs_ctx* x);
 hipError_t launch_accumulate_vi(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v);
 hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v);
-hipError_t launch_pull(const gs_ctx* x, hipStream_t s);
+// The pull gathers rows of PP floats (16-byte aligned) from `rows`: the context's interleaved
+// copy x->vI, or the caller's v itself when the state is interleaved.
+hipError_t launch_pull(const gs_ctx* x, hipStream_t s, const float* rows);
+// Rows for the pull from the caller's state array v (GS_STATE_INTERLEAVED): v itself when it
+// is 16-byte aligned, otherwise a copy enqueued into x->vI.
+const float* pull_rows_of_state(const gs_ctx* x, hipStream_t s, const float* v, hipError_t* e);
 hipError_t launch_merge_partials(const gs_ctx* x, hipStream_t s, float* merged, float* tables);
 }  // namespace gs

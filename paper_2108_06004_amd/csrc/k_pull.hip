@@ -218,6 +218,14 @@ __global__ void __launch_bounds__(kBlock) k_accumulate_vi_any(const float* __res
   }
 }
 
+// Copy of an interleaved state array that is not 16-byte aligned (any alignment, one float
+// per lane), so that the pull can load 16-byte pieces of its rows.
+__global__ void __launch_bounds__(kBlock) k_copy_rows(const float* __restrict__ src, float* __restrict__ dst,
+                                                      int64_t n) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n; e += stride) dst[e] = src[e];
+}
+
 // ------------------------------------------------------------------------------------
 // The pull: one workgroup per (tile, segment).
 
@@ -257,7 +265,9 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   const int64_t lo = off[t], n = off[t + 1] - lo;
   const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
   double* const mycol = acc + (int64_t)(4 * sub) * wt - col0;
-  int64_t eb = e0 + tid;
+  // when L does not divide the block (L = 3: 85 groups of 3 lanes), the last lane has no
+  // group: it takes no entry (its would be the next pass's first)
+  int64_t eb = tid < B ? e0 + tid : e1;
   for (; eb + (U - 1) * B < e1; eb += U * B) {
     uint32_t i[U];
 #pragma unroll
@@ -377,10 +387,10 @@ hipError_t launch_acc_vi_p(const gs_ctx* x, hipStream_t s, const float* g, float
 }
 
 template <int P>
-void launch_pull_p(const gs_ctx* x, hipStream_t s) {
+void launch_pull_p(const gs_ctx* x, hipStream_t s, const float* rows) {
   const PullPlan& pl = x->plan;
   hipLaunchKernelGGL((k_pull<P, kPullUnroll>), dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kPullBlock),
-                     (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, x->vI, x->partial);
+                     (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, rows, x->partial);
 }
 
 template <int P>
@@ -510,10 +520,10 @@ hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v) {
   return hipGetLastError();
 }
 
-hipError_t launch_pull(const gs_ctx* x, hipStream_t s) {
+hipError_t launch_pull(const gs_ctx* x, hipStream_t s, const float* rows) {
   switch (x->P) {
 #define GS_PULL_CASE(PP) \
-  case PP: launch_pull_p<PP>(x, s); break;
+  case PP: launch_pull_p<PP>(x, s, rows); break;
     GS_PULL_CASE(1) GS_PULL_CASE(2) GS_PULL_CASE(3) GS_PULL_CASE(4) GS_PULL_CASE(5) GS_PULL_CASE(6) GS_PULL_CASE(7)
     GS_PULL_CASE(8) GS_PULL_CASE(9) GS_PULL_CASE(10) GS_PULL_CASE(11) GS_PULL_CASE(12) GS_PULL_CASE(13)
     GS_PULL_CASE(14) GS_PULL_CASE(15) GS_PULL_CASE(16)
@@ -521,10 +531,22 @@ hipError_t launch_pull(const gs_ctx* x, hipStream_t s) {
     default: {
       const PullPlan& pl = x->plan;
       hipLaunchKernelGGL(k_pull_any, dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kBlock),
-                         (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, x->vI, x->partial);
+                         (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, rows, x->partial);
     }
   }
   return hipGetLastError();
+}
+
+const float* pull_rows_of_state(const gs_ctx* x, hipStream_t s, const float* v, hipError_t* e) {
+  // the unrolled pulls (P <= 16) load 16-byte pieces of a row; the generic one loads floats
+  if (x->P > 16 || ((uintptr_t)v & 15u) == 0) {
+    *e = hipSuccess;
+    return v;
+  }
+  const int64_t n = x->d * x->plan.PP;
+  hipLaunchKernelGGL(k_copy_rows, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, v, x->vI, n);
+  *e = hipGetLastError();
+  return x->vI;
 }
 
 hipError_t launch_merge_partials(const gs_ctx* x, hipStream_t s, float* merged, float* tables) {

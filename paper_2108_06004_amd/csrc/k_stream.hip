@@ -47,6 +47,82 @@ __global__ void __launch_bounds__(kBlock) k_accumulate1(const float* __restrict_
   }
 }
 
+// Worker-interleaved state (u, v rows of PP = 4G floats per coordinate; g stays [P][d]).
+// A wave covers CW = 64/G consecutive coordinates: lane l takes coordinate base + l/G and
+// the 16-byte group h = l%G of its row (workers 4h..4h+3), so consecutive lanes read and
+// write consecutive 16-byte pieces of u and v; the four gradient values come from four
+// worker rows of g (4-byte loads, 4*CW bytes contiguous per row and wave). Four chunks per
+// lane are in flight per iteration. Only full chunks run here; the tail goes to
+// k_accumulate_il_any.
+template <int G>
+__global__ void __launch_bounds__(kBlock) k_accumulate_il(const float* __restrict__ g, float* __restrict__ u,
+                                                          float* __restrict__ v, int64_t d, float rho) {
+  constexpr int CW = 64 / G;
+  constexpr int PP = 4 * G;
+  constexpr int U = 4;
+  const int lane = threadIdx.x & 63;
+  if (lane >= CW * G) return;  // G = 3: one idle lane per wave (no barrier below)
+  const int h = lane % G;
+  const int64_t sub = lane / G;
+  const int64_t nch = d / CW;
+  const int64_t wstride = (int64_t)gridDim.x * (kBlock / 64);
+  int64_t ch = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  for (; ch + (U - 1) * wstride < nch; ch += U * wstride) {
+    f4 gg[U], uu[U], ww[U];
+#pragma unroll
+    for (int m = 0; m < U; ++m) {
+      const int64_t i = (ch + m * wstride) * CW + sub;
+      const float* gq = g + (int64_t)(4 * h) * d + i;
+      gg[m].x = __builtin_nontemporal_load(gq);
+      gg[m].y = __builtin_nontemporal_load(gq + d);
+      gg[m].z = __builtin_nontemporal_load(gq + 2 * d);
+      gg[m].w = __builtin_nontemporal_load(gq + 3 * d);
+      uu[m] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(u + i * PP) + h);
+      ww[m] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(v + i * PP) + h);
+    }
+#pragma unroll
+    for (int m = 0; m < U; ++m) {
+      const int64_t i = (ch + m * wstride) * CW + sub;
+      uu[m] = rho * uu[m] + gg[m];
+      ww[m] = ww[m] + uu[m];
+      __builtin_nontemporal_store(uu[m], reinterpret_cast<f4*>(u + i * PP) + h);
+      __builtin_nontemporal_store(ww[m], reinterpret_cast<f4*>(v + i * PP) + h);
+    }
+  }
+  for (; ch < nch; ch += wstride) {
+    const int64_t i = ch * CW + sub;
+    const float* gq = g + (int64_t)(4 * h) * d + i;
+    f4 gg;
+    gg.x = gq[0];
+    gg.y = gq[d];
+    gg.z = gq[2 * d];
+    gg.w = gq[3 * d];
+    f4* up = reinterpret_cast<f4*>(u + i * PP) + h;
+    f4* vp = reinterpret_cast<f4*>(v + i * PP) + h;
+    f4 uu = *up, ww = *vp;
+    uu = rho * uu + gg;
+    ww = ww + uu;
+    *up = uu;
+    *vp = ww;
+  }
+}
+
+// Any P, any alignment: one lane per (coordinate, worker) for coordinates i >= i_lo.
+__global__ void __launch_bounds__(kBlock) k_accumulate_il_any(const float* __restrict__ g, float* __restrict__ u,
+                                                              float* __restrict__ v, int64_t d, int P, int PP,
+                                                              float rho, int64_t i_lo) {
+  const int64_t n = (d - i_lo) * P;
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n; e += stride) {
+    const int64_t i = i_lo + e / P;
+    const int q = (int)(e % P);
+    const int64_t o = i * PP + q;
+    const float un = rho * u[o] + g[(int64_t)q * d + i];
+    u[o] = un;
+    v[o] = v[o] + un;
+  }
+}
+
 __global__ void __launch_bounds__(kBlock) k_fill_zero(float* __restrict__ p, int64_t n) {
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   const int64_t n4 = n / 4;
@@ -70,7 +146,7 @@ __global__ void __launch_bounds__(kBlock) k_fill_zero1(float* __restrict__ p, in
 // merge), so the result does not depend on the atomic order beyond fp64 rounding.
 
 __global__ void __launch_bounds__(kBlock) k_sketch_atomic(HashSet hs, const float* __restrict__ v,
-                                                          double* __restrict__ acc, int64_t d, int P) {
+                                                          double* __restrict__ acc, int64_t d, int P, StateView sv) {
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   const int64_t rc = (int64_t)hs.r * hs.c;
   for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < d; i += stride) {
@@ -79,7 +155,7 @@ __global__ void __launch_bounds__(kBlock) k_sketch_atomic(HashSet hs, const floa
       hash_ij(hs, j, (uint32_t)i, col, sflip);
       double* cell = acc + (int64_t)j * hs.c + col;
       for (int q = 0; q < P; ++q)
-        unsafeAtomicAdd(cell + q * rc, (double)apply_sign(v[(int64_t)q * d + i], sflip));
+        unsafeAtomicAdd(cell + q * rc, (double)apply_sign(v[sv.at(q, i)], sflip));
     }
   }
 }
@@ -150,35 +226,35 @@ __global__ void __launch_bounds__(kBlock) k_merge64_dyn(const double* __restrict
 template <int P>
 __global__ void __launch_bounds__(kBlock) k_gather_reset(const int32_t* __restrict__ idx, int64_t k,
                                                          float* __restrict__ u, float* __restrict__ v,
-                                                         float* __restrict__ values, int64_t d, int reset_u) {
+                                                         float* __restrict__ values, StateView sv, int reset_u) {
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < k; t += stride) {
     const int64_t i = idx[t];
     float x[P];
 #pragma unroll
-    for (int q = 0; q < P; ++q) x[q] = v[q * d + i];
+    for (int q = 0; q < P; ++q) x[q] = v[sv.at(q, i)];
     values[t] = tree_sum<P>(x);
 #pragma unroll
     for (int q = 0; q < P; ++q) {
-      v[q * d + i] = 0.f;
-      if (reset_u) u[q * d + i] = 0.f;
+      v[sv.at(q, i)] = 0.f;
+      if (reset_u) u[sv.at(q, i)] = 0.f;
     }
   }
 }
 
 __global__ void __launch_bounds__(kBlock) k_gather_reset_dyn(const int32_t* __restrict__ idx, int64_t k,
                                                              float* __restrict__ u, float* __restrict__ v,
-                                                             float* __restrict__ values, int64_t d, int reset_u,
+                                                             float* __restrict__ values, StateView sv, int reset_u,
                                                              int P) {
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < k; t += stride) {
     const int64_t i = idx[t];
     float x[kMaxWorkers];
-    for (int q = 0; q < P; ++q) x[q] = v[q * d + i];
+    for (int q = 0; q < P; ++q) x[q] = v[sv.at(q, i)];
     values[t] = tree_sum_dyn(x, P);
     for (int q = 0; q < P; ++q) {
-      v[q * d + i] = 0.f;
-      if (reset_u) u[q * d + i] = 0.f;
+      v[sv.at(q, i)] = 0.f;
+      if (reset_u) u[sv.at(q, i)] = 0.f;
     }
   }
 }
@@ -201,7 +277,37 @@ __global__ void __launch_bounds__(kBlock) k_apply_update(const int32_t* __restri
 // ------------------------------------------------------------------------------------
 // Launchers
 
+namespace {
+hipError_t launch_accumulate_il(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v) {
+  const int P = x->P, PP = x->state_stride;
+  int64_t done = 0;
+  if (P % 4 == 0 && P <= 16 && aligned16(u) && aligned16(v)) {
+    const int G = P / 4;
+    const int64_t cw = 64 / G;
+    const int64_t nch = x->d / cw;
+    if (nch > 0) {
+      // about four chunks per wave (the most loads in flight measured best on the 25.6M x 8 stream)
+      const dim3 grid(grid_for(nch, 4 * (kBlock / 64), 64 * x->num_cus)), block(kBlock);
+      switch (G) {
+        case 1: hipLaunchKernelGGL(k_accumulate_il<1>, grid, block, 0, s, g, u, v, x->d, x->rho); break;
+        case 2: hipLaunchKernelGGL(k_accumulate_il<2>, grid, block, 0, s, g, u, v, x->d, x->rho); break;
+        case 3: hipLaunchKernelGGL(k_accumulate_il<3>, grid, block, 0, s, g, u, v, x->d, x->rho); break;
+        default: hipLaunchKernelGGL(k_accumulate_il<4>, grid, block, 0, s, g, u, v, x->d, x->rho); break;
+      }
+      done = nch * cw;
+    }
+  }
+  if (done < x->d) {
+    const int64_t n = (x->d - done) * P;
+    hipLaunchKernelGGL(k_accumulate_il_any, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, g, u, v,
+                       x->d, P, PP, x->rho, done);
+  }
+  return hipGetLastError();
+}
+}  // namespace
+
 hipError_t launch_accumulate(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v) {
+  if (x->state_layout == GS_STATE_INTERLEAVED) return launch_accumulate_il(x, s, g, u, v);
   const int64_t n = (int64_t)x->P * x->d;
   if (aligned16(g) && aligned16(u) && aligned16(v)) {
     const int64_t n4 = n / 4;
@@ -227,16 +333,16 @@ hipError_t launch_fill_zero(hipStream_t s, float* p, int64_t n) {
   return hipGetLastError();
 }
 
-hipError_t launch_sketch_acc(const gs_ctx* x, hipStream_t s, const float* v) {
+hipError_t launch_sketch_acc(const gs_ctx* x, hipStream_t s, const float* v, StateView sv) {
   const int64_t n = (int64_t)x->P * x->r * x->c;
   hipLaunchKernelGGL(k_zero64, dim3(grid_for(n, kBlock, 2048)), dim3(kBlock), 0, s, x->acc64, n);
   hipLaunchKernelGGL(k_sketch_atomic, dim3(grid_for(x->d, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, x->hs, v,
-                     x->acc64, x->d, x->P);
+                     x->acc64, x->d, x->P, sv);
   return hipGetLastError();
 }
 
-hipError_t launch_sketch(const gs_ctx* x, hipStream_t s, const float* v, float* tables) {
-  hipError_t e = launch_sketch_acc(x, s, v);
+hipError_t launch_sketch(const gs_ctx* x, hipStream_t s, const float* v, StateView sv, float* tables) {
+  hipError_t e = launch_sketch_acc(x, s, v, sv);
   if (e != hipSuccess) return e;
   const int64_t n = (int64_t)x->P * x->r * x->c;
   hipLaunchKernelGGL(k_round_tables, dim3(grid_for(n, kBlock, 2048)), dim3(kBlock), 0, s, x->acc64, tables, n);
@@ -277,14 +383,15 @@ hipError_t launch_gather_reset(const gs_ctx* x, hipStream_t s, const int32_t* id
                                float* values) {
   const dim3 grid(grid_for(k, kBlock, 4 * x->num_cus)), block(kBlock);
   const int ru = x->reset_momentum ? 1 : 0;
+  const StateView sv = state_view(x);
   switch (x->P) {
 #define GS_GATHER_CASE(PP) \
-  case PP: hipLaunchKernelGGL(k_gather_reset<PP>, grid, block, 0, s, idx, k, u, v, values, x->d, ru); break;
+  case PP: hipLaunchKernelGGL(k_gather_reset<PP>, grid, block, 0, s, idx, k, u, v, values, sv, ru); break;
     GS_GATHER_CASE(1) GS_GATHER_CASE(2) GS_GATHER_CASE(3) GS_GATHER_CASE(4) GS_GATHER_CASE(5) GS_GATHER_CASE(6)
     GS_GATHER_CASE(7) GS_GATHER_CASE(8) GS_GATHER_CASE(9) GS_GATHER_CASE(10) GS_GATHER_CASE(11) GS_GATHER_CASE(12)
     GS_GATHER_CASE(13) GS_GATHER_CASE(14) GS_GATHER_CASE(15) GS_GATHER_CASE(16)
 #undef GS_GATHER_CASE
-    default: hipLaunchKernelGGL(k_gather_reset_dyn, grid, block, 0, s, idx, k, u, v, values, x->d, ru, x->P); break;
+    default: hipLaunchKernelGGL(k_gather_reset_dyn, grid, block, 0, s, idx, k, u, v, values, sv, ru, x->P); break;
   }
   return hipGetLastError();
 }

@@ -87,16 +87,25 @@ def check_topk_of(est, idx, k, what):
 class Dev:
     """GPU buffers and a context for one workload shape."""
 
-    def __init__(self, d, P, r, c, k, hp, rho=0.9, reset_momentum=True):
+    def __init__(self, d, P, r, c, k, hp, rho=0.9, reset_momentum=True, layout="worker_major"):
         self.d, self.P, self.r, self.c, self.k = d, P, r, c, k
         self.hp = hp
-        self.ctx = gs.GsContext(d, P, r, c, k, hp, rho=rho, reset_momentum=reset_momentum)
+        self.ctx = gs.GsContext(d, P, r, c, k, hp, rho=rho, reset_momentum=reset_momentum, state_layout=layout)
         f32 = dict(dtype=torch.float32, device=DEV)
         self.tables = torch.empty((P, r, c), **f32)
         self.merged = torch.empty((r, c), **f32)
         self.est = torch.empty(d, **f32)
         self.idx = torch.empty(k, dtype=torch.int32, device=DEV)
         self.values = torch.empty(k, **f32)
+
+    def state(self, a):
+        """A [P][d] host array as a device state tensor in the context's layout."""
+        return self.ctx.to_state(to_dev(a))
+
+    def unstate(self, t):
+        """A device state tensor back as a [P][d] host array."""
+        torch.cuda.synchronize()
+        return self.ctx.from_state(t).cpu().numpy()
 
     def close(self):
         self.ctx.close()
@@ -109,12 +118,12 @@ def chain_check(dv: Dev, g, u0, v0, k, rho, reset_momentum=True, full_tables=Tru
     after the step (for re-syncing the next one)."""
     hp, c, d, P = dv.hp, dv.c, dv.d, dv.P
     _flush(f"[{label}] accumulate")
-    u_d, v_d, g_d = to_dev(u0), to_dev(v0), to_dev(g)
+    u_d, v_d, g_d = dv.state(u0), dv.state(v0), to_dev(g)
     dv.ctx.accumulate(g_d, u_d, v_d)
     u1, v1 = u0.copy(), v0.copy()
     oracle.accumulate(g, u1, v1, rho)
-    assert np.array_equal(host(u_d), u1), f"{label}: u after accumulate not bit-exact"
-    assert np.array_equal(host(v_d), v1), f"{label}: v after accumulate not bit-exact"
+    assert np.array_equal(dv.unstate(u_d), u1), f"{label}: u after accumulate not bit-exact"
+    assert np.array_equal(dv.unstate(v_d), v1), f"{label}: v after accumulate not bit-exact"
 
     _flush(f"[{label}] sketch")
     dv.ctx.sketch(v_d, dv.tables)
@@ -166,12 +175,12 @@ def chain_check(dv: Dev, g, u0, v0, k, rho, reset_momentum=True, full_tables=Tru
     vals_o = oracle.gather_reset(ref_idx, u2, v2, reset_momentum)
     dv.ctx.gather_reset(dv.idx[:k], k, u_d, v_d, dv.values[:k])
     assert np.array_equal(host(dv.values)[:k], vals_o), f"{label}: gathered values not bit-exact"
-    assert np.array_equal(host(u_d), u2), f"{label}: u after reset not bit-exact"
-    assert np.array_equal(host(v_d), v2), f"{label}: v after reset not bit-exact"
+    assert np.array_equal(dv.unstate(u_d), u2), f"{label}: u after reset not bit-exact"
+    assert np.array_equal(dv.unstate(v_d), v2), f"{label}: v after reset not bit-exact"
 
     if fused:
         _flush(f"[{label}] fused step")
-        uf, vf = to_dev(u0), to_dev(v0)
+        uf, vf = dv.state(u0), dv.state(v0)
         dv.ctx.step(g_d, uf, vf, k, dv.merged, dv.idx[:k], dv.values[:k])
         mf, jf, valf = host(dv.merged), host(dv.idx)[:k], host(dv.values)[:k]
         assert_tol(mf, mg, f"{label}: fused merged sketch vs separate calls")
@@ -187,7 +196,7 @@ def chain_check(dv: Dev, g, u0, v0, k, rho, reset_momentum=True, full_tables=Tru
         # values: exact tree sums of the accumulated v at the fused selection
         uc, vc = u1.copy(), v1.copy()
         assert np.array_equal(valf, oracle.gather_reset(jf, uc, vc, reset_momentum)), f"{label}: fused values"
-        uh, vh = host(uf), host(vf)
+        uh, vh = dv.unstate(uf), dv.unstate(vf)
         mask = np.zeros(d, bool)
         mask[jf] = True
         assert np.all(vh[:, mask] == 0) and np.array_equal(vh[:, ~mask], v1[:, ~mask]), f"{label}: fused v reset"
@@ -303,6 +312,8 @@ EDGE = [
     (4099, 6, 3, 64, 100),      # P = 6 tree, ragged d
     (10_007, 7, 7, 211, 500),   # P = 7 tree, r = 7
     (3001, 17, 5, 97, 60),      # P beyond the unrolled instances
+    (5_003, 12, 5, 300, 50),    # P = 9..12: three pull lanes per entry (256 threads leave one idle)
+    (6_007, 9, 3, 257, 33),
     (100_003, 1, 1, 30_011, 7), # r = 1: one signed lookup
     (65_536, 2, 16, 4096, 655), # maximum r
     (20_000, 2, 3, 500, 19_999),  # k near d: the sampled pruning bound admits fewer than k
