@@ -245,7 +245,7 @@ gs_status gs_sketch(gs_ctx* x, void* stream, const float* v, float* tables) {
       rows = gs::pull_rows_of_state(x, s, v, &e);
     else
       e = gs::launch_interleave(x, s, v);
-    if (e == hipSuccess) e = gs::launch_pull(x, s, rows);
+    if (e == hipSuccess) e = gs::launch_pull(x, s, rows, nullptr, tables);
     if (e == hipSuccess) e = gs::launch_merge_partials(x, s, nullptr, tables);
   } else {
     e = gs::launch_sketch(x, s, v, gs::state_view(x), tables);
@@ -296,7 +296,7 @@ static hipError_t launch_sketch_phase(gs_ctx* x, hipStream_t s, const float* g, 
       e = gs::launch_accumulate_vi(x, s, g, u, v);
     }
     mark(1);
-    if (e == hipSuccess) e = gs::launch_pull(x, s, rows);
+    if (e == hipSuccess) e = gs::launch_pull(x, s, rows, merged, nullptr);
     mark(2);
     if (e == hipSuccess) e = gs::launch_merge_partials(x, s, merged, nullptr);
   } else {
@@ -371,7 +371,7 @@ gs_status gs_step_sketch_momentum(gs_ctx* x, void* stream, const float* g, float
   if (x->use_pull) {
     e = gs::launch_interleave(x, s, g);
     gs::stage_mark(x, s, 1);
-    if (e == hipSuccess) e = gs::launch_pull(x, s, x->vI);
+    if (e == hipSuccess) e = gs::launch_pull(x, s, x->vI, merged, nullptr);
     gs::stage_mark(x, s, 2);
     if (e == hipSuccess) e = gs::launch_merge_partials(x, s, merged, nullptr);
   } else {

@@ -143,8 +143,12 @@ hipError_t build_pull_lists(gs_ctx* x);
 hipError_t launch_accumulate_vi(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v);
 hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v);
 // The pull gathers rows of PP floats (16-byte aligned) from `rows`: the context's interleaved
-// copy x->vI, or the caller's v itself when the state is interleaved.
-hipError_t launch_pull(const gs_ctx* x, hipStream_t s, const float* rows);
+// copy x->vI, or the caller's v itself when the state is interleaved. When pull_merges(x)
+// (P <= 16 and one list segment per tile) it also writes the per-worker tables and/or the
+// merged sketch (non-null outputs) and launch_merge_partials has nothing left to do; pass
+// the same outputs to both.
+hipError_t launch_pull(const gs_ctx* x, hipStream_t s, const float* rows, float* merged, float* tables);
+bool pull_merges(const gs_ctx* x);
 // Rows for the pull from the caller's state array v (GS_STATE_INTERLEAVED): v itself when it
 // is 16-byte aligned, otherwise a copy enqueued into x->vI.
 const float* pull_rows_of_state(const gs_ctx* x, hipStream_t s, const float* v, hipError_t* e);

@@ -244,10 +244,15 @@ __device__ __forceinline__ void load_row(const float* __restrict__ vI, uint32_t 
 
 // L = PP/4 adjacent lanes share one list entry; lane `sub` of the group gathers workers
 // [4 sub, 4 sub + 4) of the row (16 B) and adds them into the tile.
+// With one list segment per tile (S = 1) the tile holds every worker's complete fp64 cell
+// sums, so it rounds them itself: tables[q] (when non-null) and the tree-order merge into
+// `merged` (when non-null) are written directly, and the fp64 partials are not. Otherwise
+// (S > 1, or both outputs null) the partials go to `partial` for k_merge_partials.
 template <int P, int U>
 __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
                                                      const int64_t* __restrict__ off, const float* __restrict__ vI,
-                                                     double* __restrict__ partial) {
+                                                     double* __restrict__ partial, float* __restrict__ merged,
+                                                     float* __restrict__ tables) {
   extern __shared__ double acc[];  // [P][W]: worker-major, so lanes adding for one worker hit spread banks
   constexpr int PP = (P + 3) & ~3;
   constexpr int L = PP / 4;
@@ -299,6 +304,20 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   }
   __syncthreads();
   const int64_t rc = (int64_t)hs.r * hs.c;
+  if (pl.S == 1 && (merged || tables)) {
+    const int64_t cell0 = (int64_t)j * hs.c + col0;
+    for (int64_t o = threadIdx.x; o < wt; o += kPullBlock) {
+      float x[P];
+#pragma unroll
+      for (int q = 0; q < P; ++q) x[q] = (float)acc[q * wt + o];
+      if (tables) {
+#pragma unroll
+        for (int q = 0; q < P; ++q) tables[q * rc + cell0 + o] = x[q];
+      }
+      if (merged) merged[cell0 + o] = tree_sum<P>(x);
+    }
+    return;
+  }
   double* dst = partial + s * P * rc + (int64_t)j * hs.c + col0;
   for (int64_t e = threadIdx.x; e < wt * P; e += kPullBlock) {
     const int64_t q = e / wt, o = e - q * wt;
@@ -387,10 +406,11 @@ hipError_t launch_acc_vi_p(const gs_ctx* x, hipStream_t s, const float* g, float
 }
 
 template <int P>
-void launch_pull_p(const gs_ctx* x, hipStream_t s, const float* rows) {
+void launch_pull_p(const gs_ctx* x, hipStream_t s, const float* rows, float* merged, float* tables) {
   const PullPlan& pl = x->plan;
   hipLaunchKernelGGL((k_pull<P, kPullUnroll>), dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kPullBlock),
-                     (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, rows, x->partial);
+                     (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, rows, x->partial,
+                     merged, tables);
 }
 
 template <int P>
@@ -520,10 +540,10 @@ hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v) {
   return hipGetLastError();
 }
 
-hipError_t launch_pull(const gs_ctx* x, hipStream_t s, const float* rows) {
+hipError_t launch_pull(const gs_ctx* x, hipStream_t s, const float* rows, float* merged, float* tables) {
   switch (x->P) {
 #define GS_PULL_CASE(PP) \
-  case PP: launch_pull_p<PP>(x, s, rows); break;
+  case PP: launch_pull_p<PP>(x, s, rows, merged, tables); break;
     GS_PULL_CASE(1) GS_PULL_CASE(2) GS_PULL_CASE(3) GS_PULL_CASE(4) GS_PULL_CASE(5) GS_PULL_CASE(6) GS_PULL_CASE(7)
     GS_PULL_CASE(8) GS_PULL_CASE(9) GS_PULL_CASE(10) GS_PULL_CASE(11) GS_PULL_CASE(12) GS_PULL_CASE(13)
     GS_PULL_CASE(14) GS_PULL_CASE(15) GS_PULL_CASE(16)
@@ -549,7 +569,10 @@ const float* pull_rows_of_state(const gs_ctx* x, hipStream_t s, const float* v, 
   return x->vI;
 }
 
+bool pull_merges(const gs_ctx* x) { return x->P <= 16 && x->plan.S == 1; }
+
 hipError_t launch_merge_partials(const gs_ctx* x, hipStream_t s, float* merged, float* tables) {
+  if (pull_merges(x)) return hipSuccess;  // the pull wrote merged / tables itself
   const int64_t rc = (int64_t)x->r * x->c;
   const dim3 grid(grid_for(rc, kBlock, 8 * x->num_cus)), block(kBlock);
   const int S = x->plan.S;
