@@ -45,8 +45,9 @@ hipError_t alloc(T** p, int64_t count) {
 }
 
 void free_scratch(gs_ctx* x) {
-  void* ptrs[] = {x->keys, x->hist, x->hist2, x->ctl, x->cand_key, x->cand_idx, x->bitmap, x->blockcnt, x->acc64,
-                  x->list, x->tile_off, x->vI, x->partial, x->sample_keys, x->heavy, x->l2buf, x->coarse};
+  void* ptrs[] = {x->keys, x->hist,   x->hist2, x->ctl,     x->cand_key,    x->cand_idx, x->bitmap,
+                  x->blockcnt, x->acc64, x->list, x->codes, x->tile_off, x->vI, x->partial,
+                  x->sample_keys, x->heavy, x->l2buf, x->coarse};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   x->keys = nullptr;
@@ -59,6 +60,7 @@ void free_scratch(gs_ctx* x) {
   x->blockcnt = nullptr;
   x->acc64 = nullptr;
   x->list = nullptr;
+  x->codes = nullptr;
   x->tile_off = nullptr;
   x->vI = nullptr;
   x->partial = nullptr;
@@ -180,7 +182,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
     x->l2_half = (int64_t)x->r * (npad > 2048 ? npad / 2048 : 1);
     chk(alloc(&x->l2buf, 2 * x->l2_half));
   }
-  x->plan = gs::make_pull_plan(x->d, x->P, x->r, x->c, x->num_cus);
+  x->plan = gs::make_pull_plan(x->hs, x->d, x->P, x->r, x->c, x->num_cus);
   x->use_pull = (int64_t)x->plan.T * (int64_t)sizeof(uint32_t) <= gs::kMaxFillLds;
   {
     // diagnostic override: GS_SKETCH_PATH=atomic selects the fp64-atomic sketch for any plan
@@ -189,6 +191,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   }
   if (x->use_pull) {
     chk(alloc(&x->list, (int64_t)x->r * x->d));
+    chk(alloc(&x->codes, (int64_t)x->r * x->d));
     chk(alloc(&x->tile_off, (int64_t)x->plan.T + 1));
     chk(alloc(&x->vI, x->d * x->plan.PP));
     chk(alloc(&x->partial, (int64_t)x->plan.S * x->r * x->c * x->P));

@@ -36,6 +36,13 @@ struct SelectCtl {
 constexpr int kSampleMax = 16384;  // sampled estimates for the pruning bound
 
 // Geometry of the gather-based sketch: tiles of W columns of one row, all P workers, fp64.
+// The columns of row j are taken in the order of their scaled position t = theta_j * col
+// mod c (theta_j coprime to c, so this is a permutation of the columns), and tile k of the
+// row holds the columns with t in [k W, (k + 1) W). The bucket hash is affine, so
+// consecutive coordinates' columns differ by one of two constants (a_j mod c, or that less
+// p mod c when the raw hash wraps past p); theta_j is chosen to make both steps small in t,
+// so consecutive coordinates mostly share a tile and a 128-byte line of the state mostly
+// feeds one tile per row.
 struct PullPlan {
   int32_t P, PP;          // workers; vI row length (P rounded up to a multiple of 4)
   int32_t W;              // columns per tile
@@ -43,7 +50,10 @@ struct PullPlan {
   int32_t T;              // r * tiles_per_row
   int32_t S;              // list segments per tile (work items = T * S)
   int32_t NB;             // build chunks
+  int32_t slots;          // resident pull workgroups (one per CU): the size of a round
   int64_t chunk;          // coordinates per build chunk
+  uint32_t theta[kMaxRows];      // column scaling of row j
+  uint32_t theta_inv[kMaxRows];  // its inverse modulo c (position t -> column)
 };
 constexpr int64_t kMaxFillLds = 160 * 1024;  // LDS of the list-fill kernel holds T cursors
 
@@ -91,6 +101,7 @@ struct gs_ctx {
   bool use_pull = false;
   gs::PullPlan plan{};
   uint32_t* list = nullptr;       // [r*d] coordinates of each tile, ascending
+  uint16_t* codes = nullptr;      // [r*d] per list entry: position in the tile | sign << 15
   int64_t* tile_off = nullptr;    // [T+1]
   float* vI = nullptr;            // [d][PP] worker-interleaved accumulators
   double* partial = nullptr;      // [S][r][c][P] fp64 tile sums
@@ -138,7 +149,7 @@ hipError_t launch_gather_reset(const gs_ctx* x, hipStream_t s, const int32_t* id
                                float* values);
 int64_t emit_blocks_for(int64_t d);
 hipError_t prepare_prune(gs_ctx* x);
-PullPlan make_pull_plan(int64_t d, int32_t P, int32_t r, int64_t c, int num_cus);
+PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int64_t c, int num_cus);
 hipError_t build_pull_lists(gs_ctx* x);
 hipError_t launch_accumulate_vi(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v);
 hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v);

@@ -32,10 +32,32 @@ int grid_for(int64_t work_items, int per_block, int cap) {
   return (int)b;
 }
 
-__device__ __forceinline__ void tile_of(const HashSet& hs, const PullPlan& pl, int j, uint32_t i, uint32_t& col,
+// The tile of entry (j, i) and the entry's position in it (the scaled column t = theta_j *
+// col mod c, less the tile's first position), and the sign as a float sign-bit mask.
+__device__ __forceinline__ void tile_of(const HashSet& hs, const PullPlan& pl, int j, uint32_t i, uint32_t& pos,
                                         uint32_t& sflip, uint32_t& tile) {
+  uint32_t col;
   hash_ij(hs, j, i, col, sflip);
-  tile = (uint32_t)j * pl.tiles_per_row + col / (uint32_t)pl.W;
+  const uint32_t t = (uint32_t)(((uint64_t)pl.theta[j] * col) % hs.c);
+  const uint32_t k = t / (uint32_t)pl.W;
+  tile = (uint32_t)j * pl.tiles_per_row + k;
+  pos = t - k * (uint32_t)pl.W;
+}
+
+// Work item of pull workgroup b (of n): the workgroups of one round (`slots` resident at a
+// time, one per CU) are dealt to the 8 XCDs in turn (b mod 8), so each XCD is given a
+// contiguous run of the round's items, i.e. neighbouring tiles of one row. A 128-byte line
+// of the state then feeds one XCD per row instead of one per tile it touches.
+__device__ __forceinline__ int64_t grouped_item(int64_t b, int64_t n, int64_t slots) {
+  const int64_t r0 = (b / slots) * slots;
+  const int64_t nr = min(slots, n - r0);
+  const int64_t w = b - r0, x = w % 8, q = nr / 8, rem = nr % 8;
+  return r0 + x * q + min(x, rem) + w / 8;
+}
+
+// Column of position `pos` of tile k of row j (the inverse scaling).
+__device__ __forceinline__ uint32_t column_at(const HashSet& hs, const PullPlan& pl, int j, int64_t k, int64_t pos) {
+  return (uint32_t)(((uint64_t)pl.theta_inv[j] * (uint64_t)(k * pl.W + pos)) % hs.c);
 }
 
 // ------------------------------------------------------------------------------------
@@ -48,8 +70,8 @@ __global__ void __launch_bounds__(kBlock) k_build_count(HashSet hs, PullPlan pl,
   const int64_t lo = b * pl.chunk, hi = min(d, lo + pl.chunk);
   for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock) {
     for (int j = 0; j < hs.r; ++j) {
-      uint32_t col, sflip, t;
-      tile_of(hs, pl, j, (uint32_t)i, col, sflip, t);
+      uint32_t pos, sflip, t;
+      tile_of(hs, pl, j, (uint32_t)i, pos, sflip, t);
       atomicAdd(&counts[b * pl.T + t], 1u);
     }
   }
@@ -101,7 +123,8 @@ __global__ void __launch_bounds__(1024) k_build_offsets(PullPlan pl, const uint3
 // tile's list comes out sorted by coordinate.
 __global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int64_t d,
                                                    const uint32_t* __restrict__ prefix,
-                                                   const int64_t* __restrict__ off, uint32_t* __restrict__ list) {
+                                                   const int64_t* __restrict__ off, uint32_t* __restrict__ list,
+                                                   uint16_t* __restrict__ codes) {
   extern __shared__ uint32_t cursor[];  // [T]
   const int64_t b = blockIdx.x;
   const int lane = threadIdx.x;
@@ -112,8 +135,8 @@ __global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int6
     const int64_t i = base + lane;
     const bool valid = i < hi;
     for (int j = 0; j < hs.r; ++j) {
-      uint32_t col = 0, sflip = 0, t = 0;
-      if (valid) tile_of(hs, pl, j, (uint32_t)i, col, sflip, t);
+      uint32_t pos = 0, sflip = 0, t = 0;
+      if (valid) tile_of(hs, pl, j, (uint32_t)i, pos, sflip, t);
       uint32_t slot = 0;
       for (int l = 0; l < 64; ++l) {
         if (lane == l && valid) {
@@ -122,7 +145,10 @@ __global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int6
         }
         __builtin_amdgcn_wave_barrier();
       }
-      if (valid) list[off[t] + slot] = (uint32_t)i;
+      if (valid) {
+        list[off[t] + slot] = (uint32_t)i;
+        codes[off[t] + slot] = (uint16_t)(pos | (sflip >> 16));  // position < 2^15; sign in bit 15
+      }
     }
   }
 }
@@ -250,6 +276,7 @@ __device__ __forceinline__ void load_row(const float* __restrict__ vI, uint32_t 
 // (S > 1, or both outputs null) the partials go to `partial` for k_merge_partials.
 template <int P, int U>
 __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
+                                                     const uint16_t* __restrict__ codes,
                                                      const int64_t* __restrict__ off, const float* __restrict__ vI,
                                                      double* __restrict__ partial, float* __restrict__ merged,
                                                      float* __restrict__ tables) {
@@ -259,32 +286,33 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   constexpr int64_t B = kPullBlock / L;  // entries per block pass
   const int sub = threadIdx.x % L;
   const int64_t tid = threadIdx.x / L;
-  const int64_t item = blockIdx.x;
+  const int64_t item = grouped_item(blockIdx.x, gridDim.x, pl.slots);
   const int64_t t = item / pl.S, s = item - t * pl.S;
   const int j = (int)(t / pl.tiles_per_row);
-  const RowConst k = row_const(hs, j);
-  const int64_t col0 = (t - (int64_t)j * pl.tiles_per_row) * pl.W;
-  const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - col0);
+  const int64_t kt = t - (int64_t)j * pl.tiles_per_row;
+  const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - kt * pl.W);
   for (int64_t e = threadIdx.x; e < wt * P; e += kPullBlock) acc[e] = 0.0;
   __syncthreads();
   const int64_t lo = off[t], n = off[t + 1] - lo;
   const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
-  double* const mycol = acc + (int64_t)(4 * sub) * wt - col0;
+  double* const mycol = acc + (int64_t)(4 * sub) * wt;
   // when L does not divide the block (L = 3: 85 groups of 3 lanes), the last lane has no
   // group: it takes no entry (its would be the next pass's first)
   int64_t eb = tid < B ? e0 + tid : e1;
   for (; eb + (U - 1) * B < e1; eb += U * B) {
-    uint32_t i[U];
+    uint32_t i[U], code[U];
 #pragma unroll
-    for (int m = 0; m < U; ++m) i[m] = list[eb + m * B];
+    for (int m = 0; m < U; ++m) {
+      i[m] = list[eb + m * B];
+      code[m] = codes[eb + m * B];
+    }
     f4 x[U];
 #pragma unroll
     for (int m = 0; m < U; ++m) x[m] = reinterpret_cast<const f4*>(vI + (int64_t)i[m] * PP)[sub];
 #pragma unroll
     for (int m = 0; m < U; ++m) {
-      uint32_t col, sflip;
-      hash_row(k, i[m], col, sflip);
-      double* cell = mycol + col;
+      double* cell = mycol + (code[m] & 0x7fffu);
+      const uint32_t sflip = (code[m] & 0x8000u) << 16;
       const float xs[4] = {x[m].x, x[m].y, x[m].z, x[m].w};
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -292,86 +320,111 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
     }
   }
   for (; eb < e1; eb += B) {
-    const uint32_t i = list[eb];
+    const uint32_t i = list[eb], code = codes[eb];
     const f4 x = reinterpret_cast<const f4*>(vI + (int64_t)i * PP)[sub];
-    uint32_t col, sflip;
-    hash_row(k, i, col, sflip);
-    double* cell = mycol + col;
+    double* cell = mycol + (code & 0x7fffu);
+    const uint32_t sflip = (code & 0x8000u) << 16;
     const float xs[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       if (P % 4 == 0 || 4 * sub + q < P) atomicAdd(cell + q * wt, (double)apply_sign(xs[q], sflip));
   }
   __syncthreads();
+  // write out: tile position o holds column theta_inv_j * (kt W + o) mod c; along the
+  // block-stride loop that column advances by (256 theta_inv_j) mod c
   const int64_t rc = (int64_t)hs.r * hs.c;
+  const uint32_t c = hs.c;
+  const uint32_t cstep = (uint32_t)(((uint64_t)pl.theta_inv[j] * kPullBlock) % c);
+  uint32_t col = threadIdx.x < wt ? column_at(hs, pl, j, kt, threadIdx.x) : 0u;
+  const int64_t row0 = (int64_t)j * c;
   if (pl.S == 1 && (merged || tables)) {
-    const int64_t cell0 = (int64_t)j * hs.c + col0;
     for (int64_t o = threadIdx.x; o < wt; o += kPullBlock) {
       float x[P];
 #pragma unroll
       for (int q = 0; q < P; ++q) x[q] = (float)acc[q * wt + o];
       if (tables) {
 #pragma unroll
-        for (int q = 0; q < P; ++q) tables[q * rc + cell0 + o] = x[q];
+        for (int q = 0; q < P; ++q) tables[q * rc + row0 + col] = x[q];
       }
-      if (merged) merged[cell0 + o] = tree_sum<P>(x);
+      if (merged) merged[row0 + col] = tree_sum<P>(x);
+      col = col + cstep >= c ? col + cstep - c : col + cstep;
     }
     return;
   }
-  double* dst = partial + s * P * rc + (int64_t)j * hs.c + col0;
-  for (int64_t e = threadIdx.x; e < wt * P; e += kPullBlock) {
-    const int64_t q = e / wt, o = e - q * wt;
-    dst[q * rc + o] = acc[e];
+  double* dst = partial + s * P * rc + row0;
+  for (int64_t o = threadIdx.x; o < wt; o += kPullBlock) {
+#pragma unroll
+    for (int q = 0; q < P; ++q) dst[q * rc + col] = acc[q * wt + o];
+    col = col + cstep >= c ? col + cstep - c : col + cstep;
   }
 }
 
 // Runtime-P variant (P > 16): rows of PP floats read element by element.
 __global__ void __launch_bounds__(kBlock) k_pull_any(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
+                                                     const uint16_t* __restrict__ codes,
                                                      const int64_t* __restrict__ off, const float* __restrict__ vI,
                                                      double* __restrict__ partial) {
   extern __shared__ double acc[];
   const int P = pl.P, PP = pl.PP;
-  const int64_t item = blockIdx.x;
+  const int64_t item = grouped_item(blockIdx.x, gridDim.x, pl.slots);
   const int64_t t = item / pl.S, s = item - t * pl.S;
   const int j = (int)(t / pl.tiles_per_row);
-  const int64_t col0 = (t - (int64_t)j * pl.tiles_per_row) * pl.W;
-  const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - col0);
+  const int64_t kt = t - (int64_t)j * pl.tiles_per_row;
+  const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - kt * pl.W);
   for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) acc[e] = 0.0;
   __syncthreads();
   const int64_t lo = off[t], n = off[t + 1] - lo;
   const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
-  const RowConst k = row_const(hs, j);
   for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
-    const uint32_t i = list[e];
-    uint32_t col, sflip;
-    hash_row(k, i, col, sflip);
-    double* cell = acc + (col - col0);
+    const uint32_t i = list[e], code = codes[e];
+    double* cell = acc + (code & 0x7fffu);
+    const uint32_t sflip = (code & 0x8000u) << 16;
     for (int q = 0; q < P; ++q) atomicAdd(cell + q * wt, (double)apply_sign(vI[(int64_t)i * PP + q], sflip));
   }
   __syncthreads();
   const int64_t rc = (int64_t)hs.r * hs.c;
-  double* dst = partial + s * P * rc + (int64_t)j * hs.c + col0;
-  for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) {
-    const int64_t q = e / wt, o = e - q * wt;
-    dst[q * rc + o] = acc[e];
+  const uint32_t c = hs.c;
+  const uint32_t cstep = (uint32_t)(((uint64_t)pl.theta_inv[j] * kBlock) % c);
+  uint32_t col = threadIdx.x < wt ? column_at(hs, pl, j, kt, threadIdx.x) : 0u;
+  double* dst = partial + s * P * rc + (int64_t)j * c;
+  for (int64_t o = threadIdx.x; o < wt; o += kBlock) {
+    for (int q = 0; q < P; ++q) dst[q * rc + col] = acc[q * wt + o];
+    col = col + cstep >= c ? col + cstep - c : col + cstep;
   }
 }
 
 // ------------------------------------------------------------------------------------
 // Segment sum + single rounding + tree merge. partial is [S][P][r][c] fp64.
 
+// Segments are added in ascending order per worker; the P sums are independent chains and
+// the segment loop is unrolled, so many loads are in flight per lane (small sketches have
+// tens of segments).
 template <int P>
 __global__ void __launch_bounds__(kBlock) k_merge_partials(const double* __restrict__ partial, int S, int64_t rc,
                                                            float* __restrict__ merged, float* __restrict__ tables) {
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < rc; e += stride) {
+    double a[P];
+#pragma unroll
+    for (int q = 0; q < P; ++q) a[q] = partial[q * rc + e];
+    int s = 1;
+    for (; s + 3 < S; s += 4) {
+      double y[4][P];
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int q = 0; q < P; ++q) y[m][q] = partial[((int64_t)(s + m) * P + q) * rc + e];
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int q = 0; q < P; ++q) a[q] += y[m][q];
+    }
+    for (; s < S; ++s)
+#pragma unroll
+      for (int q = 0; q < P; ++q) a[q] += partial[((int64_t)s * P + q) * rc + e];
     float x[P];
 #pragma unroll
-    for (int q = 0; q < P; ++q) {
-      double a = partial[q * rc + e];
-      for (int s = 1; s < S; ++s) a += partial[((int64_t)s * P + q) * rc + e];
-      x[q] = (float)a;
-    }
+    for (int q = 0; q < P; ++q) x[q] = (float)a[q];
     if (tables) {
 #pragma unroll
       for (int q = 0; q < P; ++q) tables[q * rc + e] = x[q];
@@ -409,8 +462,8 @@ template <int P>
 void launch_pull_p(const gs_ctx* x, hipStream_t s, const float* rows, float* merged, float* tables) {
   const PullPlan& pl = x->plan;
   hipLaunchKernelGGL((k_pull<P, kPullUnroll>), dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kPullBlock),
-                     (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, rows, x->partial,
-                     merged, tables);
+                     (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->codes, x->tile_off, rows,
+                     x->partial, merged, tables);
 }
 
 template <int P>
@@ -423,8 +476,71 @@ hipError_t allow_pull_lds(size_t bytes) {
 
 // ------------------------------------------------------------------------------------
 
-PullPlan make_pull_plan(int64_t d, int32_t P, int32_t r, int64_t c, int num_cus) {
+namespace {
+
+// x^-1 mod m for gcd(x, m) = 1 (extended Euclid).
+uint32_t inverse_mod(uint32_t x, uint32_t m) {
+  if (m == 1) return 0;
+  int64_t r0 = m, r1 = x, t0 = 0, t1 = 1;
+  while (r1 != 0) {
+    const int64_t q = r0 / r1;
+    const int64_t r2 = r0 - q * r1, t2 = t0 - q * t1;
+    r0 = r1;
+    r1 = r2;
+    t0 = t1;
+    t1 = t2;
+  }
+  return (uint32_t)(t0 < 0 ? t0 + m : t0);
+}
+
+uint64_t gcd_u64(uint64_t a, uint64_t b) {
+  while (b) {
+    const uint64_t t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+
+// The column scaling of one row: with alpha = a mod c and beta = p mod c, consecutive
+// coordinates' columns differ by alpha, or by alpha - beta when the raw hash wraps past p
+// (a fraction f = a / p of the steps). theta (coprime to c) minimises the expected step
+// (1 - f) |theta alpha|_c + f |theta (alpha - beta)|_c of the scaled position, |x|_c being the
+// distance of x mod c to 0. The search runs over theta < min(c, 2^22) with adds only.
+uint32_t column_scaling(uint32_t a, int64_t c) {
+  if (c <= 2) return 1;
+  const uint64_t cu = (uint64_t)c;
+  const uint64_t alpha = a % cu, beta = (uint64_t)kMersenne % cu;
+  const uint64_t step2 = (alpha + cu - beta) % cu;
+  const double f = (double)a / (double)kMersenne;
+  const uint64_t limit = cu < (1ull << 22) ? cu : (1ull << 22);
+  uint64_t s1 = 0, s2 = 0;
+  double best = 1e300;
+  uint32_t best_theta = 1;
+  for (uint64_t th = 1; th < limit; ++th) {
+    s1 += alpha;
+    if (s1 >= cu) s1 -= cu;
+    s2 += step2;
+    if (s2 >= cu) s2 -= cu;
+    const double d1 = (double)(s1 < cu - s1 ? s1 : cu - s1);
+    const double d2 = (double)(s2 < cu - s2 ? s2 : cu - s2);
+    const double cost = (1.0 - f) * d1 + f * d2;
+    if (cost < best && gcd_u64(th, cu) == 1) {
+      best = cost;
+      best_theta = (uint32_t)th;
+    }
+  }
+  return best_theta;
+}
+
+}  // namespace
+
+PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int64_t c, int num_cus) {
   PullPlan pl{};
+  for (int j = 0; j < r; ++j) {
+    pl.theta[j] = column_scaling(hs.row[j].a, c);
+    pl.theta_inv[j] = inverse_mod(pl.theta[j] % (uint32_t)c, (uint32_t)c);
+  }
   pl.P = P;
   pl.PP = (P + 3) & ~3;
   // Tiles hold W columns x P workers of fp64 accumulators. Up to kTilesPerCu tiles of at
@@ -435,6 +551,7 @@ PullPlan make_pull_plan(int64_t d, int32_t P, int32_t r, int64_t c, int num_cus)
   int64_t W = max_w < 1 ? 1 : max_w;
   if (W > c) W = c;
   const int64_t slots = (int64_t)kTilesPerCu * num_cus;
+  pl.slots = (int32_t)(slots >= 8 ? slots / 8 * 8 : 8);
   int64_t tiles = (int64_t)r * ((c + W - 1) / W);
   if (tiles > slots) {
     const int64_t rounds = (tiles + slots - 1) / slots;
@@ -492,7 +609,7 @@ hipError_t build_pull_lists(gs_ctx* x) {
     hipLaunchKernelGGL(k_build_prefix, dim3((pl.T + kBlock - 1) / kBlock), dim3(kBlock), 0, 0, pl, counts, total);
     hipLaunchKernelGGL(k_build_offsets, dim3(1), dim3(1024), 0, 0, pl, total, x->tile_off);
     hipLaunchKernelGGL(k_build_fill, dim3(pl.NB), dim3(64), (size_t)pl.T * sizeof(uint32_t), 0, x->hs, pl, x->d,
-                       counts, x->tile_off, x->list);
+                       counts, x->tile_off, x->list, x->codes);
     e = hipGetLastError();
   }
   if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -551,7 +668,8 @@ hipError_t launch_pull(const gs_ctx* x, hipStream_t s, const float* rows, float*
     default: {
       const PullPlan& pl = x->plan;
       hipLaunchKernelGGL(k_pull_any, dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kBlock),
-                         (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->tile_off, rows, x->partial);
+                         (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->codes, x->tile_off, rows,
+                         x->partial);
     }
   }
   return hipGetLastError();
