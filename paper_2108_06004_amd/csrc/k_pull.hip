@@ -21,8 +21,13 @@ namespace gs {
 namespace {
 
 constexpr int kBlock = 256;
-constexpr int kPullBlock = 256;  // threads of a pull workgroup (one tile per CU, see make_pull_plan)
-constexpr int kPullUnroll = 4;   // list entries per lane group in flight
+// Threads of a pull workgroup (one tile per CU, see make_pull_plan) and list entries in
+// flight per lane group. The pull waits on L2 requests (each CU keeps a bounded number in
+// flight, and most first touches of a line miss), so it wants many gathers outstanding:
+// measured best at 512 threads and about 1,500 entries per CU (4 per group when one lane
+// takes an entry, P <= 4; 6 otherwise).
+constexpr int kPullBlock = 512;
+constexpr int pull_unroll(int P) { return P <= 4 ? 4 : 6; }
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 int grid_for(int64_t work_items, int per_block, int cap) {
@@ -461,14 +466,14 @@ hipError_t launch_acc_vi_p(const gs_ctx* x, hipStream_t s, const float* g, float
 template <int P>
 void launch_pull_p(const gs_ctx* x, hipStream_t s, const float* rows, float* merged, float* tables) {
   const PullPlan& pl = x->plan;
-  hipLaunchKernelGGL((k_pull<P, kPullUnroll>), dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kPullBlock),
+  hipLaunchKernelGGL((k_pull<P, pull_unroll(P)>), dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kPullBlock),
                      (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->codes, x->tile_off, rows,
                      x->partial, merged, tables);
 }
 
 template <int P>
 hipError_t allow_pull_lds(size_t bytes) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull<P, kPullUnroll>),
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull<P, pull_unroll(P)>),
                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
