@@ -257,6 +257,7 @@ __global__ void __launch_bounds__(kBlock) k_compact(const uint32_t* __restrict__
 // Steps 2 and 3: digits 2 and 3 of the k-th key, then the index cut among equal keys.
 
 constexpr int kSelUnroll = 8;    // candidate loads in flight per thread
+constexpr int kTieMax = 1024;    // ties at the k-th key resolved by ranking in LDS (else radix digits)
 constexpr int kStageBuf = 4096;  // per-block LDS buffer of k_digit2
 
 // Step 2: digit 2 of the keys in bucket b1 (many blocks): the digit-2 histogram (LDS per
@@ -322,6 +323,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
   __shared__ uint32_t h[2048];
   __shared__ uint32_t shw[kSelBlock / 64];
   __shared__ uint32_t res[2];
+  __shared__ uint32_t n_tie;
   const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
   const int64_t n2 = ctl->n_stage2;
   const uint32_t b1 = ctl->b1;
@@ -363,8 +365,40 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
   __syncthreads();
 
   uint32_t iota = 0x7fffffffu;
-  if (need3 < n_eq) {
-    // ascending index digits among keys equal to tau: bits 30..21, 20..10, 9..0
+  if (need3 < n_eq && n_eq <= kTieMax) {
+    // few keys equal to tau (the usual case: an estimate is one table cell): one pass
+    // collects their indices in LDS, and iota is the one with exactly need3 - 1 smaller
+    // (candidate indices are distinct)
+    if (threadIdx.x == 0) n_tie = 0u;
+    __syncthreads();
+    for (int64_t t0 = 0; t0 < n; t0 += (int64_t)kSelUnroll * kSelBlock) {
+      uint32_t key[kSelUnroll];
+#pragma unroll
+      for (int m = 0; m < kSelUnroll; ++m) {
+        const int64_t t = t0 + (int64_t)m * kSelBlock + threadIdx.x;
+        key[m] = t < n ? cand_key[t] : 0u;
+      }
+#pragma unroll
+      for (int m = 0; m < kSelUnroll; ++m) {
+        const int64_t t = t0 + (int64_t)m * kSelBlock + threadIdx.x;
+        if (t < n && key[m] == tau) {
+          const uint32_t pos = atomicAdd(&n_tie, 1u);
+          if (pos < (uint32_t)kTieMax) h[pos] = (uint32_t)cand_idx[t];
+        }
+      }
+    }
+    __syncthreads();
+    const uint32_t m_tie = min(n_tie, (uint32_t)kTieMax);  // == n_eq
+    for (uint32_t a = threadIdx.x; a < m_tie; a += kSelBlock) {
+      const uint32_t xa = h[a];
+      uint32_t rank = 0;
+      for (uint32_t b = 0; b < m_tie; ++b) rank += h[b] < xa ? 1u : 0u;
+      if (rank == need3 - 1) res[0] = xa;
+    }
+    __syncthreads();
+    iota = res[0];
+  } else if (need3 < n_eq) {
+    // many ties: ascending index digits among keys equal to tau: bits 30..21, 20..10, 9..0
     for (int b = threadIdx.x; b < 1024; b += kSelBlock) h[b] = 0u;
     __syncthreads();
     for (int64_t t = threadIdx.x; t < n; t += kSelBlock)
