@@ -290,7 +290,14 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   constexpr int L = PP / 4;
   constexpr int64_t B = kPullBlock / L;  // entries per block pass
   const int sub = threadIdx.x % L;
-  const int64_t tid = threadIdx.x / L;
+  // Lane group tid0 takes list entry tid (of each block pass). Consecutive entries of a tile
+  // are mostly consecutive coordinates at scaled positions t, t + s, t + 2s, ..., and with two
+  // lanes per entry (P = 5..8) such runs on neighbouring lanes made the LDS atomics conflict:
+  // permuting the entries within each aligned group of 32 (the entries one wave instruction
+  // covers, so the L2 requests are unchanged) took the pull from 0.885 to 0.739 ms at
+  // d = 25.6M x 8. With one or four lanes per entry the same permutation measured slower.
+  const int64_t tid0 = threadIdx.x / L;
+  const int64_t tid = (L == 2 && (tid0 | 31) < B) ? ((tid0 & ~31ll) | ((tid0 * 13 + 7) & 31)) : tid0;
   const int64_t item = grouped_item(blockIdx.x, gridDim.x, pl.slots);
   const int64_t t = item / pl.S, s = item - t * pl.S;
   const int j = (int)(t / pl.tiles_per_row);
@@ -303,7 +310,7 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   double* const mycol = acc + (int64_t)(4 * sub) * wt;
   // when L does not divide the block (L = 3: 85 groups of 3 lanes), the last lane has no
   // group: it takes no entry (its would be the next pass's first)
-  int64_t eb = tid < B ? e0 + tid : e1;
+  int64_t eb = tid0 < B ? e0 + tid : e1;
   for (; eb + (U - 1) * B < e1; eb += U * B) {
     uint32_t i[U], code[U];
 #pragma unroll
