@@ -98,8 +98,9 @@ typedef struct gs_ctx gs_ctx; /* opaque: a copy of the config plus device scratc
  * The sketch runs as a gather into LDS tiles from per-tile coordinate lists built here;
  * when those lists cannot be built (more than 40,960 tiles) it runs as fp64 device
  * atomics instead. Setting the environment variable GS_SKETCH_PATH=atomic before the call
- * selects the atomic form for any shape (a diagnostic override; results agree within the
- * table tolerance). */
+ * selects the atomic form for any shape, and GS_SKETCH_PATH=unpacked keeps the gather's
+ * lists in their unpacked form (diagnostic overrides; results agree within the table
+ * tolerance). */
 gs_status gs_create(const gs_config* cfg, gs_ctx** out);
 
 /* Free the context's scratch (after synchronizing the device). NULL is accepted. */

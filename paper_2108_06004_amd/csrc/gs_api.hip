@@ -46,7 +46,7 @@ hipError_t alloc(T** p, int64_t count) {
 
 void free_scratch(gs_ctx* x) {
   void* ptrs[] = {x->keys, x->hist,   x->hist2, x->ctl,     x->cand_key,    x->cand_idx, x->bitmap,
-                  x->blockcnt, x->acc64, x->list, x->codes, x->tile_off, x->vI, x->partial,
+                  x->blockcnt, x->acc64, x->list, x->codes, x->bases, x->tile_off, x->tile_n, x->vI, x->partial,
                   x->sample_keys, x->heavy, x->l2buf, x->coarse};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
@@ -61,7 +61,9 @@ void free_scratch(gs_ctx* x) {
   x->acc64 = nullptr;
   x->list = nullptr;
   x->codes = nullptr;
+  x->bases = nullptr;
   x->tile_off = nullptr;
+  x->tile_n = nullptr;
   x->vI = nullptr;
   x->partial = nullptr;
   x->sample_keys = nullptr;
@@ -185,14 +187,19 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   x->plan = gs::make_pull_plan(x->hs, x->d, x->P, x->r, x->c, x->num_cus);
   x->use_pull = (int64_t)x->plan.T * (int64_t)sizeof(uint32_t) <= gs::kMaxFillLds;
   {
-    // diagnostic override: GS_SKETCH_PATH=atomic selects the fp64-atomic sketch for any plan
+    // diagnostic overrides: GS_SKETCH_PATH=atomic selects the fp64-atomic sketch for any plan,
+    // GS_SKETCH_PATH=unpacked keeps the gather's lists unpacked (coordinates and codes)
     const char* path = std::getenv("GS_SKETCH_PATH");
     if (path && std::strcmp(path, "atomic") == 0) x->use_pull = false;
+    if (path && std::strcmp(path, "unpacked") == 0) x->plan.off_bits = 0;
   }
   if (x->use_pull) {
-    chk(alloc(&x->list, (int64_t)x->r * x->d));
-    chk(alloc(&x->codes, (int64_t)x->r * x->d));
+    x->list_cap = (int64_t)x->r * x->d + (int64_t)gs::kListGroup * x->plan.T;
+    chk(alloc(&x->list, x->list_cap));
+    chk(alloc(&x->codes, x->list_cap));
+    chk(alloc(&x->bases, x->list_cap / gs::kListGroup));
     chk(alloc(&x->tile_off, (int64_t)x->plan.T + 1));
+    chk(alloc(&x->tile_n, (int64_t)x->plan.T));
     chk(alloc(&x->vI, x->d * x->plan.PP));
     chk(alloc(&x->partial, (int64_t)x->plan.S * x->r * x->c * x->P));
   } else {

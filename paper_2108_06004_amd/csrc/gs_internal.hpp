@@ -54,7 +54,15 @@ struct PullPlan {
   int64_t chunk;          // coordinates per build chunk
   uint32_t theta[kMaxRows];      // column scaling of row j
   uint32_t theta_inv[kMaxRows];  // its inverse modulo c (position t -> column)
+  // Packed lists: each tile's list starts at a multiple of kListGroup entries; an entry is
+  // one word, the coordinate's offset from its group's base (the group's first coordinate)
+  // in the low off_bits bits, the position in the tile above it, the sign in bit 31. When a
+  // group's coordinates span too much for off_bits (or P > 16) the lists stay unpacked:
+  // coordinates in `list`, position | sign << 15 in `codes`.
+  int32_t packed;
+  int32_t off_bits;
 };
+constexpr int kListGroup = 64;
 constexpr int64_t kMaxFillLds = 160 * 1024;  // LDS of the list-fill kernel holds T cursors
 
 // Where element (worker q, coordinate i) of a per-worker array lives: q*qs + i*is.
@@ -100,9 +108,12 @@ struct gs_ctx {
   // gather-based sketch (used when the plan fits; otherwise fp64 atomics into acc64)
   bool use_pull = false;
   gs::PullPlan plan{};
-  uint32_t* list = nullptr;       // [r*d] coordinates of each tile, ascending
-  uint16_t* codes = nullptr;      // [r*d] per list entry: position in the tile | sign << 15
-  int64_t* tile_off = nullptr;    // [T+1]
+  uint32_t* list = nullptr;       // [list_cap] coordinates of each tile, ascending (or packed entries)
+  uint16_t* codes = nullptr;      // [list_cap] unpacked lists: position in the tile | sign << 15
+  uint32_t* bases = nullptr;      // [list_cap / kListGroup] packed lists: first coordinate of each group
+  int64_t list_cap = 0;           // r*d + kListGroup*T (tiles start at multiples of kListGroup)
+  int64_t* tile_off = nullptr;    // [T+1] tile starts in the list
+  uint32_t* tile_n = nullptr;     // [T] entries of each tile
   float* vI = nullptr;            // [d][PP] worker-interleaved accumulators
   double* partial = nullptr;      // [S][r][c][P] fp64 tile sums
   double* acc64 = nullptr;        // [P][r][c] fp64 cell accumulators of the atomic path

@@ -96,14 +96,16 @@ __global__ void __launch_bounds__(kBlock) k_build_prefix(PullPlan pl, uint32_t* 
   total[t] = run;
 }
 
-// Tile start offsets (exclusive scan of the totals) by one block; off[T] = r*d.
+// Tile start offsets by one block: each tile's list starts at a multiple of kListGroup
+// (exclusive scan of the totals rounded up); off[T] is the padded length. n[t] = total[t].
 __global__ void __launch_bounds__(1024) k_build_offsets(PullPlan pl, const uint32_t* __restrict__ total,
-                                                        int64_t* __restrict__ off) {
+                                                        int64_t* __restrict__ off, uint32_t* __restrict__ n) {
   __shared__ int64_t part[1024];
   const int64_t per = (pl.T + 1023) / 1024;
   const int64_t lo = threadIdx.x * per, hi = min((int64_t)pl.T, lo + per);
+  auto padded = [](uint32_t x) { return ((int64_t)x + kListGroup - 1) / kListGroup * kListGroup; };
   int64_t s = 0;
-  for (int64_t t = lo; t < hi; ++t) s += total[t];
+  for (int64_t t = lo; t < hi; ++t) s += padded(total[t]);
   part[threadIdx.x] = s;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -119,8 +121,40 @@ __global__ void __launch_bounds__(1024) k_build_offsets(PullPlan pl, const uint3
   int64_t run = part[threadIdx.x];
   for (int64_t t = lo; t < hi; ++t) {
     off[t] = run;
-    run += total[t];
+    n[t] = total[t];
+    run += padded(total[t]);
   }
+}
+
+// Group bases of the packed lists: the first coordinate of each group of kListGroup entries
+// (every group holds at least one entry of its tile: tiles start at group boundaries).
+__global__ void __launch_bounds__(kBlock) k_build_bases(const uint32_t* __restrict__ list, int64_t groups,
+                                                        uint32_t* __restrict__ bases) {
+  const int64_t stride = (int64_t)gridDim.x * kBlock;
+  for (int64_t g = (int64_t)blockIdx.x * kBlock + threadIdx.x; g < groups; g += stride)
+    bases[g] = list[g * kListGroup];
+}
+
+// One block per tile: does every entry's offset from its group base fit in off_bits bits?
+// (flag set otherwise). With pack = 1, rewrite the entries in place as packed words.
+__global__ void __launch_bounds__(kBlock) k_build_pack(uint32_t* __restrict__ list, const uint16_t* __restrict__ codes,
+                                                       const uint32_t* __restrict__ bases,
+                                                       const int64_t* __restrict__ off,
+                                                       const uint32_t* __restrict__ n, int off_bits, int pack,
+                                                       uint32_t* __restrict__ flag) {
+  const int64_t t = blockIdx.x;
+  const int64_t lo = off[t], hi = lo + n[t];
+  const uint32_t lim = 1u << off_bits;
+  bool bad = false;
+  for (int64_t e = lo + threadIdx.x; e < hi; e += kBlock) {
+    const uint32_t o = list[e] - bases[e / kListGroup];  // entries ascend within a tile
+    if (o >= lim) bad = true;
+    if (pack) {
+      const uint32_t code = codes[e];
+      list[e] = o | ((code & 0x7fffu) << off_bits) | ((code & 0x8000u) << 16);
+    }
+  }
+  if (bad) atomicOr(flag, 1u);
 }
 
 // In-order fill: one wave per build chunk walks its coordinates in ascending order; lanes
@@ -279,12 +313,29 @@ __device__ __forceinline__ void load_row(const float* __restrict__ vI, uint32_t 
 // sums, so it rounds them itself: tables[q] (when non-null) and the tree-order merge into
 // `merged` (when non-null) are written directly, and the fp64 partials are not. Otherwise
 // (S > 1, or both outputs null) the partials go to `partial` for k_merge_partials.
-template <int P, int U>
+// List entry e: its coordinate i, position in the tile and sign mask (from a packed word and
+// its group base, or from the unpacked list and codes).
+template <bool PK>
+__device__ __forceinline__ void decode_entry(uint32_t w, uint32_t aux, int off_bits, uint32_t& i, uint32_t& pos,
+                                             uint32_t& sflip) {
+  if constexpr (PK) {
+    i = aux + (w & ((1u << off_bits) - 1u));
+    pos = (w & 0x7fffffffu) >> off_bits;
+    sflip = w & 0x80000000u;
+  } else {
+    i = w;
+    pos = aux & 0x7fffu;
+    sflip = (aux & 0x8000u) << 16;
+  }
+}
+
+template <int P, int U, bool PK>
 __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
                                                      const uint16_t* __restrict__ codes,
-                                                     const int64_t* __restrict__ off, const float* __restrict__ vI,
-                                                     double* __restrict__ partial, float* __restrict__ merged,
-                                                     float* __restrict__ tables) {
+                                                     const uint32_t* __restrict__ bases,
+                                                     const int64_t* __restrict__ off, const uint32_t* __restrict__ tn,
+                                                     const float* __restrict__ vI, double* __restrict__ partial,
+                                                     float* __restrict__ merged, float* __restrict__ tables) {
   extern __shared__ double acc[];  // [P][W]: worker-major, so lanes adding for one worker hit spread banks
   constexpr int PP = (P + 3) & ~3;
   constexpr int L = PP / 4;
@@ -305,26 +356,28 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - kt * pl.W);
   for (int64_t e = threadIdx.x; e < wt * P; e += kPullBlock) acc[e] = 0.0;
   __syncthreads();
-  const int64_t lo = off[t], n = off[t + 1] - lo;
+  const int64_t lo = off[t], n = tn[t];
   const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
   double* const mycol = acc + (int64_t)(4 * sub) * wt;
   // when L does not divide the block (L = 3: 85 groups of 3 lanes), the last lane has no
   // group: it takes no entry (its would be the next pass's first)
   int64_t eb = tid0 < B ? e0 + tid : e1;
   for (; eb + (U - 1) * B < e1; eb += U * B) {
-    uint32_t i[U], code[U];
+    uint32_t i[U], pos[U], sg[U];
 #pragma unroll
     for (int m = 0; m < U; ++m) {
-      i[m] = list[eb + m * B];
-      code[m] = codes[eb + m * B];
+      const int64_t e = eb + m * B;
+      const uint32_t w = list[e];
+      const uint32_t aux = PK ? bases[e / kListGroup] : (uint32_t)codes[e];
+      decode_entry<PK>(w, aux, pl.off_bits, i[m], pos[m], sg[m]);
     }
     f4 x[U];
 #pragma unroll
     for (int m = 0; m < U; ++m) x[m] = reinterpret_cast<const f4*>(vI + (int64_t)i[m] * PP)[sub];
 #pragma unroll
     for (int m = 0; m < U; ++m) {
-      double* cell = mycol + (code[m] & 0x7fffu);
-      const uint32_t sflip = (code[m] & 0x8000u) << 16;
+      double* cell = mycol + pos[m];
+      const uint32_t sflip = sg[m];
       const float xs[4] = {x[m].x, x[m].y, x[m].z, x[m].w};
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -332,10 +385,10 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
     }
   }
   for (; eb < e1; eb += B) {
-    const uint32_t i = list[eb], code = codes[eb];
+    uint32_t i, pos, sflip;
+    decode_entry<PK>(list[eb], PK ? bases[eb / kListGroup] : (uint32_t)codes[eb], pl.off_bits, i, pos, sflip);
     const f4 x = reinterpret_cast<const f4*>(vI + (int64_t)i * PP)[sub];
-    double* cell = mycol + (code & 0x7fffu);
-    const uint32_t sflip = (code & 0x8000u) << 16;
+    double* cell = mycol + pos;
     const float xs[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int q = 0; q < 4; ++q)
@@ -374,8 +427,8 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
 // Runtime-P variant (P > 16): rows of PP floats read element by element.
 __global__ void __launch_bounds__(kBlock) k_pull_any(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
                                                      const uint16_t* __restrict__ codes,
-                                                     const int64_t* __restrict__ off, const float* __restrict__ vI,
-                                                     double* __restrict__ partial) {
+                                                     const int64_t* __restrict__ off, const uint32_t* __restrict__ tn,
+                                                     const float* __restrict__ vI, double* __restrict__ partial) {
   extern __shared__ double acc[];
   const int P = pl.P, PP = pl.PP;
   const int64_t item = grouped_item(blockIdx.x, gridDim.x, pl.slots);
@@ -385,7 +438,7 @@ __global__ void __launch_bounds__(kBlock) k_pull_any(HashSet hs, PullPlan pl, co
   const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - kt * pl.W);
   for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) acc[e] = 0.0;
   __syncthreads();
-  const int64_t lo = off[t], n = off[t + 1] - lo;
+  const int64_t lo = off[t], n = tn[t];
   const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
   for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
     const uint32_t i = list[e], code = codes[e];
@@ -473,14 +526,22 @@ hipError_t launch_acc_vi_p(const gs_ctx* x, hipStream_t s, const float* g, float
 template <int P>
 void launch_pull_p(const gs_ctx* x, hipStream_t s, const float* rows, float* merged, float* tables) {
   const PullPlan& pl = x->plan;
-  hipLaunchKernelGGL((k_pull<P, pull_unroll(P)>), dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kPullBlock),
-                     (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->codes, x->tile_off, rows,
-                     x->partial, merged, tables);
+  const dim3 grid((unsigned)((int64_t)pl.T * pl.S)), block(kPullBlock);
+  const size_t lds = (size_t)pl.W * pl.P * sizeof(double);
+  if (pl.packed)
+    hipLaunchKernelGGL((k_pull<P, pull_unroll(P), true>), grid, block, lds, s, x->hs, pl, x->list, x->codes, x->bases,
+                       x->tile_off, x->tile_n, rows, x->partial, merged, tables);
+  else
+    hipLaunchKernelGGL((k_pull<P, pull_unroll(P), false>), grid, block, lds, s, x->hs, pl, x->list, x->codes,
+                       x->bases, x->tile_off, x->tile_n, rows, x->partial, merged, tables);
 }
 
 template <int P>
 hipError_t allow_pull_lds(size_t bytes) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull<P, pull_unroll(P)>),
+  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull<P, pull_unroll(P), true>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull<P, pull_unroll(P), false>),
                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
@@ -574,6 +635,12 @@ PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int6
     }
   }
   pl.W = (int32_t)W;
+  {
+    int pos_bits = 1;  // bits of a position in the tile (< W)
+    while ((1ll << pos_bits) < W) ++pos_bits;
+    pl.off_bits = 31 - pos_bits;
+    pl.packed = 0;  // set by build_pull_lists when every group fits
+  }
   pl.tiles_per_row = (int32_t)((c + W - 1) / W);
   pl.T = r * pl.tiles_per_row;
   // small sketches: split each tile's list into segments so every CU gets work
@@ -604,7 +671,7 @@ hipError_t prepare_pull_kernels(const gs_ctx* x) {
 }
 
 hipError_t build_pull_lists(gs_ctx* x) {
-  const PullPlan& pl = x->plan;
+  PullPlan& pl = x->plan;
   const size_t fill_lds = (size_t)pl.T * sizeof(uint32_t);
   hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_build_fill),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)fill_lds);
@@ -613,20 +680,44 @@ hipError_t build_pull_lists(gs_ctx* x) {
   if (ea != hipSuccess) return ea;
   uint32_t* counts = nullptr;
   uint32_t* total = nullptr;
+  uint32_t* flag = nullptr;
   hipError_t e = hipMalloc(reinterpret_cast<void**>(&counts), (size_t)pl.NB * pl.T * sizeof(uint32_t));
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&total), (size_t)pl.T * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&flag), sizeof(uint32_t));
   if (e == hipSuccess) e = hipMemset(counts, 0, (size_t)pl.NB * pl.T * sizeof(uint32_t));
+  if (e == hipSuccess) e = hipMemset(flag, 0, sizeof(uint32_t));
   if (e == hipSuccess) {
     hipLaunchKernelGGL(k_build_count, dim3(pl.NB), dim3(kBlock), 0, 0, x->hs, pl, x->d, counts);
     hipLaunchKernelGGL(k_build_prefix, dim3((pl.T + kBlock - 1) / kBlock), dim3(kBlock), 0, 0, pl, counts, total);
-    hipLaunchKernelGGL(k_build_offsets, dim3(1), dim3(1024), 0, 0, pl, total, x->tile_off);
+    hipLaunchKernelGGL(k_build_offsets, dim3(1), dim3(1024), 0, 0, pl, total, x->tile_off, x->tile_n);
     hipLaunchKernelGGL(k_build_fill, dim3(pl.NB), dim3(64), (size_t)pl.T * sizeof(uint32_t), 0, x->hs, pl, x->d,
                        counts, x->tile_off, x->list, x->codes);
+    const int64_t groups = x->list_cap / kListGroup;
+    hipLaunchKernelGGL(k_build_bases, dim3(grid_for(groups, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, 0, x->list,
+                       groups, x->bases);
+    hipLaunchKernelGGL(k_build_pack, dim3(pl.T), dim3(kBlock), 0, 0, x->list, x->codes, x->bases, x->tile_off,
+                       x->tile_n, pl.off_bits, 0, flag);
     e = hipGetLastError();
+  }
+  uint32_t overflow = 1;
+  if (e == hipSuccess) e = hipMemcpy(&overflow, flag, sizeof(uint32_t), hipMemcpyDeviceToHost);
+  // pack when every group's span fits (and the unrolled pulls run: P <= 16); off_bits = 0
+  // keeps the lists unpacked
+  if (e == hipSuccess && overflow == 0 && x->P <= 16 && pl.off_bits > 0) {
+    hipLaunchKernelGGL(k_build_pack, dim3(pl.T), dim3(kBlock), 0, 0, x->list, x->codes, x->bases, x->tile_off,
+                       x->tile_n, pl.off_bits, 1, flag);
+    e = hipGetLastError();
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e == hipSuccess) {
+      pl.packed = 1;
+      (void)hipFree(x->codes);
+      x->codes = nullptr;
+    }
   }
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (counts) (void)hipFree(counts);
   if (total) (void)hipFree(total);
+  if (flag) (void)hipFree(flag);
   return e;
 }
 
@@ -680,8 +771,8 @@ hipError_t launch_pull(const gs_ctx* x, hipStream_t s, const float* rows, float*
     default: {
       const PullPlan& pl = x->plan;
       hipLaunchKernelGGL(k_pull_any, dim3((unsigned)((int64_t)pl.T * pl.S)), dim3(kBlock),
-                         (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->codes, x->tile_off, rows,
-                         x->partial);
+                         (size_t)pl.W * pl.P * sizeof(double), s, x->hs, pl, x->list, x->codes, x->tile_off,
+                         x->tile_n, rows, x->partial);
     }
   }
   return hipGetLastError();

@@ -375,6 +375,22 @@ def test_atomic_sketch_path(monkeypatch, d, P, r, c, k):
     dv.close()
 
 
+@pytest.mark.parametrize("d,P,r,c,k", [(65_536, 8, 5, 4096, 655), (10_007, 3, 5, 211, 300), (5_003, 12, 5, 300, 50),
+                                       (100_003, 1, 5, 2_000_003, 50)])
+def test_unpacked_lists(monkeypatch, d, P, r, c, k):
+    # the gather with its lists unpacked (coordinates and 16-bit codes): the form used when a
+    # group's coordinates span more than the packed word's offset field
+    monkeypatch.setenv("GS_SKETCH_PATH", "unpacked")
+    hp = synth.hash_params(synth.BASE_SEED + 41 * d + P, r)
+    rng = np.random.default_rng(d + 5 * P)
+    dv = Dev(d, P, r, c, k, hp, 0.9)
+    u = rng.standard_normal((P, d)).astype(np.float32)
+    v = rng.standard_normal((P, d)).astype(np.float32)
+    g = rng.laplace(0, 1e-2, (P, d)).astype(np.float32)
+    chain_check(dv, g, u, v, k, 0.9, label=f"unpacked d={d} P={P} r={r} c={c} k={k}")
+    dv.close()
+
+
 def test_single_huge_coordinate():
     d, P, r, c, k = 200_000, 4, 5, 2000, 10
     hp = synth.hash_params(synth.BASE_SEED + 6, r)
