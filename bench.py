@@ -75,7 +75,7 @@ def stage_kernels(w, layout: str = "interleaved") -> dict:
     acc = [f"k_accumulate_il<{w.P // 4}>"] if layout == "interleaved" else [f"k_accumulate_vi<{w.P}>"]
     return {
         "accumulate": acc,
-        "sketch": [f"k_pull<{w.P}, {4 if w.P <= 4 else 6}>"],
+        "sketch": [f"k_pull<{w.P}, {4 if w.P <= 4 else 6}, true>"],  # packed lists (the library's choice here)
         "merge": [f"k_merge_partials<{w.P}>"],
         "select": [f"k_sample<{w.r}, false>", "k_tau0", "k_heavy", f"k_pruned<{w.r}, false, false>",
                    f"k_survivors<{w.r}, false>", "k_cand_hist", "k_select1p", f"k_unsketch<{w.r}>", "k_select1",
