@@ -45,14 +45,17 @@ hipError_t alloc(T** p, int64_t count) {
 }
 
 void free_scratch(gs_ctx* x) {
-  void* ptrs[] = {x->keys, x->hist,   x->hist2, x->ctl,     x->cand_key,    x->cand_idx, x->bitmap,
-                  x->blockcnt, x->acc64, x->list, x->codes, x->bases, x->tile_off, x->tile_n, x->vI, x->partial,
-                  x->sample_keys, x->heavy, x->l2buf, x->coarse};
+  void* ptrs[] = {x->keys,     x->hist,     x->hist2,  x->hist_s,   x->hist_c, x->ctl,      x->cand_key,
+                  x->cand_idx, x->bitmap,   x->blockcnt, x->acc64, x->list,   x->codes,    x->bases,
+                  x->tile_off, x->tile_n,   x->vI,     x->partial,  x->sample_keys, x->heavy, x->l2buf,
+                  x->coarse};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   x->keys = nullptr;
   x->hist = nullptr;
   x->hist2 = nullptr;
+  x->hist_s = nullptr;
+  x->hist_c = nullptr;
   x->ctl = nullptr;
   x->cand_key = nullptr;
   x->cand_idx = nullptr;
@@ -172,6 +175,8 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   chk(alloc(&x->keys, x->d));
   chk(alloc(&x->hist, gs::kDigit1Bins));
   chk(alloc(&x->hist2, gs::kDigitBins));
+  chk(alloc(&x->hist_s, gs::kDigit1Bins));
+  chk(alloc(&x->hist_c, gs::kDigit1Bins));
   chk(alloc(&x->ctl, 1));
   chk(alloc(&x->cand_key, x->cand_cap));
   chk(alloc(&x->cand_idx, x->cand_cap));
@@ -207,6 +212,8 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   }
   if (ea == hipSuccess) ea = hipMemset(x->hist, 0, gs::kDigit1Bins * sizeof(uint32_t));
   if (ea == hipSuccess) ea = hipMemset(x->hist2, 0, gs::kDigitBins * sizeof(uint32_t));
+  if (ea == hipSuccess) ea = hipMemset(x->hist_s, 0, gs::kDigit1Bins * sizeof(uint32_t));
+  if (ea == hipSuccess) ea = hipMemset(x->hist_c, 0, gs::kDigit1Bins * sizeof(uint32_t));
   if (ea == hipSuccess) ea = hipMemset(x->ctl, 0, sizeof(gs::SelectCtl));
   if (ea == hipSuccess) ea = hipDeviceSynchronize();
   if (ea == hipSuccess && x->use_pull) ea = gs::build_pull_lists(x);

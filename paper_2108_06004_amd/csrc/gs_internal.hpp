@@ -89,6 +89,8 @@ struct gs_ctx {
   uint32_t* keys = nullptr;       // [d]
   uint32_t* hist = nullptr;       // [kDigit1Bins], zero between calls
   uint32_t* hist2 = nullptr;      // [kDigitBins] digit-2 histogram of bucket b1, zero between calls
+  uint32_t* hist_s = nullptr;     // [kDigit1Bins] digit-1 histogram of the sampled keys, zero between calls
+  uint32_t* hist_c = nullptr;     // [kDigit1Bins] digit-1 histogram of the pruned candidates, zero between calls
   gs::SelectCtl* ctl = nullptr;   // [1]
   uint32_t* cand_key = nullptr;   // [cand_cap]
   int32_t* cand_idx = nullptr;    // [cand_cap]

@@ -7,13 +7,14 @@
 // integers); for HEAVYMIX, heavy coordinates get 0x80000000 | bits(|est_i|) and the others
 // their fill draw. The k-th key is found by a most-significant-digit radix select entirely
 // on the device (no host synchronisation inside the call):
-//   1. candidates: every key whose digit 1 (bits 31..20) is at least that of the k-th key,
-//      either from the pruned pass (sampled bound, heavy-cell bitmap, survivor estimates;
-//      k_sample .. k_survivors, then k_cand_hist / k_select1p) or from the full estimate
-//      (k_unsketch / k_unsketch_hm, k_select1, k_compact), which also runs whenever the
-//      pruned candidates fall short of k;
+//   1. candidates: either every key reaching the pruned pass's sampled bound (k_sample ..
+//      k_survivors: bound, heavy-cell bitmap, survivor estimates, with the candidates'
+//      digit-1 histogram), or, from the full estimate, every key whose digit 1 (bits
+//      31..20) is at least that of the k-th key (k_unsketch / k_unsketch_hm, k_select1,
+//      k_compact), which also runs whenever the pruned candidates fall short of k;
 //   2. k_digit2 (many blocks): digit 2 (bits 19..10) of the keys in the k-th key's digit-1
-//      bucket, and that bucket compacted;
+//      bucket (after a pruned pass each block finds that bucket in the candidates'
+//      histogram), and that bucket compacted;
 //   3. k_select2 (one block): digit 3 (bits 9..0) gives the k-th key tau and how many keys
 //      equal to tau are taken; if not all of them, three index digits find the largest
 //      index iota taken among them (lowest indices win);
@@ -68,29 +69,31 @@ __device__ uint32_t block_scan_incl(uint32_t x, uint32_t* sh, uint32_t& total) {
   return x + add;
 }
 
-// Scan the LDS histogram h[nbins] (nbins = 1024, 2048 or 4096) in descending or ascending bin
-// order and find the first bin at which the running count reaches `need` (1 <= need <=
-// total). res[0] = that bin, res[1] = count in the bins before it (in scan order).
-__device__ void find_bucket(const uint32_t* h, int nbins, bool descending, uint32_t need, uint32_t* shw,
-                            uint32_t* res) {
-  const int per = nbins / kSelBlock;
-  uint32_t cnt[4] = {0u, 0u, 0u, 0u};
-  int bin[4] = {0, 0, 0, 0};
+// Scan the histogram h[NB] (LDS or global; NB a multiple of BS, at most 16 bins per
+// thread) in descending or ascending bin order and find the first bin at which the running
+// count reaches `need` (1 <= need <= total). res[0] = that bin, res[1] = count in the bins
+// before it (in scan order). Each thread reads its bins once. All threads must call it.
+template <int BS, int NB>
+__device__ void find_bucket(const uint32_t* h, bool descending, uint32_t need, uint32_t* shw, uint32_t* res) {
+  constexpr int kPer = NB / BS;
+  static_assert(kPer >= 1 && kPer * BS == NB && kPer <= 16, "bins per thread");
+  uint32_t cnt[kPer];
   uint32_t sum = 0;
-  for (int m = 0; m < per; ++m) {
-    const int pos = threadIdx.x * per + m;
-    bin[m] = descending ? nbins - 1 - pos : pos;
-    cnt[m] = h[bin[m]];
+#pragma unroll
+  for (int m = 0; m < kPer; ++m) {
+    const int pos = threadIdx.x * kPer + m;
+    cnt[m] = h[descending ? NB - 1 - pos : pos];
     sum += cnt[m];
   }
   uint32_t total;
-  const uint32_t incl = block_scan_incl<kSelBlock>(sum, shw, total);
+  const uint32_t incl = block_scan_incl<BS>(sum, shw, total);
   const uint32_t excl = incl - sum;
   if (excl < need && need <= incl) {
     uint32_t run = excl;
-    for (int m = 0; m < per; ++m) {
+    for (int m = 0; m < kPer; ++m) {
       if (run + cnt[m] >= need) {
-        res[0] = (uint32_t)bin[m];
+        const int pos = threadIdx.x * kPer + m;
+        res[0] = (uint32_t)(descending ? NB - 1 - pos : pos);
         res[1] = run;
         break;
       }
@@ -100,14 +103,36 @@ __device__ void find_bucket(const uint32_t* h, int nbins, bool descending, uint3
   __syncthreads();
 }
 
+// Adds 1 to the LDS histogram bin `bin` of every lane with `take` set; every lane of the
+// wave must call it. The lanes whose bin equals that of the first taking lane add with one
+// atomic, so runs of equal keys (all-zero estimates, say) do not serialise on one address.
+__device__ __forceinline__ void hist_add(uint32_t* h, bool take, uint32_t bin) {
+  const uint64_t act = __ballot(take);
+  if (act == 0ull) return;
+  const int first = __builtin_ctzll(act);
+  const uint32_t b0 = __shfl(bin, first, 64);
+  const uint64_t same = __ballot(take && bin == b0);
+  if (take && bin != b0) atomicAdd(&h[bin], 1u);
+  if ((int)(threadIdx.x & 63) == first) atomicAdd(&h[b0], (uint32_t)__popcll(same));
+}
+
 // ------------------------------------------------------------------------------------
 // Step 1, full path: estimate (HEAVYMIX query) + keys + digit-1 histogram.
+
+// After a pruned pass: true when fewer than k coordinates reached its bound, so the full
+// estimate has to run. The first kernel of the full path calls it (every block sees the
+// same counts) and raises ctl->fallback, which gates the kernels after it.
+__device__ __forceinline__ bool fallback_needed(SelectCtl* ctl) {
+  const bool fb = ctl->n_cand < ctl->k;
+  if (fb && blockIdx.x == 0 && threadIdx.x == 0) ctl->fallback = 1u;
+  return fb;
+}
 
 template <int R>
 __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __restrict__ merged, int64_t d,
                                                      float* __restrict__ est, uint32_t* __restrict__ keys,
-                                                     uint32_t* __restrict__ hist, const SelectCtl* __restrict__ gate) {
-  if (gate && gate->fallback == 0u) return;  // the pruned selection sufficed
+                                                     uint32_t* __restrict__ hist, SelectCtl* __restrict__ gate) {
+  if (gate && !fallback_needed(gate)) return;  // the pruned selection sufficed
   __shared__ uint32_t h[kDigit1Bins];
   for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
   RowConst kr[R];
@@ -162,7 +187,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select1(uint32_t* __restrict__ hi
     hist[b] = 0u;
   }
   __syncthreads();
-  find_bucket(h, kDigit1Bins, true, k, shw, res);
+  find_bucket<kSelBlock, kDigit1Bins>(h, true, k, shw, res);
   if (threadIdx.x == 0) {
     ctl->k = k;
     ctl->b1 = res[0];
@@ -262,15 +287,30 @@ constexpr int kStageBuf = 4096;  // per-block LDS buffer of k_digit2
 
 // Step 2: digit 2 of the keys in bucket b1 (many blocks): the digit-2 histogram (LDS per
 // block, added into hist2) and the bucket's keys compacted into stage2 for the digit-3
-// pass (an LDS buffer per block, one global atomic per flush).
+// pass (an LDS buffer per block, one global atomic per flush). After a pruned pass that
+// sufficed (pruned = 1, no fallback) every block finds b1 itself from the candidates'
+// digit-1 histogram hist_c, and block 0 records it; otherwise k_select1 has set it.
 __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ cand_key,
                                                    SelectCtl* __restrict__ ctl, int64_t cap,
-                                                   uint32_t* __restrict__ hist2, uint32_t* __restrict__ stage2) {
+                                                   uint32_t* __restrict__ hist2, uint32_t* __restrict__ stage2,
+                                                   const uint32_t* __restrict__ hist_c, int pruned) {
   __shared__ uint32_t h[kDigitBins];
   __shared__ uint32_t buf[kStageBuf];
+  __shared__ uint32_t shw[kBlock / 64];
+  __shared__ uint32_t res[2];
   __shared__ uint32_t bn, gbase;
   const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
-  const uint32_t b1 = ctl->b1;
+  uint32_t b1;
+  if (pruned && ctl->fallback == 0u) {  // block-uniform
+    find_bucket<kBlock, kDigit1Bins>(hist_c, true, ctl->k, shw, res);
+    b1 = res[0];
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      ctl->b1 = res[0];
+      ctl->above1 = res[1];
+    }
+  } else {
+    b1 = ctl->b1;
+  }
   const int lane = threadIdx.x & 63;
   for (int b = threadIdx.x; b < kDigitBins; b += kBlock) h[b] = 0u;
   if (threadIdx.x == 0) bn = 0u;
@@ -289,7 +329,7 @@ __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ 
     for (int m = 0; m < V; ++m) {
       const int64_t t = c0 + (int64_t)m * kBlock + threadIdx.x;
       const bool take = t < hi && (key[m] >> 20) == b1;
-      if (take) atomicAdd(&h[(key[m] >> 10) & 1023u], 1u);
+      hist_add(h, take, (key[m] >> 10) & 1023u);
       const uint64_t bal = __ballot(take);
       uint32_t wbase = 0u;
       if (lane == 0 && bal) wbase = atomicAdd(&bn, (uint32_t)__popcll(bal));
@@ -319,7 +359,8 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
                                                        const int32_t* __restrict__ cand_idx,
                                                        SelectCtl* __restrict__ ctl, int64_t cap,
                                                        uint32_t* __restrict__ hist2,
-                                                       const uint32_t* __restrict__ stage2) {
+                                                       const uint32_t* __restrict__ stage2,
+                                                       uint32_t* __restrict__ hist_c, int pruned) {
   __shared__ uint32_t h[2048];
   __shared__ uint32_t shw[kSelBlock / 64];
   __shared__ uint32_t res[2];
@@ -335,8 +376,10 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
     h[b] = hist2[b];
     hist2[b] = 0u;
   }
+  if (pruned)  // the candidates' digit-1 histogram, read by k_digit2, cleared for the next call
+    for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) hist_c[b] = 0u;
   __syncthreads();
-  find_bucket(h, kDigitBins, true, need1, shw, res);
+  find_bucket<kSelBlock, kDigitBins>(h, true, need1, shw, res);
   const uint32_t pre2 = (b1 << 10) | res[0];
   const uint32_t need2 = need1 - res[1];
   __syncthreads();
@@ -354,11 +397,11 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
 #pragma unroll
     for (int m = 0; m < kSelUnroll; ++m) {
       const int64_t t = t0 + (int64_t)m * kSelBlock + threadIdx.x;
-      if (t < n2 && (key[m] >> 10) == pre2) atomicAdd(&h[key[m] & 1023u], 1u);
+      hist_add(h, t < n2 && (key[m] >> 10) == pre2, key[m] & 1023u);
     }
   }
   __syncthreads();
-  find_bucket(h, kDigitBins, true, need2, shw, res);
+  find_bucket<kSelBlock, kDigitBins>(h, true, need2, shw, res);
   const uint32_t tau = (pre2 << 10) | res[0];
   const uint32_t need3 = need2 - res[1];  // how many keys equal to tau are taken
   const uint32_t n_eq = h[res[0]];
@@ -404,7 +447,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
     for (int64_t t = threadIdx.x; t < n; t += kSelBlock)
       if (cand_key[t] == tau) atomicAdd(&h[(uint32_t)cand_idx[t] >> 21], 1u);
     __syncthreads();
-    find_bucket(h, 1024, false, need3, shw, res);
+    find_bucket<kSelBlock, 1024>(h, false, need3, shw, res);
     const uint32_t c1 = res[0];
     const uint32_t needc = need3 - res[1];
     __syncthreads();
@@ -416,7 +459,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
       if (cand_key[t] == tau && (ix >> 21) == c1) atomicAdd(&h[(ix >> 10) & 2047u], 1u);
     }
     __syncthreads();
-    find_bucket(h, 2048, false, needc, shw, res);
+    find_bucket<kSelBlock, 2048>(h, false, needc, shw, res);
     const uint32_t pre_i = (c1 << 11) | res[0];
     const uint32_t needd = needc - res[1];
     __syncthreads();
@@ -428,7 +471,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
       if (cand_key[t] == tau && (ix >> 10) == pre_i) atomicAdd(&h[ix & 1023u], 1u);
     }
     __syncthreads();
-    find_bucket(h, 1024, false, needd, shw, res);
+    find_bucket<kSelBlock, 1024>(h, false, needd, shw, res);
     iota = (pre_i << 10) | res[0];
   }
   if (threadIdx.x == 0) {
@@ -474,52 +517,74 @@ __device__ __forceinline__ uint32_t estimate_key(const RowConst (&kr)[R], const 
 }
 
 // Sampled keys at M evenly spaced coordinates: |est| keys, or (HEAVYMIX) the fill keys
-// rnd >> 1, whose rho-th largest bounds the fill from below.
+// rnd >> 1, whose rho-th largest bounds the fill from below. Their digit-1 histogram is
+// added into hist_s for k_tau0.
 template <int R, bool HM>
 __global__ void __launch_bounds__(kBlock) k_sample(HashSet hs, const float* __restrict__ merged, int64_t d, int M,
-                                                   const uint32_t* __restrict__ rnd, uint32_t* __restrict__ out) {
+                                                   const uint32_t* __restrict__ rnd, uint32_t* __restrict__ out,
+                                                   uint32_t* __restrict__ hist_s) {
+  __shared__ uint32_t h[kDigit1Bins];
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
+  __syncthreads();
   const int s = blockIdx.x * kBlock + threadIdx.x;
-  if (s >= M) return;
-  const uint32_t i = (uint32_t)(((int64_t)s * d) / M);
-  if constexpr (HM) {
-    out[s] = rnd[i] >> 1;
-  } else {
-    RowConst kr[R];
+  const bool ok = s < M;
+  uint32_t key = 0u;
+  if (ok) {
+    const uint32_t i = (uint32_t)(((int64_t)s * d) / M);
+    if constexpr (HM) {
+      key = rnd[i] >> 1;
+    } else {
+      RowConst kr[R];
 #pragma unroll
-    for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
-    out[s] = estimate_key<R>(kr, merged, i);
+      for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
+      key = estimate_key<R>(kr, merged, i);
+    }
+    out[s] = key;
+  }
+  hist_add(h, ok, key >> kDigit1Shift);
+  __syncthreads();
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) {
+    const uint32_t c = h[b];
+    if (c) atomicAdd(&hist_s[b], c);
   }
 }
 
-// tau0 = the rho-th largest sampled key (three radix digits in one block).
+// tau0 = the rho-th largest sampled key (one block): digit 1 from k_sample's histogram
+// (cleared here for the next call), digits 2 and 3 over the sampled keys held in registers.
 __global__ void __launch_bounds__(kSelBlock) k_tau0(const uint32_t* __restrict__ sample, int M, uint32_t rho,
-                                                    SelectCtl* __restrict__ ctl, uint32_t k) {
-  __shared__ uint32_t key[kSampleMax];
-  __shared__ uint32_t h[kDigit1Bins];
+                                                    SelectCtl* __restrict__ ctl, uint32_t k,
+                                                    uint32_t* __restrict__ hist_s) {
+  constexpr int kPer = kSampleMax / kSelBlock;
+  __shared__ uint32_t h[kDigitBins];
   __shared__ uint32_t shw[kSelBlock / 64];
   __shared__ uint32_t res[2];
-  for (int t = threadIdx.x; t < M; t += kSelBlock) key[t] = sample[t];
-  for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) h[b] = 0u;
-  __syncthreads();
-  for (int t = threadIdx.x; t < M; t += kSelBlock) atomicAdd(&h[key[t] >> 20], 1u);
-  __syncthreads();
-  find_bucket(h, kDigit1Bins, true, rho, shw, res);
+  uint32_t key[kPer];
+#pragma unroll
+  for (int m = 0; m < kPer; ++m) {
+    const int t = m * kSelBlock + threadIdx.x;
+    key[m] = t < M ? sample[t] : 0u;
+  }
+  for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
+  find_bucket<kSelBlock, kDigit1Bins>(hist_s, true, rho, shw, res);
   const uint32_t b1 = res[0], need2 = rho - res[1];
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) hist_s[b] = 0u;
+#pragma unroll
+  for (int m = 0; m < kPer; ++m) {
+    const bool take = m * kSelBlock + (int)threadIdx.x < M && (key[m] >> kDigit1Shift) == b1;
+    hist_add(h, take, (key[m] >> 10) & 1023u);
+  }
   __syncthreads();
-  for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
-  __syncthreads();
-  for (int t = threadIdx.x; t < M; t += kSelBlock)
-    if ((key[t] >> 20) == b1) atomicAdd(&h[(key[t] >> 10) & 1023u], 1u);
-  __syncthreads();
-  find_bucket(h, kDigitBins, true, need2, shw, res);
+  find_bucket<kSelBlock, kDigitBins>(h, true, need2, shw, res);
   const uint32_t pre = (b1 << 10) | res[0], need3 = need2 - res[1];
-  __syncthreads();
   for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
   __syncthreads();
-  for (int t = threadIdx.x; t < M; t += kSelBlock)
-    if ((key[t] >> 10) == pre) atomicAdd(&h[key[t] & 1023u], 1u);
+#pragma unroll
+  for (int m = 0; m < kPer; ++m) {
+    const bool take = m * kSelBlock + (int)threadIdx.x < M && (key[m] >> 10) == pre;
+    hist_add(h, take, key[m] & 1023u);
+  }
   __syncthreads();
-  find_bucket(h, kDigitBins, true, need3, shw, res);
+  find_bucket<kSelBlock, kDigitBins>(h, true, need3, shw, res);
   if (threadIdx.x == 0) {
     ctl->tau0 = (pre << 10) | res[0];
     ctl->k = k;
@@ -687,10 +752,13 @@ template <int R, bool HM>
 __global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* __restrict__ merged,
                                                       SelectCtl* __restrict__ ctl, const uint32_t* __restrict__ queue,
                                                       uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx,
-                                                      int64_t cap, const uint32_t* __restrict__ rnd) {
+                                                      int64_t cap, const uint32_t* __restrict__ rnd,
+                                                      uint32_t* __restrict__ hist_c) {
   __shared__ uint32_t bkey[kSurvBuf];
   __shared__ int32_t bidx[kSurvBuf];
+  __shared__ uint32_t h[kDigit1Bins];
   __shared__ uint32_t bn, gbase, nheavy;
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
   RowConst kr[R];
 #pragma unroll
   for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
@@ -722,6 +790,7 @@ __global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* _
         cand = key >= tau0;
       }
     }
+    hist_add(h, cand, key >> kDigit1Shift);
     // block-local append (one LDS atomic per wave); at most kBlock per pass, so the buffer,
     // flushed whenever it is half full, never overflows
     const uint64_t bal = __ballot(cand);
@@ -752,49 +821,14 @@ __global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* _
   }
   if constexpr (HM) {
     if (mine) atomicAdd(&nheavy, mine);
-    __syncthreads();
+  }
+  __syncthreads();
+  if constexpr (HM) {
     if (threadIdx.x == 0 && nheavy) atomicAdd(&ctl->n_heavy, (unsigned long long)nheavy);
   }
-}
-
-// Digit-1 histogram of the candidates (skipped when the fallback will run).
-__global__ void __launch_bounds__(kBlock) k_cand_hist(const uint32_t* __restrict__ cand_key,
-                                                      const SelectCtl* __restrict__ ctl, int64_t cap,
-                                                      uint32_t* __restrict__ hist) {
-  if (ctl->n_cand < ctl->k) return;
-  __shared__ uint32_t h[kDigit1Bins];
-  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
-  __syncthreads();
-  const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
-  const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n; t += stride)
-    atomicAdd(&h[cand_key[t] >> kDigit1Shift], 1u);
-  __syncthreads();
   for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) {
     const uint32_t c = h[b];
-    if (c) atomicAdd(&hist[b], c);
-  }
-}
-
-// Digit-1 bucket over the candidates, or raise the fallback flag.
-__global__ void __launch_bounds__(kSelBlock) k_select1p(uint32_t* __restrict__ hist, SelectCtl* __restrict__ ctl) {
-  __shared__ uint32_t h[kDigit1Bins];
-  __shared__ uint32_t shw[kSelBlock / 64];
-  __shared__ uint32_t res[2];
-  const uint32_t k = ctl->k;
-  if (ctl->n_cand < k) {
-    if (threadIdx.x == 0) ctl->fallback = 1u;
-    return;
-  }
-  for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) {
-    h[b] = hist[b];
-    hist[b] = 0u;
-  }
-  __syncthreads();
-  find_bucket(h, kDigit1Bins, true, k, shw, res);
-  if (threadIdx.x == 0) {
-    ctl->b1 = res[0];
-    ctl->above1 = res[1];
+    if (c) atomicAdd(&hist_c[b], c);
   }
 }
 
@@ -921,7 +955,7 @@ __global__ void __launch_bounds__(kBlock) k_unsketch_hm(HashSet hs, const float*
                                                         const uint32_t* __restrict__ rnd, float* __restrict__ est,
                                                         uint32_t* __restrict__ keys, uint32_t* __restrict__ hist,
                                                         SelectCtl* __restrict__ ctl, int gated, int count_heavy) {
-  if (gated && ctl->fallback == 0u) return;
+  if (gated && !fallback_needed(ctl)) return;
   __shared__ uint32_t h[kDigit1Bins];
   __shared__ uint32_t nh;
   for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
@@ -977,7 +1011,7 @@ __global__ void k_hm_out(const SelectCtl* __restrict__ ctl, int64_t* __restrict_
 }
 
 template <int R>
-void launch_unsketch_r(gs_ctx* x, hipStream_t s, const float* merged, float* est, const SelectCtl* gate) {
+void launch_unsketch_r(gs_ctx* x, hipStream_t s, const float* merged, float* est, SelectCtl* gate) {
   hipLaunchKernelGGL(k_unsketch<R>, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->hs, merged,
                      x->d, est, x->keys, x->hist, gate);
 }
@@ -991,8 +1025,9 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
   if (rho_d > M) rho_d = M;
   if (rho_d < 1) rho_d = 1;
   hipLaunchKernelGGL((k_sample<R, HM>), dim3((M + kBlock - 1) / kBlock), dim3(kBlock), 0, s, x->hs, merged, x->d, M,
-                     rnd, x->sample_keys);
-  hipLaunchKernelGGL(k_tau0, dim3(1), dim3(kSelBlock), 0, s, x->sample_keys, M, (uint32_t)rho_d, x->ctl, (uint32_t)k);
+                     rnd, x->sample_keys, x->hist_s);
+  hipLaunchKernelGGL(k_tau0, dim3(1), dim3(kSelBlock), 0, s, x->sample_keys, M, (uint32_t)rho_d, x->ctl, (uint32_t)k,
+                     x->hist_s);
   const int64_t rc = (int64_t)x->r * x->c;
   hipLaunchKernelGGL(k_heavy, dim3(grid_for(rc, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, merged, rc, x->ctl,
                      x->heavy, HM ? 1 : 0);
@@ -1010,10 +1045,7 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
                        x->ctl, x->heavy, x->heavy, x->prune_map_words, x->prune_map_in_lds, 0, x->prune_buf_cap,
                        x->keys, x->bitmap, rnd);
   hipLaunchKernelGGL((k_survivors<R, HM>), dim3(x->num_cus), dim3(kBlock), 0, s, x->hs, merged, x->ctl, x->keys,
-                     x->cand_key, x->cand_idx, x->cand_cap, rnd);
-  hipLaunchKernelGGL(k_cand_hist, dim3(grid_for(4 * k, kBlock, x->num_cus)), dim3(kBlock), 0, s, x->cand_key, x->ctl,
-                     x->cand_cap, x->hist);
-  hipLaunchKernelGGL(k_select1p, dim3(1), dim3(kSelBlock), 0, s, x->hist, x->ctl);
+                     x->cand_key, x->cand_idx, x->cand_cap, rnd, x->hist_c);
 }
 
 template <int R>
@@ -1043,9 +1075,9 @@ hipError_t launch_select_tail(gs_ctx* x, hipStream_t s, int64_t k, int gated, in
                        x->cand_idx, x->cand_cap, x->bitmap, per_block, gated);
   }
   hipLaunchKernelGGL(k_digit2, dim3(x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->ctl, x->cand_cap, x->hist2,
-                     x->keys);
+                     x->keys, x->hist_c, gated);
   hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap,
-                     x->hist2, x->keys);
+                     x->hist2, x->keys, x->hist_c, gated);
   hipLaunchKernelGGL(k_finalize, dim3(4 * x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl,
                      x->cand_cap, x->bitmap);
   const int64_t words = (x->d + 31) / 32;
@@ -1111,7 +1143,7 @@ hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, i
   // Otherwise the pruned path runs and the unpruned kernels only act if it raised the
   // fallback flag.
   const bool prune = (est == nullptr);
-  const SelectCtl* gate = prune ? x->ctl : nullptr;
+  SelectCtl* gate = prune ? x->ctl : nullptr;
   switch (x->r) {
 #define GS_R_CASE(RR) \
   case RR:                                            \
