@@ -45,10 +45,10 @@ hipError_t alloc(T** p, int64_t count) {
 }
 
 void free_scratch(gs_ctx* x) {
-  void* ptrs[] = {x->keys,     x->hist,     x->hist2,  x->hist_s,   x->hist_c, x->ctl,      x->cand_key,
-                  x->cand_idx, x->bitmap,   x->blockcnt, x->acc64, x->list,   x->codes,    x->bases,
-                  x->tile_off, x->tile_n,   x->vI,     x->partial,  x->sample_keys, x->heavy, x->l2buf,
-                  x->coarse};
+  void* ptrs[] = {x->keys,     x->hist,     x->hist2,       x->hist_s, x->hist_c, x->ctl,     x->stage_idx,
+                  x->cand_key, x->cand_idx, x->bitmap,      x->blockcnt, x->acc64, x->list,  x->codes,
+                  x->bases,    x->tile_off, x->tile_n,      x->vI,     x->partial, x->sample_keys,
+                  x->heavy,    x->l2buf,    x->coarse};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   x->keys = nullptr;
@@ -57,6 +57,7 @@ void free_scratch(gs_ctx* x) {
   x->hist_s = nullptr;
   x->hist_c = nullptr;
   x->ctl = nullptr;
+  x->stage_idx = nullptr;
   x->cand_key = nullptr;
   x->cand_idx = nullptr;
   x->bitmap = nullptr;
@@ -178,6 +179,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   chk(alloc(&x->hist_s, gs::kDigit1Bins));
   chk(alloc(&x->hist_c, gs::kDigit1Bins));
   chk(alloc(&x->ctl, 1));
+  chk(alloc(&x->stage_idx, x->d));
   chk(alloc(&x->cand_key, x->cand_cap));
   chk(alloc(&x->cand_idx, x->cand_cap));
   chk(alloc(&x->bitmap, words));

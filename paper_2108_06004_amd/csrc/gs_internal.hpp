@@ -20,17 +20,17 @@ struct SelectCtl {
   uint32_t k;           // number to select
   uint32_t b1;          // digit-1 bucket holding the k-th key
   uint32_t above1;      // keys in digit-1 buckets above b1
-  uint32_t n_cand;      // candidates appended by the compaction pass (digit 1 >= b1)
+  uint32_t n_cand;      // candidates appended by the pruned pass (dense candidates: d)
   uint32_t tau;         // the k-th largest key
   uint32_t iota;        // largest index taken among keys equal to tau
-  uint32_t status;      // 0 ok; nonzero: candidate overflow (must not happen)
+  uint32_t status;      // 0 ok (reserved)
   uint32_t tau0;        // pruning bound: a key no larger than the k-th key (when no fallback)
   uint32_t fallback;    // 1: fewer than k coordinates reach tau0, run the unpruned selection
   uint32_t n_surv;      // coordinates queued by the pruned pass for an exact estimate
   double l2sq;          // HEAVYMIX: l2-norm-squared estimate (median of the pairwise row sums)
   double theta;         // HEAVYMIX: heavy threshold l2sq / k
   unsigned long long n_heavy;  // HEAVYMIX: |H|
-  uint32_t n_stage2;    // keys of the digit-1 bucket b1 compacted for the digit-3 pass
+  uint32_t n_stage2;    // keys of the digit-1 bucket b1 staged for the digit-3 pass
   uint32_t pad2;
 };
 constexpr int kSampleMax = 16384;  // sampled estimates for the pruning bound
@@ -86,12 +86,13 @@ struct gs_ctx {
   int num_cus = 256;
 
   // scratch (device)
-  uint32_t* keys = nullptr;       // [d]
+  uint32_t* keys = nullptr;       // [d] survivor queue of the pruned pass, then the staged keys
   uint32_t* hist = nullptr;       // [kDigit1Bins], zero between calls
   uint32_t* hist2 = nullptr;      // [kDigitBins] digit-2 histogram of bucket b1, zero between calls
   uint32_t* hist_s = nullptr;     // [kDigit1Bins] digit-1 histogram of the sampled keys, zero between calls
   uint32_t* hist_c = nullptr;     // [kDigit1Bins] digit-1 histogram of the pruned candidates, zero between calls
   gs::SelectCtl* ctl = nullptr;   // [1]
+  int32_t* stage_idx = nullptr;   // [d] coordinates of the keys staged in `keys` for the digit-3 pass
   uint32_t* cand_key = nullptr;   // [cand_cap]
   int32_t* cand_idx = nullptr;    // [cand_cap]
   int64_t cand_cap = 0;

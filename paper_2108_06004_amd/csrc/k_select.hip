@@ -9,15 +9,14 @@
 // on the device (no host synchronisation inside the call):
 //   1. candidates: either every key reaching the pruned pass's sampled bound (k_sample ..
 //      k_survivors: bound, heavy-cell bitmap, survivor estimates, with the candidates'
-//      digit-1 histogram), or, from the full estimate, every key whose digit 1 (bits
-//      31..20) is at least that of the k-th key (k_unsketch / k_unsketch_hm, k_select1,
-//      k_compact), which also runs whenever the pruned candidates fall short of k;
-//   2. k_digit2 (many blocks): digit 2 (bits 19..10) of the keys in the k-th key's digit-1
-//      bucket (after a pruned pass each block finds that bucket in the candidates'
-//      histogram), and that bucket compacted;
-//   3. k_select2 (one block): digit 3 (bits 9..0) gives the k-th key tau and how many keys
-//      equal to tau are taken; if not all of them, three index digits find the largest
-//      index iota taken among them (lowest indices win);
+//      digit-1 histogram), or every coordinate, from the full estimate (k_unsketch /
+//      k_unsketch_hm), which also runs whenever the pruned candidates fall short of k;
+//   2. k_digit2 (many blocks): each block finds the digit-1 bucket (bits 31..20) of the
+//      k-th key in the candidates' histogram; digit 2 (bits 19..10) of that bucket's keys,
+//      and the bucket compacted (keys and coordinates);
+//   3. k_select2 (one block): digit 3 (bits 9..0) of the bucket gives the k-th key tau and
+//      how many keys equal to tau are taken; if not all of them, the largest coordinate iota
+//      taken among them (lowest coordinates win), by rank or by three index digits;
 //   4. k_finalize: candidates with key > tau, or key == tau and index <= iota, set their bit;
 //   5. emit: the bitmap is turned into ascending indices (per-block popcounts, then a
 //      block-local scan offset by the preceding blocks' totals).
@@ -117,7 +116,9 @@ __device__ __forceinline__ void hist_add(uint32_t* h, bool take, uint32_t bin) {
 }
 
 // ------------------------------------------------------------------------------------
-// Step 1, full path: estimate (HEAVYMIX query) + keys + digit-1 histogram.
+// Step 1, full path: every coordinate is a candidate ("dense" candidates: candidate t is
+// coordinate t, so no index array). The estimate, its key in cand_key[i], the digit-1
+// histogram in hist, and the output bitmap cleared.
 
 // After a pruned pass: true when fewer than k coordinates reached its bound, so the full
 // estimate has to run. The first kernel of the full path calls it (every block sees the
@@ -131,7 +132,8 @@ __device__ __forceinline__ bool fallback_needed(SelectCtl* ctl) {
 template <int R>
 __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __restrict__ merged, int64_t d,
                                                      float* __restrict__ est, uint32_t* __restrict__ keys,
-                                                     uint32_t* __restrict__ hist, SelectCtl* __restrict__ gate) {
+                                                     uint32_t* __restrict__ hist, uint32_t* __restrict__ bitmap,
+                                                     SelectCtl* __restrict__ gate) {
   if (gate && !fallback_needed(gate)) return;  // the pruned selection sufficed
   __shared__ uint32_t h[kDigit1Bins];
   for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
@@ -164,6 +166,7 @@ __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __
     const uint32_t key = abs_key(e);
     keys[i] = key;
     atomicAdd(&h[key >> kDigit1Shift], 1u);
+    if ((i & 31) == 0) bitmap[i >> 5] = 0u;
   }
   __syncthreads();
   for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) {
@@ -173,143 +176,43 @@ __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __
 }
 
 // ------------------------------------------------------------------------------------
-// Step 1, full path: digit-1 bucket of the k-th key. Clears the histogram for the next
-// call and the candidate counter for the compaction pass.
-
-__global__ void __launch_bounds__(kSelBlock) k_select1(uint32_t* __restrict__ hist, SelectCtl* __restrict__ ctl,
-                                                       uint32_t k, int gated) {
-  if (gated && ctl->fallback == 0u) return;
-  __shared__ uint32_t h[kDigit1Bins];
-  __shared__ uint32_t shw[kSelBlock / 64];
-  __shared__ uint32_t res[2];
-  for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) {
-    h[b] = hist[b];
-    hist[b] = 0u;
-  }
-  __syncthreads();
-  find_bucket<kSelBlock, kDigit1Bins>(h, true, k, shw, res);
-  if (threadIdx.x == 0) {
-    ctl->k = k;
-    ctl->b1 = res[0];
-    ctl->above1 = res[1];
-    ctl->n_cand = 0u;
-    ctl->status = 0u;
-  }
-}
-
-// ------------------------------------------------------------------------------------
-// Step 1, full path: candidate compaction (digit 1 >= b1) and bitmap clearing.
-
-// Each block scans a contiguous range of keys and collects its candidates in an LDS buffer
-// (one LDS atomic per wave), flushing it to the global list with a single global atomic
-// when it could overflow and at the end: the global counter sees a few hundred atomics
-// instead of one per wave.
-constexpr int kCompactBuf = 4096;
-
-__global__ void __launch_bounds__(kBlock) k_compact(const uint32_t* __restrict__ keys, int64_t d,
-                                                    SelectCtl* __restrict__ ctl, uint32_t* __restrict__ cand_key,
-                                                    int32_t* __restrict__ cand_idx, int64_t cap,
-                                                    uint32_t* __restrict__ bitmap, int64_t per_block, int gated) {
-  if (gated && ctl->fallback == 0u) return;
-  __shared__ uint32_t bkey[kCompactBuf];
-  __shared__ int32_t bidx[kCompactBuf];
-  __shared__ uint32_t bn;
-  __shared__ uint32_t gbase;
-  const uint32_t b1 = ctl->b1;
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const uint64_t below = (1ull << lane) - 1ull;
-  if (threadIdx.x == 0) bn = 0;
-  __syncthreads();
-  const int64_t lo = (int64_t)blockIdx.x * per_block, hi = min(d, lo + per_block);
-  for (int64_t blk = lo; blk < hi; blk += 4 * kBlock) {  // block-uniform: 1024 keys per pass
-    const int64_t base = blk + (int64_t)wid * 256;
-    const int64_t i0 = base + 4 * lane;
-    uint32_t key[4];
-    if (i0 + 3 < hi) {
-      const uint4 k4 = *reinterpret_cast<const uint4*>(keys + i0);
-      key[0] = k4.x; key[1] = k4.y; key[2] = k4.z; key[3] = k4.w;
-    } else {
-#pragma unroll
-      for (int m = 0; m < 4; ++m) key[m] = (i0 + m < hi) ? keys[i0 + m] : 0u;
-    }
-    bool take[4];
-    uint64_t mask[4];
-    uint32_t cnt[4], total = 0;
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-      take[m] = (i0 + m < hi) && (key[m] >> kDigit1Shift) >= b1;
-      mask[m] = __ballot(take[m]);
-      cnt[m] = (uint32_t)__popcll(mask[m]);
-      total += cnt[m];
-    }
-    if (total) {
-      uint32_t slot = 0;
-      if (lane == 0) slot = atomicAdd(&bn, total);
-      slot = __shfl(slot, 0, 64);
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        if (take[m]) {
-          const uint32_t pos = slot + (uint32_t)__popcll(mask[m] & below);
-          bkey[pos] = key[m];
-          bidx[pos] = (int32_t)(i0 + m);
-        }
-        slot += cnt[m];
-      }
-    }
-    if (lane < 8 && base + 32 * lane < hi) bitmap[(base >> 5) + lane] = 0u;
-    __syncthreads();
-    const uint32_t n = bn;
-    const bool last = blk + 4 * kBlock >= hi;
-    if (n > kCompactBuf - 4 * kBlock || (last && n > 0)) {  // the next pass could overflow, or done
-      if (threadIdx.x == 0) gbase = atomicAdd(&ctl->n_cand, n);
-      __syncthreads();
-      const uint32_t g0 = gbase;
-      for (uint32_t t = threadIdx.x; t < n; t += kBlock) {
-        const int64_t pos = (int64_t)g0 + t;
-        if (pos < cap) {
-          cand_key[pos] = bkey[t];
-          cand_idx[pos] = bidx[t];
-        }
-      }
-      __syncthreads();
-      if (threadIdx.x == 0) bn = 0;
-    }
-    __syncthreads();
-  }
-}
-
-// ------------------------------------------------------------------------------------
 // Steps 2 and 3: digits 2 and 3 of the k-th key, then the index cut among equal keys.
+// Candidates are either the pruned pass's (keys in cand_key, coordinates in cand_idx,
+// digit-1 histogram in hist_c) or dense (after the full estimate: every coordinate, key
+// in cand_key, histogram in hist). dense_cands() tells which.
 
 constexpr int kSelUnroll = 8;    // candidate loads in flight per thread
 constexpr int kTieMax = 1024;    // ties at the k-th key resolved by ranking in LDS (else radix digits)
-constexpr int kStageBuf = 4096;  // per-block LDS buffer of k_digit2
+constexpr int kStageBuf = 2048;  // per-block LDS buffer of k_digit2 (keys and coordinates)
 
-// Step 2: digit 2 of the keys in bucket b1 (many blocks): the digit-2 histogram (LDS per
-// block, added into hist2) and the bucket's keys compacted into stage2 for the digit-3
-// pass (an LDS buffer per block, one global atomic per flush). After a pruned pass that
-// sufficed (pruned = 1, no fallback) every block finds b1 itself from the candidates'
-// digit-1 histogram hist_c, and block 0 records it; otherwise k_select1 has set it.
+__device__ __forceinline__ bool dense_cands(const SelectCtl* ctl, int pruned) {
+  return !pruned || ctl->fallback != 0u;
+}
+
+// Step 2 (many blocks): every block finds the digit-1 bucket b1 of the k-th key in the
+// candidates' histogram (block 0 records it); then the digit-2 histogram of the bucket's
+// keys (LDS per block, added into hist2) and the bucket compacted, key and coordinate, into
+// stage_key / stage_idx (an LDS buffer per block, one global atomic per flush).
 __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ cand_key,
-                                                   SelectCtl* __restrict__ ctl, int64_t cap,
-                                                   uint32_t* __restrict__ hist2, uint32_t* __restrict__ stage2,
-                                                   const uint32_t* __restrict__ hist_c, int pruned) {
+                                                   const int32_t* __restrict__ cand_idx,
+                                                   SelectCtl* __restrict__ ctl, int64_t cap, int64_t d,
+                                                   const uint32_t* __restrict__ hist_c,
+                                                   const uint32_t* __restrict__ hist, int pruned, uint32_t k,
+                                                   uint32_t* __restrict__ hist2, uint32_t* __restrict__ stage_key,
+                                                   int32_t* __restrict__ stage_idx) {
   __shared__ uint32_t h[kDigitBins];
-  __shared__ uint32_t buf[kStageBuf];
+  __shared__ uint32_t bkey[kStageBuf];
+  __shared__ int32_t bidx[kStageBuf];
   __shared__ uint32_t shw[kBlock / 64];
   __shared__ uint32_t res[2];
   __shared__ uint32_t bn, gbase;
-  const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
-  uint32_t b1;
-  if (pruned && ctl->fallback == 0u) {  // block-uniform
-    find_bucket<kBlock, kDigit1Bins>(hist_c, true, ctl->k, shw, res);
-    b1 = res[0];
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-      ctl->b1 = res[0];
-      ctl->above1 = res[1];
-    }
-  } else {
-    b1 = ctl->b1;
+  const bool dense = dense_cands(ctl, pruned);
+  const int64_t n = dense ? d : (ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap);
+  find_bucket<kBlock, kDigit1Bins>(dense ? hist : hist_c, true, k, shw, res);
+  const uint32_t b1 = res[0];
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    ctl->b1 = res[0];
+    ctl->above1 = res[1];
   }
   const int lane = threadIdx.x & 63;
   for (int b = threadIdx.x; b < kDigitBins; b += kBlock) h[b] = 0u;
@@ -328,13 +231,17 @@ __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ 
 #pragma unroll
     for (int m = 0; m < V; ++m) {
       const int64_t t = c0 + (int64_t)m * kBlock + threadIdx.x;
-      const bool take = t < hi && (key[m] >> 20) == b1;
+      const bool take = t < hi && (key[m] >> kDigit1Shift) == b1;
       hist_add(h, take, (key[m] >> 10) & 1023u);
       const uint64_t bal = __ballot(take);
       uint32_t wbase = 0u;
       if (lane == 0 && bal) wbase = atomicAdd(&bn, (uint32_t)__popcll(bal));
       wbase = __shfl(wbase, 0);
-      if (take) buf[wbase + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull))] = key[m];
+      if (take) {
+        const uint32_t pos = wbase + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull));
+        bkey[pos] = key[m];
+        bidx[pos] = dense ? (int32_t)t : cand_idx[t];
+      }
     }
     __syncthreads();
     const uint32_t nb = bn;  // < kStageBuf / 2 + V * kBlock <= kStageBuf
@@ -342,7 +249,10 @@ __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ 
       if (threadIdx.x == 0) gbase = atomicAdd(&ctl->n_stage2, nb);
       __syncthreads();
       const uint32_t g0 = gbase;
-      for (uint32_t t = threadIdx.x; t < nb; t += kBlock) stage2[g0 + t] = buf[t];
+      for (uint32_t t = threadIdx.x; t < nb; t += kBlock) {
+        stage_key[g0 + t] = bkey[t];
+        stage_idx[g0 + t] = bidx[t];
+      }
       __syncthreads();
       if (threadIdx.x == 0) bn = 0u;
     }
@@ -354,37 +264,39 @@ __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ 
   }
 }
 
-// Step 3: the digit-2 bucket from the histogram, digit 3 and the index cut (one block).
-__global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restrict__ cand_key,
-                                                       const int32_t* __restrict__ cand_idx,
-                                                       SelectCtl* __restrict__ ctl, int64_t cap,
-                                                       uint32_t* __restrict__ hist2,
-                                                       const uint32_t* __restrict__ stage2,
-                                                       uint32_t* __restrict__ hist_c, int pruned) {
+// Step 3 (one block): the digit-2 bucket from the histogram, digit 3 over the staged keys,
+// and the index cut among the staged keys equal to tau. Clears the histograms it and
+// k_digit2 consumed for the next call.
+__global__ void __launch_bounds__(kSelBlock) k_select2(SelectCtl* __restrict__ ctl, uint32_t* __restrict__ hist2,
+                                                       const uint32_t* __restrict__ stage_key,
+                                                       const int32_t* __restrict__ stage_idx,
+                                                       uint32_t* __restrict__ hist_c, uint32_t* __restrict__ hist,
+                                                       int pruned, uint32_t k) {
   __shared__ uint32_t h[2048];
   __shared__ uint32_t shw[kSelBlock / 64];
   __shared__ uint32_t res[2];
   __shared__ uint32_t n_tie;
-  const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
   const int64_t n2 = ctl->n_stage2;
   const uint32_t b1 = ctl->b1;
-  const uint32_t need1 = ctl->k - ctl->above1;
+  const uint32_t need1 = k - ctl->above1;
+  const bool dense = dense_cands(ctl, pruned);
 
-  // digit 2 (key bits 19..10) among keys in bucket b1, scanned from the top (histogram
-  // from k_digit2, cleared here for the next call)
+  // digit 2 (key bits 19..10) among keys in bucket b1, scanned from the top
   for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) {
     h[b] = hist2[b];
     hist2[b] = 0u;
   }
-  if (pruned)  // the candidates' digit-1 histogram, read by k_digit2, cleared for the next call
+  if (pruned)
     for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) hist_c[b] = 0u;
+  if (dense)
+    for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) hist[b] = 0u;
   __syncthreads();
   find_bucket<kSelBlock, kDigitBins>(h, true, need1, shw, res);
   const uint32_t pre2 = (b1 << 10) | res[0];
   const uint32_t need2 = need1 - res[1];
   __syncthreads();
 
-  // digit 3 (key bits 9..0) among the bucket's keys with the 22-bit prefix pre2
+  // digit 3 (key bits 9..0) among the staged keys with the 22-bit prefix pre2
   for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
   __syncthreads();
   for (int64_t t0 = 0; t0 < n2; t0 += (int64_t)kSelUnroll * kSelBlock) {
@@ -392,7 +304,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
 #pragma unroll
     for (int m = 0; m < kSelUnroll; ++m) {
       const int64_t t = t0 + (int64_t)m * kSelBlock + threadIdx.x;
-      key[m] = t < n2 ? stage2[t] : 0u;
+      key[m] = t < n2 ? stage_key[t] : 0u;
     }
 #pragma unroll
     for (int m = 0; m < kSelUnroll; ++m) {
@@ -407,26 +319,27 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
   const uint32_t n_eq = h[res[0]];
   __syncthreads();
 
+  // every key equal to tau is in the stage (its digit 1 is b1)
   uint32_t iota = 0x7fffffffu;
   if (need3 < n_eq && n_eq <= kTieMax) {
     // few keys equal to tau (the usual case: an estimate is one table cell): one pass
-    // collects their indices in LDS, and iota is the one with exactly need3 - 1 smaller
-    // (candidate indices are distinct)
+    // collects their coordinates in LDS, and iota is the one with exactly need3 - 1 smaller
+    // (the coordinates are distinct)
     if (threadIdx.x == 0) n_tie = 0u;
     __syncthreads();
-    for (int64_t t0 = 0; t0 < n; t0 += (int64_t)kSelUnroll * kSelBlock) {
+    for (int64_t t0 = 0; t0 < n2; t0 += (int64_t)kSelUnroll * kSelBlock) {
       uint32_t key[kSelUnroll];
 #pragma unroll
       for (int m = 0; m < kSelUnroll; ++m) {
         const int64_t t = t0 + (int64_t)m * kSelBlock + threadIdx.x;
-        key[m] = t < n ? cand_key[t] : 0u;
+        key[m] = t < n2 ? stage_key[t] : 0u;
       }
 #pragma unroll
       for (int m = 0; m < kSelUnroll; ++m) {
         const int64_t t = t0 + (int64_t)m * kSelBlock + threadIdx.x;
-        if (t < n && key[m] == tau) {
+        if (t < n2 && key[m] == tau) {
           const uint32_t pos = atomicAdd(&n_tie, 1u);
-          if (pos < (uint32_t)kTieMax) h[pos] = (uint32_t)cand_idx[t];
+          if (pos < (uint32_t)kTieMax) h[pos] = (uint32_t)stage_idx[t];
         }
       }
     }
@@ -444,8 +357,11 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
     // many ties: ascending index digits among keys equal to tau: bits 30..21, 20..10, 9..0
     for (int b = threadIdx.x; b < 1024; b += kSelBlock) h[b] = 0u;
     __syncthreads();
-    for (int64_t t = threadIdx.x; t < n; t += kSelBlock)
-      if (cand_key[t] == tau) atomicAdd(&h[(uint32_t)cand_idx[t] >> 21], 1u);
+    for (int64_t t0 = 0; t0 < n2; t0 += kSelBlock) {  // block-uniform
+      const int64_t t = t0 + threadIdx.x;
+      const bool tie = t < n2 && stage_key[t] == tau;
+      hist_add(h, tie, tie ? (uint32_t)stage_idx[t] >> 21 : 0u);
+    }
     __syncthreads();
     find_bucket<kSelBlock, 1024>(h, false, need3, shw, res);
     const uint32_t c1 = res[0];
@@ -454,9 +370,11 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
 
     for (int b = threadIdx.x; b < 2048; b += kSelBlock) h[b] = 0u;
     __syncthreads();
-    for (int64_t t = threadIdx.x; t < n; t += kSelBlock) {
-      const uint32_t ix = (uint32_t)cand_idx[t];
-      if (cand_key[t] == tau && (ix >> 21) == c1) atomicAdd(&h[(ix >> 10) & 2047u], 1u);
+    for (int64_t t0 = 0; t0 < n2; t0 += kSelBlock) {
+      const int64_t t = t0 + threadIdx.x;
+      const uint32_t ix = t < n2 && stage_key[t] == tau ? (uint32_t)stage_idx[t] : 0xffffffffu;
+      const bool in = ix != 0xffffffffu && (ix >> 21) == c1;
+      hist_add(h, in, (ix >> 10) & 2047u);
     }
     __syncthreads();
     find_bucket<kSelBlock, 2048>(h, false, needc, shw, res);
@@ -466,9 +384,11 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
 
     for (int b = threadIdx.x; b < 1024; b += kSelBlock) h[b] = 0u;
     __syncthreads();
-    for (int64_t t = threadIdx.x; t < n; t += kSelBlock) {
-      const uint32_t ix = (uint32_t)cand_idx[t];
-      if (cand_key[t] == tau && (ix >> 10) == pre_i) atomicAdd(&h[ix & 1023u], 1u);
+    for (int64_t t0 = 0; t0 < n2; t0 += kSelBlock) {
+      const int64_t t = t0 + threadIdx.x;
+      const uint32_t ix = t < n2 && stage_key[t] == tau ? (uint32_t)stage_idx[t] : 0xffffffffu;
+      const bool in = ix != 0xffffffffu && (ix >> 10) == pre_i;
+      hist_add(h, in, ix & 1023u);
     }
     __syncthreads();
     find_bucket<kSelBlock, 1024>(h, false, needd, shw, res);
@@ -478,7 +398,6 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
     ctl->tau = tau;
     ctl->iota = iota;
     ctl->n_stage2 = 0u;
-    if ((uint64_t)ctl->n_cand > (uint64_t)cap) ctl->status = 1u;
   }
 }
 
@@ -487,15 +406,17 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(const uint32_t* __restric
 
 __global__ void __launch_bounds__(kBlock) k_finalize(const uint32_t* __restrict__ cand_key,
                                                      const int32_t* __restrict__ cand_idx,
-                                                     const SelectCtl* __restrict__ ctl, int64_t cap,
-                                                     uint32_t* __restrict__ bitmap) {
-  const int64_t n = ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap;
+                                                     const SelectCtl* __restrict__ ctl, int64_t cap, int64_t d,
+                                                     int pruned, uint32_t* __restrict__ bitmap) {
+  const bool dense = dense_cands(ctl, pruned);
+  const int64_t n = dense ? d : (ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap);
   const uint32_t tau = ctl->tau, iota = ctl->iota;
   const int64_t stride = (int64_t)gridDim.x * kBlock;
   for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n; t += stride) {
     const uint32_t key = cand_key[t];
-    const uint32_t ix = (uint32_t)cand_idx[t];
-    if (key > tau || (key == tau && ix <= iota)) atomicOr(&bitmap[ix >> 5], 1u << (ix & 31u));
+    if (key < tau) continue;
+    const uint32_t ix = dense ? (uint32_t)t : (uint32_t)cand_idx[t];
+    if (key > tau || ix <= iota) atomicOr(&bitmap[ix >> 5], 1u << (ix & 31u));
   }
 }
 
@@ -954,7 +875,8 @@ template <int R>
 __global__ void __launch_bounds__(kBlock) k_unsketch_hm(HashSet hs, const float* __restrict__ merged, int64_t d,
                                                         const uint32_t* __restrict__ rnd, float* __restrict__ est,
                                                         uint32_t* __restrict__ keys, uint32_t* __restrict__ hist,
-                                                        SelectCtl* __restrict__ ctl, int gated, int count_heavy) {
+                                                        uint32_t* __restrict__ bitmap, SelectCtl* __restrict__ ctl,
+                                                        int gated, int count_heavy) {
   if (gated && !fallback_needed(ctl)) return;
   __shared__ uint32_t h[kDigit1Bins];
   __shared__ uint32_t nh;
@@ -994,6 +916,7 @@ __global__ void __launch_bounds__(kBlock) k_unsketch_hm(HashSet hs, const float*
     mine += heavy ? 1u : 0u;
     keys[i] = key;
     atomicAdd(&h[key >> kDigit1Shift], 1u);
+    if ((i & 31) == 0) bitmap[i >> 5] = 0u;
   }
   if (mine) atomicAdd(&nh, mine);
   __syncthreads();
@@ -1013,7 +936,7 @@ __global__ void k_hm_out(const SelectCtl* __restrict__ ctl, int64_t* __restrict_
 template <int R>
 void launch_unsketch_r(gs_ctx* x, hipStream_t s, const float* merged, float* est, SelectCtl* gate) {
   hipLaunchKernelGGL(k_unsketch<R>, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->hs, merged,
-                     x->d, est, x->keys, x->hist, gate);
+                     x->d, est, x->cand_key, x->hist, x->bitmap, gate);
 }
 
 template <int R, bool HM>
@@ -1061,25 +984,15 @@ hipError_t allow_prune_lds(size_t bytes) {
   return hipSuccess;
 }
 
-// select1 -> compact -> select2 -> finalize -> emit over the keys in x->keys (digit-1
-// histogram already in x->hist). gated: act only if the pruned pass raised the fallback.
-hipError_t launch_select_tail(gs_ctx* x, hipStream_t s, int64_t k, int gated, int32_t* idx) {
-  hipLaunchKernelGGL(k_select1, dim3(1), dim3(kSelBlock), 0, s, x->hist, x->ctl, (uint32_t)k, gated);
-  {
-    // contiguous ranges, a multiple of 1024 keys each (so bitmap words never straddle blocks)
-    const int64_t nb = grid_for(x->d, 4 * kBlock, 4 * x->num_cus);
-    int64_t per_block = (x->d + nb - 1) / nb;
-    per_block = (per_block + 4 * kBlock - 1) / (4 * kBlock) * (4 * kBlock);
-    const int64_t grid = (x->d + per_block - 1) / per_block;
-    hipLaunchKernelGGL(k_compact, dim3((unsigned)grid), dim3(kBlock), 0, s, x->keys, x->d, x->ctl, x->cand_key,
-                       x->cand_idx, x->cand_cap, x->bitmap, per_block, gated);
-  }
-  hipLaunchKernelGGL(k_digit2, dim3(x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->ctl, x->cand_cap, x->hist2,
-                     x->keys, x->hist_c, gated);
-  hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap,
-                     x->hist2, x->keys, x->hist_c, gated);
+// digit2 -> select2 -> finalize -> emit over the candidates: the pruned pass's (pruned = 1,
+// unless it fell short of k) or the full estimate's dense ones.
+hipError_t launch_select_tail(gs_ctx* x, hipStream_t s, int64_t k, int pruned, int32_t* idx) {
+  hipLaunchKernelGGL(k_digit2, dim3(x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap,
+                     x->d, x->hist_c, x->hist, pruned, (uint32_t)k, x->hist2, x->keys, x->stage_idx);
+  hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->ctl, x->hist2, x->keys, x->stage_idx, x->hist_c,
+                     x->hist, pruned, (uint32_t)k);
   hipLaunchKernelGGL(k_finalize, dim3(4 * x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl,
-                     x->cand_cap, x->bitmap);
+                     x->cand_cap, x->d, pruned, x->bitmap);
   const int64_t words = (x->d + 31) / 32;
   hipLaunchKernelGGL(k_emit_count, dim3((unsigned)x->emit_blocks), dim3(kSelBlock), 0, s, x->bitmap, words,
                      x->blockcnt);
@@ -1185,7 +1098,8 @@ hipError_t launch_heavymix_topk(gs_ctx* x, hipStream_t s, const float* merged, i
   case RR:                                                                                                         \
     if (prune) launch_prune_r<RR, true>(x, s, merged, k, rnd);                                                     \
     hipLaunchKernelGGL(k_unsketch_hm<RR>, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->hs, \
-                       merged, x->d, rnd, est, x->keys, x->hist, x->ctl, prune ? 1 : 0, prune ? 0 : 1);            \
+                       merged, x->d, rnd, est, x->cand_key, x->hist, x->bitmap, x->ctl, prune ? 1 : 0,            \
+                       prune ? 0 : 1);                                                                             \
     break;
     GS_R_CASE(1) GS_R_CASE(2) GS_R_CASE(3) GS_R_CASE(4) GS_R_CASE(5) GS_R_CASE(6) GS_R_CASE(7) GS_R_CASE(8)
     GS_R_CASE(9) GS_R_CASE(10) GS_R_CASE(11) GS_R_CASE(12) GS_R_CASE(13) GS_R_CASE(14) GS_R_CASE(15) GS_R_CASE(16)
