@@ -21,6 +21,7 @@
 //   5. emit: the bitmap is turned into ascending indices (per-block popcounts, then a
 //      block-local scan offset by the preceding blocks' totals).
 #include <cmath>
+#include <type_traits>
 
 #include "gs_internal.hpp"
 
@@ -573,22 +574,27 @@ __global__ void __launch_bounds__(kBlock) k_coarse(const uint32_t* __restrict__ 
 // dynamic LDS of k_pruned: [map words?][buf indices]
 constexpr int kPruneBlock = 1024;  // 16 waves per CU; the heavy bitmap fills the LDS
 
-// coarse_log2 > 0: `lmap` is the coarse map (one bit per 2^coarse_log2 cells, set when any
-// of them is heavy), kept in LDS; a set coarse bit is confirmed in the fine map `heavy` in
-// global memory, so the count is the same as with the fine map alone.
-template <int R, bool HM, bool COARSE>
+// Where the pruned pass finds a cell's heavy bit. The map's address space is fixed at
+// compile time so that LDS lookups are LDS instructions, not generic ones.
+constexpr int kMapFine = 0;    // the fine map (one bit per cell), copied into LDS
+constexpr int kMapCoarse = 1;  // a coarse map in LDS (one bit per 2^coarse_log2 cells, set when
+                               // any of them is heavy); a set bit is confirmed in the fine map
+                               // in global memory, so the count equals the fine map's
+constexpr int kMapGlobal = 2;  // the fine map read from global memory
+
+template <int R, bool HM, int MAP>
 __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, SelectCtl* __restrict__ ctl,
                                                    const uint32_t* __restrict__ heavy,
                                                    const uint32_t* __restrict__ lmap, int64_t map_words,
-                                                   int map_in_lds, int coarse_log2, int buf_cap,
-                                                   uint32_t* __restrict__ queue, uint32_t* __restrict__ bitmap,
-                                                   const uint32_t* __restrict__ rnd) {
+                                                   int coarse_log2, int buf_cap, uint32_t* __restrict__ queue,
+                                                   uint32_t* __restrict__ bitmap, const uint32_t* __restrict__ rnd) {
   constexpr int U = 4;  // coordinates per lane per pass: independent hash chains in flight
+  // flat cell index j*c + col; below 2^32 whenever a map fits in LDS
+  using Cell = typename std::conditional<MAP == kMapGlobal, uint64_t, uint32_t>::type;
   extern __shared__ uint32_t sm[];
   __shared__ uint32_t bn, gbase;
-  const uint32_t* map = lmap;
   uint32_t* buf = sm;
-  if (map_in_lds) {
+  if constexpr (MAP != kMapGlobal) {
     // map_words is even and the map 8-byte aligned: copy 16 bytes per lane, 8 loads in flight
     const int64_t n4 = map_words / 4;
     const uint4* src = reinterpret_cast<const uint4*>(lmap);
@@ -603,7 +609,6 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
     }
     for (; w < n4; w += kPruneBlock) dst[w] = src[w];
     for (int64_t x = 4 * n4 + threadIdx.x; x < map_words; x += kPruneBlock) sm[x] = lmap[x];
-    map = sm;
     buf = sm + map_words;
   }
   RowConst kr[R];
@@ -624,23 +629,30 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
       hb[j][m] = mod_mersenne_affine(kr[j].a, kr[j].b, (uint32_t)(base0 + threadIdx.x + (int64_t)m * kPruneBlock));
   }
   for (int64_t base = base0; base < d; base += stride) {  // block-uniform
+    // all U * R lookups first (independent), then the appends
+    uint32_t cnt[U];
 #pragma unroll
     for (int m = 0; m < U; ++m) {
-      const int64_t i = base + threadIdx.x + (int64_t)m * kPruneBlock;
-      int cnt = 0;
+      cnt[m] = 0u;
 #pragma unroll
       for (int j = 0; j < R; ++j) {
         const uint32_t col = mod_c(hb[j][m], kr[j].c, kr[j].magic, kr[j].shift);
         hb[j][m] = add_mod_mersenne(hb[j][m], db[j]);
-        const int64_t e = (int64_t)j * kr[j].c + col;
-        if constexpr (!COARSE) {
-          cnt += (map[e >> 5] >> (e & 31)) & 1u;
+        const Cell e = (Cell)j * kr[j].c + col;
+        if constexpr (MAP == kMapFine) {
+          cnt[m] += (sm[e >> 5] >> (e & 31)) & 1u;
+        } else if constexpr (MAP == kMapCoarse) {
+          const uint32_t cb = e >> coarse_log2;
+          if ((sm[cb >> 5] >> (cb & 31)) & 1u) cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
         } else {
-          const int64_t cb = e >> coarse_log2;
-          if ((map[cb >> 5] >> (cb & 31)) & 1u) cnt += (heavy[e >> 5] >> (e & 31)) & 1u;
+          cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
         }
       }
-      bool keep = i < d && cnt >= need;
+    }
+#pragma unroll
+    for (int m = 0; m < U; ++m) {
+      const int64_t i = base + threadIdx.x + (int64_t)m * kPruneBlock;
+      bool keep = i < d && cnt[m] >= (uint32_t)need;
       if constexpr (HM) keep = keep || (i < d && (rnd[i] >> 1) >= tau0);
       if (keep) {
         const uint32_t pos = atomicAdd(&bn, 1u);
@@ -956,27 +968,32 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
                      x->heavy, HM ? 1 : 0);
   // with the bitmap in LDS one block fits a CU: launch one per CU so the map is loaded once
   const int pgrid = grid_for(x->d, 4 * kPruneBlock, x->prune_map_in_lds ? x->num_cus : 2 * x->num_cus);
-  if (x->prune_coarse_log2 > 0)
+  const dim3 pb(kPruneBlock);
+  if (!x->prune_map_in_lds) {
+    hipLaunchKernelGGL((k_pruned<R, HM, kMapGlobal>), dim3(pgrid), pb, x->prune_lds, s, x->hs, x->d, x->ctl,
+                       x->heavy, x->heavy, x->prune_map_words, 0, x->prune_buf_cap, x->keys, x->bitmap, rnd);
+  } else if (x->prune_coarse_log2 > 0) {
     hipLaunchKernelGGL(k_coarse, dim3(grid_for(x->prune_coarse_words, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s,
                        x->heavy, (rc + 63) / 64 * 2, x->prune_coarse_log2, x->coarse, x->prune_coarse_words);
-  if (x->prune_coarse_log2 > 0)
-    hipLaunchKernelGGL((k_pruned<R, HM, true>), dim3(pgrid), dim3(kPruneBlock), x->prune_lds, s, x->hs, x->d,
-                       x->ctl, x->heavy, x->coarse, x->prune_map_words, x->prune_map_in_lds, x->prune_coarse_log2,
-                       x->prune_buf_cap, x->keys, x->bitmap, rnd);
-  else
-    hipLaunchKernelGGL((k_pruned<R, HM, false>), dim3(pgrid), dim3(kPruneBlock), x->prune_lds, s, x->hs, x->d,
-                       x->ctl, x->heavy, x->heavy, x->prune_map_words, x->prune_map_in_lds, 0, x->prune_buf_cap,
-                       x->keys, x->bitmap, rnd);
+    hipLaunchKernelGGL((k_pruned<R, HM, kMapCoarse>), dim3(pgrid), pb, x->prune_lds, s, x->hs, x->d, x->ctl,
+                       x->heavy, x->coarse, x->prune_map_words, x->prune_coarse_log2, x->prune_buf_cap, x->keys,
+                       x->bitmap, rnd);
+  } else {
+    hipLaunchKernelGGL((k_pruned<R, HM, kMapFine>), dim3(pgrid), pb, x->prune_lds, s, x->hs, x->d, x->ctl,
+                       x->heavy, x->heavy, x->prune_map_words, 0, x->prune_buf_cap, x->keys, x->bitmap, rnd);
+  }
   hipLaunchKernelGGL((k_survivors<R, HM>), dim3(x->num_cus), dim3(kBlock), 0, s, x->hs, merged, x->ctl, x->keys,
                      x->cand_key, x->cand_idx, x->cand_cap, rnd, x->hist_c);
 }
 
 template <int R>
 hipError_t allow_prune_lds(size_t bytes) {
-  const void* fns[] = {reinterpret_cast<const void*>(&k_pruned<R, false, false>),
-                       reinterpret_cast<const void*>(&k_pruned<R, true, false>),
-                       reinterpret_cast<const void*>(&k_pruned<R, false, true>),
-                       reinterpret_cast<const void*>(&k_pruned<R, true, true>)};
+  const void* fns[] = {reinterpret_cast<const void*>(&k_pruned<R, false, kMapFine>),
+                       reinterpret_cast<const void*>(&k_pruned<R, true, kMapFine>),
+                       reinterpret_cast<const void*>(&k_pruned<R, false, kMapCoarse>),
+                       reinterpret_cast<const void*>(&k_pruned<R, true, kMapCoarse>),
+                       reinterpret_cast<const void*>(&k_pruned<R, false, kMapGlobal>),
+                       reinterpret_cast<const void*>(&k_pruned<R, true, kMapGlobal>)};
   for (const void* f : fns) {
     const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess) return e;
