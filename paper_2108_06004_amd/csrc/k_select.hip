@@ -20,6 +20,7 @@
 //   4. k_finalize: candidates with key > tau, or key == tau and index <= iota, set their bit;
 //   5. emit: the bitmap is turned into ascending indices (per-block popcounts, then a
 //      block-local scan offset by the preceding blocks' totals).
+#include <algorithm>
 #include <cmath>
 #include <type_traits>
 
@@ -649,6 +650,10 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
         }
       }
     }
+    // keep the lookups together, ahead of the appends (the compiler would otherwise sink
+    // each coordinate's into its own guarded block and wait once per coordinate)
+#pragma unroll
+    for (int m = 0; m < U; ++m) asm volatile("" : "+v"(cnt[m]));
 #pragma unroll
     for (int m = 0; m < U; ++m) {
       const int64_t i = base + threadIdx.x + (int64_t)m * kPruneBlock;
@@ -1004,7 +1009,11 @@ hipError_t allow_prune_lds(size_t bytes) {
 // digit2 -> select2 -> finalize -> emit over the candidates: the pruned pass's (pruned = 1,
 // unless it fell short of k) or the full estimate's dense ones.
 hipError_t launch_select_tail(gs_ctx* x, hipStream_t s, int64_t k, int pruned, int32_t* idx) {
-  hipLaunchKernelGGL(k_digit2, dim3(x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap,
+  // one block per CU for the pruned candidates (a few times k); the full estimate's dense
+  // ones (d) get up to eight per CU (a pruned pass's fallback keeps the smaller grid)
+  int g2 = x->num_cus;
+  if (!pruned) g2 = std::max(g2, grid_for(x->d, 8192, 8 * x->num_cus));
+  hipLaunchKernelGGL(k_digit2, dim3(g2), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap,
                      x->d, x->hist_c, x->hist, pruned, (uint32_t)k, x->hist2, x->keys, x->stage_idx);
   hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->ctl, x->hist2, x->keys, x->stage_idx, x->hist_c,
                      x->hist, pruned, (uint32_t)k);
