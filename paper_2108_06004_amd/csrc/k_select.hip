@@ -642,11 +642,16 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
         const Cell e = (Cell)j * kr[j].c + col;
         if constexpr (MAP == kMapFine) {
           cnt[m] += (sm[e >> 5] >> (e & 31)) & 1u;
-        } else if constexpr (MAP == kMapCoarse) {
-          const uint32_t cb = e >> coarse_log2;
-          if ((sm[cb >> 5] >> (cb & 31)) & 1u) cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
         } else {
-          cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
+          // global reads are the cost here (L2 requests): skip a row once the coordinate
+          // cannot reach `need` with the rows left, which leaves the keep decision unchanged
+          const bool alive = cnt[m] + (uint32_t)(R - j) >= (uint32_t)need;
+          if constexpr (MAP == kMapCoarse) {
+            const uint32_t cb = e >> coarse_log2;
+            if (alive && ((sm[cb >> 5] >> (cb & 31)) & 1u)) cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
+          } else {
+            if (alive) cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
+          }
         }
       }
     }
