@@ -51,9 +51,10 @@ __global__ void __launch_bounds__(kBlock) k_accumulate1(const float* __restrict_
 // A wave covers CW = 64/G consecutive coordinates: lane l takes coordinate base + l/G and
 // the 16-byte group h = l%G of its row (workers 4h..4h+3), so consecutive lanes read and
 // write consecutive 16-byte pieces of u and v; the four gradient values come from four
-// worker rows of g (4-byte loads, 4*CW bytes contiguous per row and wave). Four chunks per
-// lane are in flight per iteration. Only full chunks run here; the tail goes to
-// k_accumulate_il_any.
+// worker rows of g (4-byte loads, 4*CW bytes contiguous per row and wave). Each pass a wave
+// takes four consecutive chunks, all in flight together, so when CW*4 bytes is less than a
+// 128-byte line (G = 3, 4) the rest of the line is read by the wave's next instruction.
+// Only full chunks run here; the tail goes to k_accumulate_il_any.
 template <int G>
 __global__ void __launch_bounds__(kBlock) k_accumulate_il(const float* __restrict__ g, float* __restrict__ u,
                                                           float* __restrict__ v, int64_t d, float rho) {
@@ -66,12 +67,13 @@ __global__ void __launch_bounds__(kBlock) k_accumulate_il(const float* __restric
   const int64_t sub = lane / G;
   const int64_t nch = d / CW;
   const int64_t wstride = (int64_t)gridDim.x * (kBlock / 64);
-  int64_t ch = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
-  for (; ch + (U - 1) * wstride < nch; ch += U * wstride) {
+  const int64_t ngr = nch / U;  // groups of U consecutive chunks, one group per wave and pass
+  const int64_t w0 = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  for (int64_t gr = w0; gr < ngr; gr += wstride) {
     f4 gg[U], uu[U], ww[U];
 #pragma unroll
     for (int m = 0; m < U; ++m) {
-      const int64_t i = (ch + m * wstride) * CW + sub;
+      const int64_t i = (gr * U + m) * CW + sub;
       const float* gq = g + (int64_t)(4 * h) * d + i;
       gg[m].x = __builtin_nontemporal_load(gq);
       gg[m].y = __builtin_nontemporal_load(gq + d);
@@ -82,14 +84,14 @@ __global__ void __launch_bounds__(kBlock) k_accumulate_il(const float* __restric
     }
 #pragma unroll
     for (int m = 0; m < U; ++m) {
-      const int64_t i = (ch + m * wstride) * CW + sub;
+      const int64_t i = (gr * U + m) * CW + sub;
       uu[m] = rho * uu[m] + gg[m];
       ww[m] = ww[m] + uu[m];
       __builtin_nontemporal_store(uu[m], reinterpret_cast<f4*>(u + i * PP) + h);
       __builtin_nontemporal_store(ww[m], reinterpret_cast<f4*>(v + i * PP) + h);
     }
   }
-  for (; ch < nch; ch += wstride) {
+  for (int64_t ch = ngr * U + w0; ch < nch; ch += wstride) {  // chunks past the last group
     const int64_t i = ch * CW + sub;
     const float* gq = g + (int64_t)(4 * h) * d + i;
     f4 gg;
