@@ -77,7 +77,7 @@ def stage_kernels(w, layout: str = "interleaved") -> dict:
         "accumulate": acc,
         "sketch": [f"k_pull<{w.P}, {4 if w.P <= 4 else 6}, true>"],  # packed lists (the library's choice here)
         "merge": [f"k_merge_partials<{w.P}>"],
-        "select": [f"k_sample<{w.r}, false>", "k_tau0", "k_heavy", f"k_pruned<{w.r}, false, 0>",
+        "select": [f"k_sample<{w.r}, false>", "k_heavy", f"k_pruned<{w.r}, false, 0>",
                    f"k_survivors<{w.r}, false>", f"k_unsketch<{w.r}>", "k_digit2", "k_select2", "k_finalize",
                    "k_emit_count", "k_emit_write"],
         "gather_reset": [f"k_gather_reset<{w.P}>"],

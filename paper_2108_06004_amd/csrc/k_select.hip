@@ -441,7 +441,7 @@ __device__ __forceinline__ uint32_t estimate_key(const RowConst (&kr)[R], const 
 
 // Sampled keys at M evenly spaced coordinates: |est| keys, or (HEAVYMIX) the fill keys
 // rnd >> 1, whose rho-th largest bounds the fill from below. Their digit-1 histogram is
-// added into hist_s for k_tau0.
+// added into hist_s for k_heavy's bound.
 template <int R, bool HM>
 __global__ void __launch_bounds__(kBlock) k_sample(HashSet hs, const float* __restrict__ merged, int64_t d, int M,
                                                    const uint32_t* __restrict__ rnd, uint32_t* __restrict__ out,
@@ -472,63 +472,68 @@ __global__ void __launch_bounds__(kBlock) k_sample(HashSet hs, const float* __re
   }
 }
 
-// tau0 = the rho-th largest sampled key (one block): digit 1 from k_sample's histogram
-// (cleared here for the next call), digits 2 and 3 over the sampled keys held in registers.
-__global__ void __launch_bounds__(kSelBlock) k_tau0(const uint32_t* __restrict__ sample, int M, uint32_t rho,
-                                                    SelectCtl* __restrict__ ctl, uint32_t k,
-                                                    uint32_t* __restrict__ hist_s) {
-  constexpr int kPer = kSampleMax / kSelBlock;
-  __shared__ uint32_t h[kDigitBins];
-  __shared__ uint32_t shw[kSelBlock / 64];
-  __shared__ uint32_t res[2];
+// tau0 = the rho-th largest sampled key, found by one block of BS threads: digit 1 from
+// k_sample's histogram hist_s, digits 2 and 3 over the sampled keys held in registers. h is
+// an LDS histogram of kDigitBins words. All threads must call it; each gets tau0.
+template <int BS>
+__device__ uint32_t sampled_bound(const uint32_t* __restrict__ sample, int M, uint32_t rho,
+                                  const uint32_t* __restrict__ hist_s, uint32_t* h, uint32_t* shw, uint32_t* res) {
+  constexpr int kPer = kSampleMax / BS;
   uint32_t key[kPer];
 #pragma unroll
   for (int m = 0; m < kPer; ++m) {
-    const int t = m * kSelBlock + threadIdx.x;
+    const int t = m * BS + threadIdx.x;
     key[m] = t < M ? sample[t] : 0u;
   }
-  for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
-  find_bucket<kSelBlock, kDigit1Bins>(hist_s, true, rho, shw, res);
+  for (int b = threadIdx.x; b < kDigitBins; b += BS) h[b] = 0u;
+  find_bucket<BS, kDigit1Bins>(hist_s, true, rho, shw, res);
   const uint32_t b1 = res[0], need2 = rho - res[1];
-  for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) hist_s[b] = 0u;
 #pragma unroll
   for (int m = 0; m < kPer; ++m) {
-    const bool take = m * kSelBlock + (int)threadIdx.x < M && (key[m] >> kDigit1Shift) == b1;
+    const bool take = m * BS + (int)threadIdx.x < M && (key[m] >> kDigit1Shift) == b1;
     hist_add(h, take, (key[m] >> 10) & 1023u);
   }
   __syncthreads();
-  find_bucket<kSelBlock, kDigitBins>(h, true, need2, shw, res);
+  find_bucket<BS, kDigitBins>(h, true, need2, shw, res);
   const uint32_t pre = (b1 << 10) | res[0], need3 = need2 - res[1];
-  for (int b = threadIdx.x; b < kDigitBins; b += kSelBlock) h[b] = 0u;
+  for (int b = threadIdx.x; b < kDigitBins; b += BS) h[b] = 0u;
   __syncthreads();
 #pragma unroll
   for (int m = 0; m < kPer; ++m) {
-    const bool take = m * kSelBlock + (int)threadIdx.x < M && (key[m] >> 10) == pre;
+    const bool take = m * BS + (int)threadIdx.x < M && (key[m] >> 10) == pre;
     hist_add(h, take, key[m] & 1023u);
   }
   __syncthreads();
-  find_bucket<kSelBlock, kDigitBins>(h, true, need3, shw, res);
-  if (threadIdx.x == 0) {
-    ctl->tau0 = (pre << 10) | res[0];
+  find_bucket<BS, kDigitBins>(h, true, need3, shw, res);
+  return (pre << 10) | res[0];
+}
+
+// Heavy-cell bitmap: bit e of the flat [r][c] sketch is |merged[e]| >= tau0, or (HEAVYMIX,
+// hm = 1) merged[e]^2 >= theta in fp64 (one ballot per 64 cells); with hm the sampled fill
+// bound tau0 is still found here, for the pruned pass. A coordinate with
+// est^2 >= theta has ceil(r/2) cells with |cell| >= |est| (see the pruned pass), and the
+// squares of fp32 values are exact in fp64, so those cells pass the same test.
+// Every block first finds tau0 itself (the sampled keys are read from L2; block 0 records
+// it and resets the selection counters), so no single-block kernel runs in between.
+__global__ void __launch_bounds__(kSelBlock) k_heavy(const float* __restrict__ merged, int64_t rc,
+                                                  SelectCtl* __restrict__ ctl, uint32_t* __restrict__ heavy,
+                                                  int hm, const uint32_t* __restrict__ sample, int M,
+                                                  uint32_t rho, uint32_t k, const uint32_t* __restrict__ hist_s) {
+  __shared__ uint32_t h[kDigitBins];
+  __shared__ uint32_t shw[kSelBlock / 64];
+  __shared__ uint32_t res[2];
+  const uint32_t tau0 = sampled_bound<kSelBlock>(sample, M, rho, hist_s, h, shw, res);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    ctl->tau0 = tau0;
     ctl->k = k;
     ctl->n_cand = 0u;
     ctl->n_surv = 0u;
     ctl->fallback = 0u;
     ctl->status = 0u;
   }
-}
-
-// Heavy-cell bitmap: bit e of the flat [r][c] sketch is |merged[e]| >= tau0, or (HEAVYMIX,
-// hm = 1) merged[e]^2 >= theta in fp64 (one ballot per 64 cells). A coordinate with
-// est^2 >= theta has ceil(r/2) cells with |cell| >= |est| (see the pruned pass), and the
-// squares of fp32 values are exact in fp64, so those cells pass the same test.
-__global__ void __launch_bounds__(kBlock) k_heavy(const float* __restrict__ merged, int64_t rc,
-                                                  const SelectCtl* __restrict__ ctl, uint32_t* __restrict__ heavy,
-                                                  int hm) {
-  const uint32_t tau0 = ctl->tau0;
   const double theta = ctl->theta;
-  const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t base = ((int64_t)blockIdx.x * kBlock + threadIdx.x) & ~63ll; base < rc; base += stride) {
+  const int64_t stride = (int64_t)gridDim.x * kSelBlock;
+  for (int64_t base = ((int64_t)blockIdx.x * kSelBlock + threadIdx.x) & ~63ll; base < rc; base += stride) {
     const int64_t e = base + (threadIdx.x & 63);
     bool hv = false;
     if (e < rc) {
@@ -588,12 +593,15 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
                                                    const uint32_t* __restrict__ heavy,
                                                    const uint32_t* __restrict__ lmap, int64_t map_words,
                                                    int coarse_log2, int buf_cap, uint32_t* __restrict__ queue,
-                                                   uint32_t* __restrict__ bitmap, const uint32_t* __restrict__ rnd) {
+                                                   uint32_t* __restrict__ bitmap, const uint32_t* __restrict__ rnd,
+                                                   uint32_t* __restrict__ hist_s) {
   constexpr int U = 4;  // coordinates per lane per pass: independent hash chains in flight
   // flat cell index j*c + col; below 2^32 whenever a map fits in LDS
   using Cell = typename std::conditional<MAP == kMapGlobal, uint64_t, uint32_t>::type;
   extern __shared__ uint32_t sm[];
   __shared__ uint32_t bn, gbase;
+  if (blockIdx.x == 0)  // the samples' histogram, read by k_heavy, cleared for the next call
+    for (int b = threadIdx.x; b < kDigit1Bins; b += kPruneBlock) hist_s[b] = 0u;
   uint32_t* buf = sm;
   if constexpr (MAP != kMapGlobal) {
     // map_words is even and the map 8-byte aligned: copy 16 bytes per lane, 8 loads in flight
@@ -971,26 +979,26 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
   if (rho_d < 1) rho_d = 1;
   hipLaunchKernelGGL((k_sample<R, HM>), dim3((M + kBlock - 1) / kBlock), dim3(kBlock), 0, s, x->hs, merged, x->d, M,
                      rnd, x->sample_keys, x->hist_s);
-  hipLaunchKernelGGL(k_tau0, dim3(1), dim3(kSelBlock), 0, s, x->sample_keys, M, (uint32_t)rho_d, x->ctl, (uint32_t)k,
-                     x->hist_s);
   const int64_t rc = (int64_t)x->r * x->c;
-  hipLaunchKernelGGL(k_heavy, dim3(grid_for(rc, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, merged, rc, x->ctl,
-                     x->heavy, HM ? 1 : 0);
+  hipLaunchKernelGGL(k_heavy, dim3(grid_for(rc, kSelBlock, x->num_cus)), dim3(kSelBlock), 0, s, merged, rc, x->ctl,
+                     x->heavy, HM ? 1 : 0, x->sample_keys, M, (uint32_t)rho_d, (uint32_t)k, x->hist_s);
   // with the bitmap in LDS one block fits a CU: launch one per CU so the map is loaded once
   const int pgrid = grid_for(x->d, 4 * kPruneBlock, x->prune_map_in_lds ? x->num_cus : 2 * x->num_cus);
   const dim3 pb(kPruneBlock);
   if (!x->prune_map_in_lds) {
     hipLaunchKernelGGL((k_pruned<R, HM, kMapGlobal>), dim3(pgrid), pb, x->prune_lds, s, x->hs, x->d, x->ctl,
-                       x->heavy, x->heavy, x->prune_map_words, 0, x->prune_buf_cap, x->keys, x->bitmap, rnd);
+                       x->heavy, x->heavy, x->prune_map_words, 0, x->prune_buf_cap, x->keys, x->bitmap, rnd,
+                       x->hist_s);
   } else if (x->prune_coarse_log2 > 0) {
     hipLaunchKernelGGL(k_coarse, dim3(grid_for(x->prune_coarse_words, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s,
                        x->heavy, (rc + 63) / 64 * 2, x->prune_coarse_log2, x->coarse, x->prune_coarse_words);
     hipLaunchKernelGGL((k_pruned<R, HM, kMapCoarse>), dim3(pgrid), pb, x->prune_lds, s, x->hs, x->d, x->ctl,
                        x->heavy, x->coarse, x->prune_map_words, x->prune_coarse_log2, x->prune_buf_cap, x->keys,
-                       x->bitmap, rnd);
+                       x->bitmap, rnd, x->hist_s);
   } else {
     hipLaunchKernelGGL((k_pruned<R, HM, kMapFine>), dim3(pgrid), pb, x->prune_lds, s, x->hs, x->d, x->ctl,
-                       x->heavy, x->heavy, x->prune_map_words, 0, x->prune_buf_cap, x->keys, x->bitmap, rnd);
+                       x->heavy, x->heavy, x->prune_map_words, 0, x->prune_buf_cap, x->keys, x->bitmap, rnd,
+                       x->hist_s);
   }
   hipLaunchKernelGGL((k_survivors<R, HM>), dim3(x->num_cus), dim3(kBlock), 0, s, x->hs, merged, x->ctl, x->keys,
                      x->cand_key, x->cand_idx, x->cand_cap, rnd, x->hist_c);
