@@ -60,14 +60,23 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_source_digest() -> str:
-    """SHA-256 over the HIP sources (file names and contents, sorted)."""
-    h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2108_06004_amd", "csrc", "*"))):
-        h.update(os.path.basename(p).encode())
-        with open(p, "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()
+CSRC = os.path.join(ROOT, "paper_2108_06004_amd", "csrc")
+# launch configuration and shared device helpers: a change there can change any kernel
+SHARED_SOURCES = ("gs_api.hip", "gs_internal.hpp", "gs_device.hpp")
+
+
+def file_sha256(path: str) -> str:
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def kernel_source_file(name: str):
+    """The HIP source that defines kernel `name` (template arguments ignored), or None."""
+    base = name.split("<")[0].strip()
+    for p in sorted(glob.glob(os.path.join(CSRC, "*.hip"))):
+        if re.search(r"__global__[^;{]*\b" + re.escape(base) + r"\s*\(", open(p).read()):
+            return os.path.basename(p)
+    return None
 
 
 def stage_kernels(w, layout: str = "interleaved") -> dict:
@@ -86,18 +95,24 @@ def stage_kernels(w, layout: str = "interleaved") -> dict:
 
 def measured_traffic(w, stage: str, layout: str = "interleaved"):
     """HBM-side bytes per launch of `stage` from the committed counter summary, or None when
-    there is none for this workload and state layout or the kernels changed since it was taken."""
+    there is none for this workload and state layout, or when a source file the stage's kernels
+    depend on (their own file and the shared ones) differs from the one the counters ran."""
     path = os.path.join(ROOT, "profiles", f"traffic_gs_step_{w.name}_{layout}.md")
     if not os.path.exists(path):
         return None
     text = open(path).read()
-    m = re.search(r"source_sha256: ([0-9a-f]{64})", text)
-    if not m or m.group(1) != kernel_source_digest():
-        return None
+    recorded = dict(re.findall(r"source_sha256\[([\w.]+)\]: ([0-9a-f]{64})", text))
     table = {name.strip(): float(val) for name, val in re.findall(r"traffic: (.+?) \| ([0-9.]+)", text)}
     names = stage_kernels(w, layout).get(stage)
     if not names or not all(n in table for n in names):
         return None
+    for n in names:
+        f = kernel_source_file(n)
+        if f is None:
+            return None
+        for dep in (f,) + SHARED_SOURCES:
+            if recorded.get(dep) != file_sha256(os.path.join(CSRC, dep)):
+                return None
     return sum(table[n] for n in names)
 
 
