@@ -23,7 +23,6 @@ struct SelectCtl {
   uint32_t n_cand;      // candidates appended by the pruned pass (dense candidates: d)
   uint32_t tau;         // the k-th largest key
   uint32_t iota;        // largest index taken among keys equal to tau
-  uint32_t status;      // 0 ok (reserved)
   uint32_t tau0;        // pruning bound: a key no larger than the k-th key (when no fallback)
   uint32_t fallback;    // 1: fewer than k coordinates reach tau0, run the unpruned selection
   uint32_t n_surv;      // coordinates queued by the pruned pass for an exact estimate
@@ -31,7 +30,6 @@ struct SelectCtl {
   double theta;         // HEAVYMIX: heavy threshold l2sq / k
   unsigned long long n_heavy;  // HEAVYMIX: |H|
   uint32_t n_stage2;    // keys of the digit-1 bucket b1 staged for the digit-3 pass
-  uint32_t pad2;
 };
 constexpr int kSampleMax = 16384;  // sampled estimates for the pruning bound
 

@@ -529,7 +529,6 @@ __global__ void __launch_bounds__(kSelBlock) k_heavy(const float* __restrict__ m
     ctl->n_cand = 0u;
     ctl->n_surv = 0u;
     ctl->fallback = 0u;
-    ctl->status = 0u;
   }
   const double theta = ctl->theta;
   const int64_t stride = (int64_t)gridDim.x * kSelBlock;
