@@ -1,0 +1,91 @@
+"""Host-side logic of bench.py (no GPU): the kernel names it reports exist in the sources, and
+committed traffic counters are used only while the sources they were taken on are unchanged."""
+import hashlib
+import os
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+import synth  # noqa: E402
+
+
+def test_kernel_source_file_maps_kernels_to_their_files():
+    assert bench.kernel_source_file("k_accumulate_il<2>") == "k_stream.hip"
+    assert bench.kernel_source_file("k_pull<8, 6, true>") == "k_pull.hip"
+    assert bench.kernel_source_file("k_digit2") == "k_select.hip"
+    assert bench.kernel_source_file("k_no_such_kernel") is None
+
+
+@pytest.mark.parametrize("layout", ["interleaved", "worker_major"])
+@pytest.mark.parametrize("name", list(synth.WORKLOADS))
+def test_stage_kernels_name_existing_kernels(name, layout):
+    # a renamed or removed kernel left in the stage lists would silently void the roofline's
+    # traffic figure; every name must resolve to a __global__ definition
+    w = synth.WORKLOADS[name]
+    for stage, names in bench.stage_kernels(w, layout).items():
+        for n in names:
+            assert bench.kernel_source_file(n) is not None, f"{stage}: {n} is not defined in csrc"
+
+
+def _profile(tmp_path, w, layout, hashes, traffic):
+    d = tmp_path / "profiles"
+    d.mkdir(exist_ok=True)
+    lines = [f"    source_sha256[{f}]: {h}" for f, h in hashes.items()]
+    lines += [f"    traffic: {n} | {v:.0f}" for n, v in traffic.items()]
+    (d / f"traffic_gs_step_{w.name}_{layout}.md").write_text("\n".join(lines) + "\n")
+
+
+def _current_hashes():
+    out = {}
+    for f in sorted(os.listdir(bench.CSRC)):
+        with open(os.path.join(bench.CSRC, f), "rb") as fh:
+            out[f] = hashlib.sha256(fh.read()).hexdigest()
+    return out
+
+
+def test_traffic_used_while_sources_match(tmp_path, monkeypatch):
+    w = synth.WORKLOADS["laplace53-d25.6M-P8"]
+    acc = bench.stage_kernels(w)["accumulate"][0]
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    _profile(tmp_path, w, "interleaved", _current_hashes(), {acc: 4.096e9})
+    assert bench.measured_traffic(w, "accumulate") == pytest.approx(4.096e9)
+
+
+def test_traffic_dropped_when_a_dependency_changed(tmp_path, monkeypatch):
+    w = synth.WORKLOADS["laplace53-d25.6M-P8"]
+    acc = bench.stage_kernels(w)["accumulate"][0]
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    # the kernel's own file
+    h = _current_hashes()
+    h[bench.kernel_source_file(acc)] = "0" * 64
+    _profile(tmp_path, w, "interleaved", h, {acc: 4.096e9})
+    assert bench.measured_traffic(w, "accumulate") is None
+    # a shared launcher/header file
+    h = _current_hashes()
+    h["gs_api.hip"] = "0" * 64
+    _profile(tmp_path, w, "interleaved", h, {acc: 4.096e9})
+    assert bench.measured_traffic(w, "accumulate") is None
+    # another kernel's file does not matter
+    h = _current_hashes()
+    h["k_select.hip"] = "0" * 64
+    _profile(tmp_path, w, "interleaved", h, {acc: 4.096e9})
+    assert bench.measured_traffic(w, "accumulate") == pytest.approx(4.096e9)
+
+
+def test_traffic_absent_without_profile_or_kernel_entry(tmp_path, monkeypatch):
+    w = synth.WORKLOADS["laplace53-d25.6M-P8"]
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.measured_traffic(w, "accumulate") is None
+    _profile(tmp_path, w, "interleaved", _current_hashes(), {"k_other": 1.0})
+    assert bench.measured_traffic(w, "accumulate") is None
+
+
+def test_gpu_count_above_one_exits_with_a_message(monkeypatch, capsys):
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--gpus", "2"])
+    with pytest.raises(SystemExit) as e:
+        bench.main()
+    assert e.value.code not in (0, None)
