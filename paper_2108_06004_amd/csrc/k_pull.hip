@@ -643,8 +643,9 @@ PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int6
   }
   pl.tiles_per_row = (int32_t)((c + W - 1) / W);
   pl.T = r * pl.tiles_per_row;
-  // small sketches: split each tile's list into segments so every CU gets work
-  int64_t S = (slots + pl.T - 1) / pl.T;
+  // small sketches: split each tile's list into segments so every CU gets work, at most one
+  // round of workgroups (T * S <= slots: a second round would hold only the leftovers)
+  int64_t S = slots / pl.T;
   const int64_t per_tile = (int64_t)r * d / pl.T;
   if (S > per_tile / 512) S = per_tile / 512;  // keep segments at least 512 entries long
   if (S < 1) S = 1;
