@@ -100,7 +100,10 @@ typedef struct gs_ctx gs_ctx; /* opaque: a copy of the config plus device scratc
  * atomics instead. Setting the environment variable GS_SKETCH_PATH=atomic before the call
  * selects the atomic form for any shape, and GS_SKETCH_PATH=unpacked keeps the gather's
  * lists in their unpacked form (diagnostic overrides; results agree within the table
- * tolerance). */
+ * tolerance). A selection without an estimate vector prunes (estimates only coordinates
+ * with enough heavy cells) when d*r exceeds 2,000,000 and estimates every coordinate
+ * otherwise; GS_SELECT_PATH=pruned or =full fixes that choice (the selected set is the same
+ * either way). */
 gs_status gs_create(const gs_config* cfg, gs_ctx** out);
 
 /* Free the context's scratch (after synchronizing the device). NULL is accepted. */

@@ -199,6 +199,11 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
     const char* path = std::getenv("GS_SKETCH_PATH");
     if (path && std::strcmp(path, "atomic") == 0) x->use_pull = false;
     if (path && std::strcmp(path, "unpacked") == 0) x->plan.off_bits = 0;
+    // GS_SELECT_PATH=pruned prunes every selection without an estimate vector, =full none
+    x->prune_min_cells = gs::kPruneMinCells;
+    const char* sel = std::getenv("GS_SELECT_PATH");
+    if (sel && std::strcmp(sel, "pruned") == 0) x->prune_min_cells = 0;
+    if (sel && std::strcmp(sel, "full") == 0) x->prune_min_cells = INT64_MAX;
   }
   if (x->use_pull) {
     x->list_cap = (int64_t)x->r * x->d + (int64_t)gs::kListGroup * x->plan.T;

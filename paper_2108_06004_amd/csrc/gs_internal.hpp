@@ -32,6 +32,7 @@ struct SelectCtl {
   uint32_t n_stage2;    // keys of the digit-1 bucket b1 staged for the digit-3 pass
 };
 constexpr int kSampleMax = 16384;  // sampled estimates for the pruning bound
+constexpr int64_t kPruneMinCells = 2000000;  // d*r below which the full estimate is faster (measured)
 
 // Geometry of the gather-based sketch: tiles of W columns of one row, all P workers, fp64.
 // The columns of row j are taken in the order of their scaled position t = theta_j * col
@@ -106,6 +107,9 @@ struct gs_ctx {
   int prune_buf_cap = 0;            // LDS candidate buffer entries of the pruned pass
   size_t prune_lds = 0;             // dynamic LDS bytes of the pruned pass
   int64_t emit_blocks = 0;
+  // selections without an estimate vector prune when d*r exceeds this (0: always); below it
+  // the full estimate takes fewer launches than the pruned pass's chain
+  int64_t prune_min_cells = 0;
   // gather-based sketch (used when the plan fits; otherwise fp64 atomics into acc64)
   bool use_pull = false;
   gs::PullPlan plan{};

@@ -1090,10 +1090,11 @@ hipError_t prepare_prune(gs_ctx* x) {
 }
 
 hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, float* est, int32_t* idx) {
-  // With an estimate vector requested every coordinate is estimated (unpruned path).
-  // Otherwise the pruned path runs and the unpruned kernels only act if it raised the
-  // fallback flag.
-  const bool prune = (est == nullptr);
+  // With an estimate vector requested, or a sketch small enough (d*r at most
+  // prune_min_cells) that the full estimate is the cheaper chain, every coordinate is
+  // estimated. Otherwise the pruned path runs and the full estimate only acts if the pruned
+  // candidates fell short of k.
+  const bool prune = est == nullptr && x->d * x->r > x->prune_min_cells;
   SelectCtl* gate = prune ? x->ctl : nullptr;
   switch (x->r) {
 #define GS_R_CASE(RR) \
@@ -1128,9 +1129,9 @@ hipError_t launch_heavymix_topk(gs_ctx* x, hipStream_t s, const float* merged, i
     first = false;
   }
   hipLaunchKernelGGL(k_theta, dim3(1), dim3(64), 0, s, in, x->r, k, x->ctl);
-  // With an estimate vector requested every coordinate is estimated; otherwise the pruned
-  // pass runs and the full one only acts if the pruned candidates fell short of k.
-  const bool prune = (est == nullptr);
+  // As in launch_unsketch_topk: the full estimate with an estimate vector or a small sketch,
+  // else the pruned pass, with the full one acting only if its candidates fell short of k.
+  const bool prune = est == nullptr && x->d * x->r > x->prune_min_cells;
   switch (x->r) {
 #define GS_R_CASE(RR)                                                                                              \
   case RR:                                                                                                         \

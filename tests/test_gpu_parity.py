@@ -375,6 +375,24 @@ def test_atomic_sketch_path(monkeypatch, d, P, r, c, k):
     dv.close()
 
 
+@pytest.mark.parametrize("mode", ["auto", "full"])
+@pytest.mark.parametrize("name", ["t3planted-d65536-P4", "laplace20-d270000-P4"])
+def test_selection_path_by_size(monkeypatch, name, mode):
+    # small sketches (d*r at most 2,000,000) select through the full estimate unless told
+    # otherwise; the fused step's selection must still equal the oracle's top-k
+    if mode == "auto":
+        monkeypatch.delenv("GS_SELECT_PATH", raising=False)
+    else:
+        monkeypatch.setenv("GS_SELECT_PATH", mode)
+    w = synth.WORKLOADS[name]
+    hp = synth.hash_params(w)
+    dv = Dev(w.d, w.P, w.r, w.c, w.k, hp, w.rho)
+    g = synth.gradients(w, 0)
+    z = np.zeros_like(g)
+    chain_check(dv, g, z, z.copy(), w.k, w.rho, label=f"selection path {mode} {name}")
+    dv.close()
+
+
 @pytest.mark.parametrize("d,P,r,c,k", [(65_536, 8, 5, 4096, 655), (10_007, 3, 5, 211, 300), (5_003, 12, 5, 300, 50),
                                        (100_003, 1, 5, 2_000_003, 50)])
 def test_unpacked_lists(monkeypatch, d, P, r, c, k):
