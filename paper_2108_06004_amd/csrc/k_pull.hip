@@ -647,7 +647,10 @@ PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int6
   // round of workgroups (T * S <= slots: a second round would hold only the leftovers)
   int64_t S = slots / pl.T;
   const int64_t per_tile = (int64_t)r * d / pl.T;
-  if (S > per_tile / 512) S = per_tile / 512;  // keep segments at least 512 entries long
+  // every segment's workgroup zeroes and writes out a whole fp64 tile however short its list,
+  // so segments stay long: at least 16 Ki entries (measured best over 0.5 .. 64 Ki at
+  // d = 65,536 and 270,000)
+  if (S > per_tile / 16384) S = per_tile / 16384;
   if (S < 1) S = 1;
   pl.S = (int32_t)S;
   // build chunks: 64 Ki coordinates each
