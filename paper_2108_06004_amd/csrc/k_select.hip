@@ -642,22 +642,44 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
 #pragma unroll
     for (int m = 0; m < U; ++m) {
       cnt[m] = 0u;
+      if constexpr (MAP == kMapCoarse) {
+        // a coarse bit covers its cells' heavy bits, so a coordinate with fewer than `need`
+        // coarse-set rows is out without a global read; the others confirm their set rows in
+        // the fine map (global reads, the cost here: L2 requests) while `need` is in reach
+        Cell ev[R];
+        uint32_t cset = 0u, nset = 0u;
 #pragma unroll
-      for (int j = 0; j < R; ++j) {
-        const uint32_t col = mod_c(hb[j][m], kr[j].c, kr[j].magic, kr[j].shift);
-        hb[j][m] = add_mod_mersenne(hb[j][m], db[j]);
-        const Cell e = (Cell)j * kr[j].c + col;
-        if constexpr (MAP == kMapFine) {
-          cnt[m] += (sm[e >> 5] >> (e & 31)) & 1u;
-        } else {
-          // global reads are the cost here (L2 requests): skip a row once the coordinate
-          // cannot reach `need` with the rows left, which leaves the keep decision unchanged
-          const bool alive = cnt[m] + (uint32_t)(R - j) >= (uint32_t)need;
-          if constexpr (MAP == kMapCoarse) {
-            const uint32_t cb = e >> coarse_log2;
-            if (alive && ((sm[cb >> 5] >> (cb & 31)) & 1u)) cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
+        for (int j = 0; j < R; ++j) {
+          const uint32_t col = mod_c(hb[j][m], kr[j].c, kr[j].magic, kr[j].shift);
+          hb[j][m] = add_mod_mersenne(hb[j][m], db[j]);
+          ev[j] = (Cell)j * kr[j].c + col;
+          const uint32_t cb = ev[j] >> coarse_log2;
+          const uint32_t bit = (sm[cb >> 5] >> (cb & 31)) & 1u;
+          cset |= bit << j;
+          nset += bit;
+        }
+        if (nset >= (uint32_t)need) {
+          uint32_t left = nset;  // coarse-set rows not yet confirmed, this one included
+#pragma unroll
+          for (int j = 0; j < R; ++j) {
+            if ((cset >> j) & 1u) {
+              if (cnt[m] + left >= (uint32_t)need) cnt[m] += (heavy[ev[j] >> 5] >> (ev[j] & 31)) & 1u;
+              --left;
+            }
+          }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+          const uint32_t col = mod_c(hb[j][m], kr[j].c, kr[j].magic, kr[j].shift);
+          hb[j][m] = add_mod_mersenne(hb[j][m], db[j]);
+          const Cell e = (Cell)j * kr[j].c + col;
+          if constexpr (MAP == kMapFine) {
+            cnt[m] += (sm[e >> 5] >> (e & 31)) & 1u;
           } else {
-            if (alive) cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
+            // global reads are the cost here (L2 requests): skip a row once the coordinate
+            // cannot reach `need` with the rows left, which leaves the keep decision unchanged
+            if (cnt[m] + (uint32_t)(R - j) >= (uint32_t)need) cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
           }
         }
       }
