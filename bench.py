@@ -82,7 +82,7 @@ def kernel_source_file(name: str):
 
 def stage_kernels(w, layout: str = "interleaved") -> dict:
     """The kernels each stage of the fused step launches (names as rocprofv3 reports them)."""
-    acc = [f"k_accumulate_il<{w.P // 4}>"] if layout == "interleaved" else [f"k_accumulate_vi<{w.P}>"]
+    acc = [f"k_accumulate_il<{w.P // 4}>"] if layout == "interleaved" else [f"k_vi_il<{w.P}, true>"]
     return {
         "accumulate": acc,
         "sketch": [f"k_pull<{w.P}, {4 if w.P <= 4 else 6}, true>"],  # packed lists (the library's choice here)

@@ -15,6 +15,8 @@
 //      worker's table value) and merges the workers in the binomial-tree order.
 // All tiles walk their lists in ascending coordinate order at similar rates, so at any
 // moment the gathers of all tiles fall in a narrow band of vI that stays in cache.
+#include <type_traits>
+
 #include "gs_internal.hpp"
 
 namespace gs {
@@ -196,80 +198,91 @@ __global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int6
 // Per step: accumulation that also writes the worker-interleaved copy of v.
 // One lane handles 4 consecutive coordinates of every worker (float4 per worker row).
 
-// Rows 4t .. 4t+3 of vI from the P workers' values vv[q][m] of coordinate 4t + m.
-template <int P>
-__device__ __forceinline__ void write_vi_rows(float* __restrict__ vI, int64_t t, const float (&vv)[P][4]) {
+// Worker-major arrays ([P][d]) into the interleaved copy vI ([d][PP] rows, PP = P rounded up
+// to 4), with (ACC) or without the accumulation of u and v on the way. A wave covers CW =
+// 64/G consecutive coordinates, G = PP/4 16-byte pieces per row: lane l takes coordinate
+// l/G and piece h = l%G (workers 4h .. 4h+3). So the worker-major loads and stores are 4
+// bytes per lane and 4*CW contiguous bytes per worker row and instruction, and the vI
+// stores 16 bytes per lane, 16*CW*G contiguous bytes per instruction. Each pass a wave takes
+// U consecutive chunks, all in flight together. Workers past P read nothing and write 0 into
+// vI. Full chunks only; the tail goes to k_accumulate_vi_any.
+template <int P, bool ACC>
+__global__ void __launch_bounds__(kBlock) k_vi_il(const float* __restrict__ g, float* __restrict__ u,
+                                                  float* __restrict__ v, float* __restrict__ vI, int64_t d,
+                                                  float rho) {
   constexpr int PP = (P + 3) & ~3;
-  f4* dst = reinterpret_cast<f4*>(vI + (4 * t) * PP);
+  constexpr int G = PP / 4;
+  constexpr int CW = 64 / G;
+  constexpr int U = 4;
+  const int lane = threadIdx.x & 63;
+  if (lane >= CW * G) return;  // G = 3: one idle lane per wave (no barrier below)
+  const int h = lane % G;
+  const int64_t sub = lane / G;
+  const int64_t nch = d / CW;
+  const int64_t ngr = nch / U;
+  const int64_t wstride = (int64_t)gridDim.x * (kBlock / 64);
+  const int64_t w0 = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  // one pass over n consecutive chunks starting at chunk c0
+  auto pass = [&](int64_t c0, auto n_const) {
+    constexpr int N = decltype(n_const)::value;
+    float x[N][4], uu[N][4], gg[N][4];
 #pragma unroll
-  for (int m = 0; m < 4; ++m) {
+    for (int m = 0; m < N; ++m) {
+      const int64_t i = (c0 + m) * CW + sub;
 #pragma unroll
-    for (int q0 = 0; q0 < PP; q0 += 4) {
-      f4 x;
-      x.x = q0 + 0 < P ? vv[q0 + 0 < P ? q0 + 0 : 0][m] : 0.f;
-      x.y = q0 + 1 < P ? vv[q0 + 1 < P ? q0 + 1 : 0][m] : 0.f;
-      x.z = q0 + 2 < P ? vv[q0 + 2 < P ? q0 + 2 : 0][m] : 0.f;
-      x.w = q0 + 3 < P ? vv[q0 + 3 < P ? q0 + 3 : 0][m] : 0.f;
-      dst[(m * PP + q0) / 4] = x;
+      for (int q = 0; q < 4; ++q) {
+        const int w = 4 * h + q;
+        x[m][q] = 0.f;
+        uu[m][q] = 0.f;
+        gg[m][q] = 0.f;
+        if (w < P) {
+          const int64_t o = (int64_t)w * d + i;
+          if constexpr (ACC) {
+            gg[m][q] = __builtin_nontemporal_load(g + o);
+            uu[m][q] = __builtin_nontemporal_load(u + o);
+          }
+          x[m][q] = __builtin_nontemporal_load(v + o);
+        }
+      }
     }
-  }
-}
-
-template <int P>
-__global__ void __launch_bounds__(kBlock) k_accumulate_vi(const float* __restrict__ g, float* __restrict__ u,
-                                                          float* __restrict__ v, float* __restrict__ vI, int64_t d,
-                                                          float rho) {
-  const int64_t n4 = d / 4;
-  const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n4; t += stride) {
-    float vv[P][4];
 #pragma unroll
-    for (int q = 0; q < P; ++q) {
-      const int64_t o = q * n4 + t;
-      const f4 gg = __builtin_nontemporal_load(reinterpret_cast<const f4*>(g) + o);
-      f4 uu = __builtin_nontemporal_load(reinterpret_cast<const f4*>(u) + o);
-      f4 w = __builtin_nontemporal_load(reinterpret_cast<const f4*>(v) + o);
-      uu = rho * uu + gg;
-      w = w + uu;
-      __builtin_nontemporal_store(uu, reinterpret_cast<f4*>(u) + o);
-      __builtin_nontemporal_store(w, reinterpret_cast<f4*>(v) + o);
-      vv[q][0] = w.x;
-      vv[q][1] = w.y;
-      vv[q][2] = w.z;
-      vv[q][3] = w.w;
-    }
-    write_vi_rows<P>(vI, t, vv);
-  }
-}
-
-// Interleave only (the sketch of a given [P][d] array, e.g. the gradients).
-template <int P>
-__global__ void __launch_bounds__(kBlock) k_interleave4(const float* __restrict__ src, float* __restrict__ vI,
-                                                        int64_t d) {
-  const int64_t n4 = d / 4;
-  const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n4; t += stride) {
-    float vv[P][4];
+    for (int m = 0; m < N; ++m) {
+      const int64_t i = (c0 + m) * CW + sub;
 #pragma unroll
-    for (int q = 0; q < P; ++q) {
-      const f4 w = __builtin_nontemporal_load(reinterpret_cast<const f4*>(src) + q * n4 + t);
-      vv[q][0] = w.x;
-      vv[q][1] = w.y;
-      vv[q][2] = w.z;
-      vv[q][3] = w.w;
+      for (int q = 0; q < 4; ++q) {
+        const int w = 4 * h + q;
+        if (ACC && w < P) {
+          const int64_t o = (int64_t)w * d + i;
+          uu[m][q] = rho * uu[m][q] + gg[m][q];
+          x[m][q] = x[m][q] + uu[m][q];
+          __builtin_nontemporal_store(uu[m][q], u + o);
+          __builtin_nontemporal_store(x[m][q], v + o);
+        }
+      }
+      f4 row;
+      row.x = x[m][0];
+      row.y = x[m][1];
+      row.z = x[m][2];
+      row.w = x[m][3];
+      reinterpret_cast<f4*>(vI + i * PP)[h] = row;
     }
-    write_vi_rows<P>(vI, t, vv);
-  }
+  };
+  for (int64_t gr = w0; gr < ngr; gr += wstride) pass(gr * U, std::integral_constant<int, U>());
+  for (int64_t ch = ngr * U + w0; ch < nch; ch += wstride) pass(ch, std::integral_constant<int, 1>());
 }
 
 // Generic (any P, any d, any alignment): one lane per (coordinate, worker).
+// Coordinates from i_lo on.
 __global__ void __launch_bounds__(kBlock) k_accumulate_vi_any(const float* __restrict__ g, float* __restrict__ u,
                                                               float* __restrict__ v, float* __restrict__ vI,
-                                                              int64_t d, int P, int PP, float rho, int do_acc) {
-  const int64_t n = (int64_t)P * d;
+                                                              int64_t d, int P, int PP, float rho, int do_acc,
+                                                              int64_t i_lo) {
+  const int64_t dt = d - i_lo;
+  const int64_t n = (int64_t)P * dt;
   const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t e = (int64_t)blockIdx.x * kBlock + threadIdx.x; e < n; e += stride) {
-    const int64_t q = e / d, i = e - q * d;
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n; t += stride) {
+    const int64_t q = t / dt, i = i_lo + (t - q * dt);
+    const int64_t e = q * d + i;
     float w;
     if (do_acc) {
       const float un = rho * u[e] + g[e];
@@ -514,12 +527,21 @@ __global__ void __launch_bounds__(kBlock) k_merge_partials_any(const double* __r
   }
 }
 
-template <int P>
-hipError_t launch_acc_vi_p(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v) {
-  const int64_t n4 = x->d / 4;
-  // about one pass per lane: the most loads in flight (measured best on the 25.6M x 8 stream)
-  hipLaunchKernelGGL(k_accumulate_vi<P>, dim3(grid_for(n4, kBlock, 64 * x->num_cus)), dim3(kBlock), 0, s, g, u, v,
-                     x->vI, x->d, x->rho);
+// k_vi_il over the full chunks, then k_accumulate_vi_any for the rest; g and u only with ACC.
+template <int P, bool ACC>
+hipError_t launch_vi_il_p(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v) {
+  constexpr int CW = 64 / (((P + 3) & ~3) / 4);
+  const int64_t nch = x->d / CW;
+  if (nch > 0) {
+    const dim3 grid(grid_for(nch, 4 * (kBlock / 64), 64 * x->num_cus)), block(kBlock);
+    hipLaunchKernelGGL((k_vi_il<P, ACC>), grid, block, 0, s, g, u, v, x->vI, x->d, x->rho);
+  }
+  const int64_t done = nch * CW;
+  if (done < x->d) {
+    const int64_t n = (int64_t)P * (x->d - done);
+    hipLaunchKernelGGL(k_accumulate_vi_any, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, g, u, v,
+                       x->vI, x->d, P, x->plan.PP, x->rho, ACC ? 1 : 0, done);
+  }
   return hipGetLastError();
 }
 
@@ -726,41 +748,35 @@ hipError_t build_pull_lists(gs_ctx* x) {
 }
 
 hipError_t launch_accumulate_vi(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v) {
-  const bool fast = (x->d % 4 == 0) && ((uintptr_t)g % 16 == 0) && ((uintptr_t)u % 16 == 0) &&
-                    ((uintptr_t)v % 16 == 0) && x->P <= 16;
-  if (fast) {
-    switch (x->P) {
+  switch (x->P) {
 #define GS_ACCVI_CASE(PP) \
-  case PP: return launch_acc_vi_p<PP>(x, s, g, u, v);
-      GS_ACCVI_CASE(1) GS_ACCVI_CASE(2) GS_ACCVI_CASE(3) GS_ACCVI_CASE(4) GS_ACCVI_CASE(5) GS_ACCVI_CASE(6)
-      GS_ACCVI_CASE(7) GS_ACCVI_CASE(8) GS_ACCVI_CASE(9) GS_ACCVI_CASE(10) GS_ACCVI_CASE(11) GS_ACCVI_CASE(12)
-      GS_ACCVI_CASE(13) GS_ACCVI_CASE(14) GS_ACCVI_CASE(15) GS_ACCVI_CASE(16)
+  case PP: return launch_vi_il_p<PP, true>(x, s, g, u, v);
+    GS_ACCVI_CASE(1) GS_ACCVI_CASE(2) GS_ACCVI_CASE(3) GS_ACCVI_CASE(4) GS_ACCVI_CASE(5) GS_ACCVI_CASE(6)
+    GS_ACCVI_CASE(7) GS_ACCVI_CASE(8) GS_ACCVI_CASE(9) GS_ACCVI_CASE(10) GS_ACCVI_CASE(11) GS_ACCVI_CASE(12)
+    GS_ACCVI_CASE(13) GS_ACCVI_CASE(14) GS_ACCVI_CASE(15) GS_ACCVI_CASE(16)
 #undef GS_ACCVI_CASE
-      default: break;
-    }
+    default: break;
   }
   const int64_t n = (int64_t)x->P * x->d;
   hipLaunchKernelGGL(k_accumulate_vi_any, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, g, u, v,
-                     x->vI, x->d, x->P, x->plan.PP, x->rho, 1);
+                     x->vI, x->d, x->P, x->plan.PP, x->rho, 1, (int64_t)0);
   return hipGetLastError();
 }
 
 hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v) {
-  if ((x->d % 4 == 0) && ((uintptr_t)v % 16 == 0) && x->P <= 16) {
-    const dim3 grid(grid_for(x->d / 4, kBlock, 64 * x->num_cus)), block(kBlock);
-    switch (x->P) {
+  float* src = const_cast<float*>(v);  // read only (no accumulation)
+  switch (x->P) {
 #define GS_IL_CASE(PP) \
-  case PP: hipLaunchKernelGGL(k_interleave4<PP>, grid, block, 0, s, v, x->vI, x->d); return hipGetLastError();
-      GS_IL_CASE(1) GS_IL_CASE(2) GS_IL_CASE(3) GS_IL_CASE(4) GS_IL_CASE(5) GS_IL_CASE(6) GS_IL_CASE(7) GS_IL_CASE(8)
-      GS_IL_CASE(9) GS_IL_CASE(10) GS_IL_CASE(11) GS_IL_CASE(12) GS_IL_CASE(13) GS_IL_CASE(14) GS_IL_CASE(15)
-      GS_IL_CASE(16)
+  case PP: return launch_vi_il_p<PP, false>(x, s, nullptr, nullptr, src);
+    GS_IL_CASE(1) GS_IL_CASE(2) GS_IL_CASE(3) GS_IL_CASE(4) GS_IL_CASE(5) GS_IL_CASE(6) GS_IL_CASE(7) GS_IL_CASE(8)
+    GS_IL_CASE(9) GS_IL_CASE(10) GS_IL_CASE(11) GS_IL_CASE(12) GS_IL_CASE(13) GS_IL_CASE(14) GS_IL_CASE(15)
+    GS_IL_CASE(16)
 #undef GS_IL_CASE
-      default: break;
-    }
+    default: break;
   }
   const int64_t n = (int64_t)x->P * x->d;
   hipLaunchKernelGGL(k_accumulate_vi_any, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, nullptr,
-                     nullptr, const_cast<float*>(v), x->vI, x->d, x->P, x->plan.PP, x->rho, 0);
+                     nullptr, src, x->vI, x->d, x->P, x->plan.PP, x->rho, 0, (int64_t)0);
   return hipGetLastError();
 }
 
