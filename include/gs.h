@@ -26,6 +26,9 @@
  *   - Calls on one context must not overlap on different streams: the context's scratch
  *     memory (histograms, candidate lists, bitmaps, internal tables) is shared by them.
  *     Different contexts are independent.
+ *   - Only gs_create allocates. The per-step calls (everything but gs_create, gs_destroy,
+ *     gs_step_profiled and gs_timing_*) neither allocate, synchronize nor clear memory with
+ *     a memset, so they can be captured in a HIP graph and replayed.
  *   - Inputs must be finite; results for NaN or infinite inputs are unspecified.
  */
 #ifndef GS_H
