@@ -342,6 +342,16 @@ __device__ __forceinline__ void decode_entry(uint32_t w, uint32_t aux, int off_b
   }
 }
 
+// Segment s of the S segments of a tile's list [lo, lo + n): inner boundaries are rounded
+// down to multiples of kListGroup entries from lo, which is itself such a multiple, so a
+// segment never splits a group of the packed list.
+__device__ __forceinline__ void segment_bounds(int64_t lo, int64_t n, int64_t s, int64_t S, int64_t& e0,
+                                               int64_t& e1) {
+  constexpr int64_t g = kListGroup;
+  e0 = lo + (n * s / S) / g * g;
+  e1 = s + 1 == S ? lo + n : lo + (n * (s + 1) / S) / g * g;
+}
+
 template <int P, int U, bool PK>
 __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
                                                      const uint16_t* __restrict__ codes,
@@ -369,8 +379,8 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - kt * pl.W);
   for (int64_t e = threadIdx.x; e < wt * P; e += kPullBlock) acc[e] = 0.0;
   __syncthreads();
-  const int64_t lo = off[t], n = tn[t];
-  const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
+  int64_t e0, e1;
+  segment_bounds(off[t], tn[t], s, pl.S, e0, e1);
   double* const mycol = acc + (int64_t)(4 * sub) * wt;
   // when L does not divide the block (L = 3: 85 groups of 3 lanes), the last lane has no
   // group: it takes no entry (its would be the next pass's first)
@@ -381,7 +391,16 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
     for (int m = 0; m < U; ++m) {
       const int64_t e = eb + m * B;
       const uint32_t w = list[e];
-      const uint32_t aux = PK ? bases[e / kListGroup] : (uint32_t)codes[e];
+      uint32_t aux;
+      if constexpr (PK && (L == 1 || L == 2 || L == 4)) {
+        // e0 is group-aligned, B is a multiple of kListGroup and a wave's lanes take 64 / L
+        // consecutive entries of an aligned run (permuted within it): every lane active in
+        // this pass needs the same group base, so the wave loads it once, as a scalar. The
+        // tail loop below cannot do this (its lanes may be one pass apart).
+        aux = bases[__builtin_amdgcn_readfirstlane((uint32_t)(e / kListGroup))];
+      } else {
+        aux = PK ? bases[e / kListGroup] : (uint32_t)codes[e];
+      }
       decode_entry<PK>(w, aux, pl.off_bits, i[m], pos[m], sg[m]);
     }
     f4 x[U];
@@ -451,8 +470,8 @@ __global__ void __launch_bounds__(kBlock) k_pull_any(HashSet hs, PullPlan pl, co
   const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - kt * pl.W);
   for (int64_t e = threadIdx.x; e < wt * P; e += kBlock) acc[e] = 0.0;
   __syncthreads();
-  const int64_t lo = off[t], n = tn[t];
-  const int64_t e0 = lo + n * s / pl.S, e1 = lo + n * (s + 1) / pl.S;
+  int64_t e0, e1;
+  segment_bounds(off[t], tn[t], s, pl.S, e0, e1);
   for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
     const uint32_t i = list[e], code = codes[e];
     double* cell = acc + (code & 0x7fffu);
