@@ -106,7 +106,11 @@ typedef struct gs_ctx gs_ctx; /* opaque: a copy of the config plus device scratc
  * tolerance). A selection without an estimate vector prunes (estimates only coordinates
  * with enough heavy cells) when d*r exceeds 2,000,000 and estimates every coordinate
  * otherwise; GS_SELECT_PATH=pruned or =full fixes that choice (the selected set is the same
- * either way). */
+ * either way).
+ * Device scratch is about (16 + 4 PP + 4.1 r) d + 8 S P r c bytes (PP = P rounded up to 4; S
+ * list segments per tile, 1 unless the sketch is small), plus 2 r d bytes while the lists are
+ * built: 1.8 GB at d = 25.6M, P = 8, r = 5, c = 256,000 and 95 GB at d = 2^31 - 2, P = 2,
+ * r = 3. The atomic form replaces the lists and the interleaved copy with 8 P r c bytes. */
 gs_status gs_create(const gs_config* cfg, gs_ctx** out);
 
 /* Free the context's scratch (after synchronizing the device). NULL is accepted. */
