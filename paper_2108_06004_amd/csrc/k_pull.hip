@@ -393,6 +393,7 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
       const uint32_t w = list[e];
       uint32_t aux;
       if constexpr (PK && (L == 1 || L == 2 || L == 4)) {
+        static_assert(B % kListGroup == 0 && kListGroup % (64 / L) == 0, "a wave's entries must share a group");
         // e0 is group-aligned, B is a multiple of kListGroup and a wave's lanes take 64 / L
         // consecutive entries of an aligned run (permuted within it): every lane active in
         // this pass needs the same group base, so the wave loads it once, as a scalar. The
