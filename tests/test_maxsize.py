@@ -1,4 +1,5 @@
-"""The largest coordinate count the bucket hash admits, d = 2^31 - 2, through every entry point.
+"""The largest coordinate count the bucket hash admits, d = 2^31 - 2, through every entry point
+(HEAVYMIX included).
 
 At this size P*d (worker-major state), 4*d (interleaved rows) and r*d (the tile lists) all
 exceed 2^32, so every flat index on the path is past 32 bits. The input is zero except 16
@@ -74,6 +75,38 @@ def expected(hp: dict) -> dict:
                 u_acc=u_acc, v_acc=v_acc, u_end=u, v_end=v)
 
 
+# HEAVYMIX draws: zero except at these coordinates (the top of the range among them). The
+# draws are multiples of 2^20, so the fill keys (draw >> 1) are exact as fp32 values and the
+# oracle's magnitude top-k ranks them.
+DRAWN = np.array([5, 2**30 + 5, 10**9 + 1, 2**31 - 7, D_MAX - 4, D_MAX - 3, 63, 2**30, D_MAX - 65, D_MAX - 1,
+                  3 * 2**29, 77_777_777], dtype=np.int64)
+
+
+def expected_heavymix(exp: dict) -> dict:
+    """HEAVYMIX (Alg. 2) on the same merged sketch: the heavy set, the fill and the step's
+    values and reset, from the oracle at the coordinates that can matter."""
+    l2 = oracle.l2sq_estimate(exp["merged"])
+    nh = oracle.heavy_count(exp["est"], K_SEL, l2)  # zero estimates are never heavy (l2 > 0)
+    assert 0 < nh < K_SEL
+    hpos, _ = oracle.topk(exp["est"], nh)  # est^2 >= l2/k is monotone in |est|: the nh largest
+    heavy = exp["cand"][hpos]
+    order = np.argsort(DRAWN)
+    drawn = DRAWN[order]
+    draws = ((np.arange(DRAWN.size, dtype=np.uint32)[order] + 1) << 20).astype(np.uint32)
+    light = ~np.isin(drawn, heavy)
+    assert light.sum() > K_SEL - nh, "the fill must come from nonzero draws"
+    fpos, _ = oracle.topk((draws[light] >> 1).astype(np.float32), K_SEL - nh)
+    idx = np.sort(np.concatenate([heavy, drawn[light][fpos]])).astype(np.int32)
+    coords = np.union1d(exp["cand"], DRAWN)
+    g = np.zeros((P, coords.size), np.float32)
+    g[:, np.searchsorted(coords, PLANTED)] = exp["gp"]
+    u, v = np.zeros_like(g), np.zeros_like(g)
+    oracle.accumulate(g, u, v, RHO)
+    values = oracle.gather_reset(np.searchsorted(coords, idx), u, v)
+    return dict(l2sq=l2, n_heavy=nh, drawn=drawn, draws=draws, idx=idx, coords=coords, values=values, u_end=u,
+                v_end=v)
+
+
 def test_sharing_matches_brute_force():
     # the preimage listing against every coordinate's bucket, on a size where all fit
     d, c = 2_000_003, 16_384
@@ -97,6 +130,9 @@ def test_maximum_d_expectation_is_consistent():
     assert np.count_nonzero(exp["est"]) >= K_SEL
     assert exp["cand"].size > PLANTED.size
     assert exp["idx"].dtype == np.int32 and exp["idx"][-1] == D_MAX - 1
+    hm = expected_heavymix(exp)
+    assert hm["idx"].size == K_SEL and np.unique(hm["idx"]).size == K_SEL
+    assert np.isin(D_MAX - 3, hm["idx"]) and np.isin(D_MAX - 1, hm["idx"])  # a fill and a heavy one at the top
 
 
 @pytest.mark.gpu
@@ -114,9 +150,9 @@ def test_maximum_d_every_entry_point(layout):
     cand_t = torch.from_numpy(exp["cand"]).to(dev)
     f32 = dict(dtype=torch.float32, device=dev)
 
-    def state_at(t):
-        """[P][len(cand)] host copy of a state tensor at the candidate coordinates."""
-        x = t[:, cand_t] if layout == "worker_major" else t[cand_t, :P].t()
+    def state_at(t, at):
+        """[P][len(at)] host copy of a state tensor at the coordinates `at`."""
+        x = t[:, at] if layout == "worker_major" else t[at, :P].t()
         return x.cpu().numpy()
 
     def nnz(t):
@@ -125,10 +161,10 @@ def test_maximum_d_every_entry_point(layout):
         flat = t.view(-1)
         return sum(int(torch.count_nonzero(flat[o:o + (1 << 28)]).item()) for o in range(0, flat.numel(), 1 << 28))
 
-    def check_state(u, v, u_ref, v_ref, what):
+    def check_state(u, v, u_ref, v_ref, what, at=cand_t):
         torch.cuda.synchronize()
-        assert np.array_equal(state_at(u), u_ref), f"{what}: u at the candidate coordinates"
-        assert np.array_equal(state_at(v), v_ref), f"{what}: v at the candidate coordinates"
+        assert np.array_equal(state_at(u, at), u_ref), f"{what}: u at the candidate coordinates"
+        assert np.array_equal(state_at(v, at), v_ref), f"{what}: v at the candidate coordinates"
         # every other coordinate (and the interleaved padding) holds exactly zero
         assert nnz(u) == np.count_nonzero(u_ref), f"{what}: u nonzero elsewhere"
         assert nnz(v) == np.count_nonzero(v_ref), f"{what}: v nonzero elsewhere"
@@ -187,6 +223,38 @@ def test_maximum_d_every_entry_point(layout):
     assert np.array_equal(idx.cpu().numpy(), exp["idx"]), "fused step: top-k"
     assert np.array_equal(values.cpu().numpy(), exp["values"]), "fused step: gathered values"
     check_state(u, v, exp["u_end"], exp["v_end"], "fused step")
+
+    say("heavymix_topk with the estimate vector (every coordinate estimated)")
+    hm = expected_heavymix(exp)
+    rnd = torch.zeros(D_MAX, dtype=torch.int32, device=dev)
+    rnd[torch.from_numpy(hm["drawn"]).to(dev)] = torch.from_numpy(hm["draws"].view(np.int32)).to(dev)
+    est = torch.empty(D_MAX, **f32)
+    nh = torch.zeros(1, dtype=torch.int64, device=dev)
+    l2 = torch.zeros(1, dtype=torch.float64, device=dev)
+    ctx.heavymix_topk(torch.from_numpy(exp["merged"]).to(dev), K_SEL, rnd, idx, est=est, n_heavy=nh, l2sq=l2)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), hm["idx"]), "HEAVYMIX selection from the full estimate"
+    assert nh.item() == hm["n_heavy"], "|H|"
+    assert l2.item() == hm["l2sq"], "l2-norm-squared estimate"
+    assert np.array_equal(est[cand_t].cpu().numpy(), exp["est"]), "HEAVYMIX estimates at the candidates"
+    assert nnz(est) == np.count_nonzero(exp["est"]), "HEAVYMIX: nonzero estimates elsewhere"
+    del est
+
+    say("fused HEAVYMIX step from zero state (pruned selection)")
+    u.zero_()
+    v.zero_()
+    merged.fill_(7.0)
+    idx.fill_(-1)
+    values.fill_(7.0)
+    nh.zero_()
+    ctx.step_heavymix(g, u, v, K_SEL, rnd, merged, idx, values, n_heavy=nh)
+    torch.cuda.synchronize()
+    assert np.array_equal(merged.cpu().numpy(), exp["merged"]), "fused HEAVYMIX step: merged sketch"
+    assert np.array_equal(idx.cpu().numpy(), hm["idx"]), "fused HEAVYMIX step: selection"
+    assert nh.item() == hm["n_heavy"], "fused HEAVYMIX step: |H|"
+    assert np.array_equal(values.cpu().numpy(), hm["values"]), "fused HEAVYMIX step: gathered values"
+    check_state(u, v, hm["u_end"], hm["v_end"], "fused HEAVYMIX step", at=torch.from_numpy(hm["coords"]).to(dev))
+    del rnd
     say("done")
     ctx.close()
     del g, u, v
