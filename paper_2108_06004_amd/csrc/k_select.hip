@@ -637,6 +637,13 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
       hb[j][m] = mod_mersenne_affine(kr[j].a, kr[j].b, (uint32_t)(base0 + threadIdx.x + (int64_t)m * kPruneBlock));
   }
   for (int64_t base = base0; base < d; base += stride) {  // block-uniform
+    // HEAVYMIX: the draws are loaded first, so their memory latency overlaps the lookups
+    uint32_t fill[U];
+#pragma unroll
+    for (int m = 0; m < U; ++m) {
+      const int64_t i = base + threadIdx.x + (int64_t)m * kPruneBlock;
+      fill[m] = HM && i < d ? rnd[i] >> 1 : 0u;
+    }
     // all U * R lookups first (independent), then the appends
     uint32_t cnt[U];
 #pragma unroll
@@ -692,7 +699,7 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
     for (int m = 0; m < U; ++m) {
       const int64_t i = base + threadIdx.x + (int64_t)m * kPruneBlock;
       bool keep = i < d && cnt[m] >= (uint32_t)need;
-      if constexpr (HM) keep = keep || (i < d && (rnd[i] >> 1) >= tau0);
+      if constexpr (HM) keep = keep || (i < d && fill[m] >= tau0);
       if (keep) {
         const uint32_t pos = atomicAdd(&bn, 1u);
         if (pos < (uint32_t)buf_cap) {
