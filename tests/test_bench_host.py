@@ -89,3 +89,12 @@ def test_gpu_count_above_one_exits_with_a_message(monkeypatch, capsys):
     with pytest.raises(SystemExit) as e:
         bench.main()
     assert e.value.code not in (0, None)
+
+
+def test_cpu_baseline_runs_whole_steps_within_its_bounds():
+    # consecutive oracle steps until the minimum time has passed; the rate counts every step
+    w = synth.WORKLOADS["t3planted-d65536-P4"]
+    r = bench.cpu_baseline(w, synth.gradients(w, 0), budget_s=5.0, min_s=0.2)
+    assert r["kind"] == "oracle" and r["cores"] == 1 and r["steps"] >= 1
+    assert 0.2 <= r["seconds"] <= 5.0
+    assert r["value"] == pytest.approx(r["steps"] * w.P * w.d / r["seconds"], rel=1e-2)
