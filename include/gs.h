@@ -26,9 +26,10 @@
  *   - Calls on one context must not overlap on different streams: the context's scratch
  *     memory (histograms, candidate lists, bitmaps, internal tables) is shared by them.
  *     Different contexts are independent.
- *   - Only gs_create allocates. The per-step calls (everything but gs_create, gs_destroy,
- *     gs_step_profiled and gs_timing_*) neither allocate, synchronize nor clear memory with
- *     a memset, so they can be captured in a HIP graph and replayed.
+ *   - Only gs_create allocates (gs_unsketch_topk_static uses a fixed array instead). The
+ *     per-step calls (everything but gs_create, gs_destroy, gs_step_profiled and
+ *     gs_timing_*) neither allocate, synchronize nor clear memory with a memset, so they
+ *     can be captured in a HIP graph and replayed.
  *   - Inputs must be finite; results for NaN or infinite inputs are unspecified.
  */
 #ifndef GS_H
@@ -227,11 +228,34 @@ gs_status gs_step_profiled(gs_ctx* ctx, void* stream, const float* g, float* u, 
 gs_status gs_timing_start(gs_ctx* ctx, int32_t max_steps);
 gs_status gs_timing_stop(gs_ctx* ctx, float* stage_ms, int32_t* n_steps);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): gs_unsketch_topk without a context.
+ * Same results as gs_unsketch_topk on a context with the same d, r, c and hash parameters
+ * (it runs that call's kernels with every coordinate estimated): est (when non-NULL) the
+ * median estimates, idx the k largest |estimate|, ties to the lower index, ascending.
+ *   cfg     host pointer; d, r, c and the four host hash arrays are used, with the ranges
+ *           of gs_create and 1 <= d <= GS_STATIC_MAX_D; P, k_max, rho, reset_momentum and
+ *           state_layout are ignored. 1 <= k <= d.
+ *   merged  [r][c] device input; est [d] device output or NULL; idx [k] device output.
+ * Scratch: no call allocates or frees. The selection's scratch is a fixed array of the
+ * library in device memory, 12.1 bytes per coordinate of GS_STATIC_MAX_D (48.6 MiB), of
+ * which each GPU the library runs on holds its own copy until the process ends; the first
+ * call on a device looks up that device's copy. Calls on one GPU share the array and keep
+ * the last call's contents: calls that overlap on one GPU (other streams or threads without
+ * ordering between them) race. Each call clears what must start at zero with a kernel (no
+ * memset), so a call can be captured in a HIP graph once the device has been set up.
+ * Errors: GS_ERR_INVALID_ARG before anything is enqueued (a larger d among them),
+ * GS_ERR_DEVICE for a failed set-up or launch; gs_last_error(NULL) holds the message. */
+#define GS_STATIC_MAX_D 4194304
+gs_status gs_unsketch_topk_static(const gs_config* cfg, void* stream, const float* merged, int64_t k, float* est,
+                                  int32_t* idx);
+
 /* Static description of a status code. */
 const char* gs_status_string(gs_status status);
 
 /* Message describing the last failing call on `ctx` ("" if none); valid until the next
- * call on the context. With ctx == NULL: the last gs_create failure on this thread. */
+ * call on the context. With ctx == NULL: the last failing context-free call (gs_create or
+ * gs_unsketch_topk_static) on this thread. */
 const char* gs_last_error(const gs_ctx* ctx);
 
 #ifdef __cplusplus

@@ -24,8 +24,9 @@ GS_MAX_WORKERS = 64
 GS_MAX_ROWS = 16
 EXPORTED = ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
             "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_sketch_momentum",
-            "gs_apply_update", "gs_step_profiled", "gs_timing_start", "gs_timing_stop", "gs_status_string",
-            "gs_last_error")
+            "gs_apply_update", "gs_step_profiled", "gs_timing_start", "gs_timing_stop", "gs_unsketch_topk_static",
+            "gs_status_string", "gs_last_error")
+GS_STATIC_MAX_D = 4194304  # largest d of gs_unsketch_topk_static (its fixed scratch array)
 GS_NUM_STAGES = 5
 STAGES = ("accumulate", "sketch", "merge", "select", "gather_reset")
 # layouts of the per-worker state u, v (gs_config.state_layout)
@@ -92,9 +93,11 @@ def load_library():
     lib.gs_apply_update.argtypes = [vp, vp, vp, vp, i64, ctypes.c_float, vp]
     lib.gs_timing_start.argtypes = [vp, ctypes.c_int32]
     lib.gs_timing_stop.argtypes = [vp, vp, vp]
+    lib.gs_unsketch_topk_static.argtypes = [ctypes.POINTER(gs_config), vp, vp, i64, vp, vp]
     for name in ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
                  "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_sketch_momentum",
-                 "gs_apply_update", "gs_step_profiled", "gs_timing_start", "gs_timing_stop"):
+                 "gs_apply_update", "gs_step_profiled", "gs_timing_start", "gs_timing_stop",
+                 "gs_unsketch_topk_static"):
         getattr(lib, name).restype = st
     lib.gs_status_string.argtypes = [st]
     lib.gs_status_string.restype = ctypes.c_char_p
@@ -151,6 +154,25 @@ def gs_create(d: int, P: int, r: int, c: int, k_max: int, hash_a, hash_b, sign_a
     out = ctypes.c_void_p()
     _check(lib.gs_create(ctypes.byref(cfg), ctypes.byref(out)), None, "gs_create")
     return out.value
+
+
+def gs_unsketch_topk_static(d: int, r: int, c: int, hash_params: dict, merged, k: int, est, idx,
+                            stream=None) -> None:
+    """gs_unsketch_topk without a context and without allocating (the library's fixed
+    scratch array; d <= GS_STATIC_MAX_D). merged: [r][c] fp32; est: [d] fp32 or None;
+    idx: [k] int32. Errors are read from gs_last_error(NULL)."""
+    import torch
+
+    lib = load_library()
+    arrs = [np.ascontiguousarray(hash_params[n], dtype=np.uint32) for n in ("a", "b", "a2", "b2")]
+    if any(a.size != r for a in arrs):
+        raise ValueError("hash parameter arrays must have r entries")
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    cfg = gs_config(d, 1, r, c, max(1, k), 0.0, 1, *(a.ctypes.data_as(u32p) for a in arrs), GS_STATE_WORKER_MAJOR)
+    _check(lib.gs_unsketch_topk_static(ctypes.byref(cfg), _stream(stream),
+                                       _ptr(merged, torch.float32, r * c, "merged"), k,
+                                       _ptr(est, torch.float32, d, "est"), _ptr(idx, torch.int32, k, "idx")),
+           None, "gs_unsketch_topk_static")
 
 
 def gs_destroy(ctx: int) -> None:

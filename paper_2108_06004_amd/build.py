@@ -11,7 +11,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libgs.so")
-SOURCES = ["gs_api.hip", "k_stream.hip", "k_select.hip", "k_pull.hip", "k_sketch_state.hip"]
+SOURCES = ["gs_api.hip", "k_stream.hip", "k_select.hip", "k_pull.hip", "k_sketch_state.hip", "gs_static.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -12,7 +12,9 @@
 
 namespace {
 
-thread_local std::string g_create_error;
+// message of the last failing context-free call on this thread (gs_create,
+// gs_unsketch_topk_static): a fixed buffer, so that setting it allocates nothing
+thread_local char g_free_error[512];
 
 constexpr int64_t kP = GS_MERSENNE_P;
 
@@ -24,17 +26,6 @@ gs_status fail(gs_ctx* x, gs_status st, const std::string& msg) {
 gs_status device_status(gs_ctx* x, hipError_t e, const char* where) {
   if (e == hipSuccess) return GS_OK;
   return fail(x, GS_ERR_DEVICE, std::string(where) + ": " + hipGetErrorString(e));
-}
-
-// Granlund-Montgomery reciprocal for 31-bit dividends: l = ceil(log2 c), m = ceil(2^(31+l)/c)
-// (m < 2^32; for c = 1, l = 0 and m = 2^31), and floor(x / c) = floor(x * m / 2^(31+l)).
-void set_divisor(gs::HashSet& hs, uint32_t c) {
-  uint32_t l = 0;
-  while ((1ull << l) < c) ++l;
-  const uint64_t num = 1ull << (31 + l);
-  hs.c = c;
-  hs.magic = (uint32_t)((num + c - 1) / c);
-  hs.shift = 31 + l;
 }
 
 template <typename T>
@@ -87,6 +78,19 @@ hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 }  // namespace
 
 namespace gs {
+// Granlund-Montgomery reciprocal for 31-bit dividends: l = ceil(log2 c), m = ceil(2^(31+l)/c)
+// (m < 2^32; for c = 1, l = 0 and m = 2^31), and floor(x / c) = floor(x * m / 2^(31+l)).
+void set_divisor(HashSet& hs, uint32_t c) {
+  uint32_t l = 0;
+  while ((1ull << l) < c) ++l;
+  const uint64_t num = 1ull << (31 + l);
+  hs.c = c;
+  hs.magic = (uint32_t)((num + c - 1) / c);
+  hs.shift = 31 + l;
+}
+
+void set_free_error(const char* msg) { std::snprintf(g_free_error, sizeof g_free_error, "%s", msg ? msg : ""); }
+
 void stage_mark(gs_ctx* x, hipStream_t s, int t) {
   if (!x->timing || x->t_step >= x->t_max) return;
   (void)hipEventRecord(x->t_events[(int64_t)x->t_step * kStageMarks + t], s);
@@ -107,12 +111,12 @@ const char* gs_status_string(gs_status st) {
   return "unknown status";
 }
 
-const char* gs_last_error(const gs_ctx* x) { return x ? x->last_error.c_str() : g_create_error.c_str(); }
+const char* gs_last_error(const gs_ctx* x) { return x ? x->last_error.c_str() : g_free_error; }
 
 gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
-  g_create_error.clear();
+  gs::set_free_error("");
   auto bad = [](const char* m) {
-    g_create_error = m;
+    gs::set_free_error(m);
     return GS_ERR_INVALID_ARG;
   };
   if (!out) return bad("out is NULL");
@@ -133,7 +137,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
 
   gs_ctx* x = new (std::nothrow) gs_ctx();
   if (!x) {
-    g_create_error = "host allocation failed";
+    gs::set_free_error("host allocation failed");
     return GS_ERR_OUT_OF_MEMORY;
   }
   x->d = cfg->d;
@@ -152,7 +156,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
     x->hs.row[j].a2 = cfg->sign_a[j];
     x->hs.row[j].b2 = cfg->sign_b[j];
   }
-  set_divisor(x->hs, (uint32_t)cfg->c);
+  gs::set_divisor(x->hs, (uint32_t)cfg->c);
 
   hipError_t e = hipGetDevice(&x->device);
   if (e == hipSuccess) {
@@ -161,7 +165,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
     if (e == hipSuccess) x->num_cus = prop.multiProcessorCount > 0 ? prop.multiProcessorCount : 256;
   }
   if (e != hipSuccess) {
-    g_create_error = std::string("HIP device query failed: ") + hipGetErrorString(e);
+    gs::set_free_error((std::string("HIP device query failed: ") + hipGetErrorString(e)).c_str());
     delete x;
     return GS_ERR_DEVICE;
   }
@@ -227,7 +231,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   if (ea == hipSuccess) ea = gs::prepare_prune(x);
   if (ea != hipSuccess) {
     const bool oom = ea == hipErrorOutOfMemory || ea == hipErrorMemoryAllocation;
-    g_create_error = std::string("device scratch allocation failed: ") + hipGetErrorString(ea);
+    gs::set_free_error((std::string("device scratch allocation failed: ") + hipGetErrorString(ea)).c_str());
     (void)hipGetLastError();
     free_scratch(x);
     delete x;

@@ -31,6 +31,23 @@ struct SelectCtl {
   unsigned long long n_heavy;  // HEAVYMIX: |H|
   uint32_t n_stage2;    // keys of the digit-1 bucket b1 staged for the digit-3 pass
 };
+// Buffers of the dense selection (every coordinate a candidate) and of its radix tail: the
+// context's scratch for gs_unsketch_topk and friends, or the static scratch of
+// gs_unsketch_topk_static. hist, hist2, hist_c and ctl->n_stage2 are zero between calls.
+struct SelectBufs {
+  uint32_t* cand_key;   // [cand_cap] candidate keys (dense: key of coordinate t at t)
+  int32_t* cand_idx;    // [cand_cap] candidate coordinates (read only for pruned candidates)
+  int64_t cand_cap;
+  uint32_t* keys;       // [d] staged keys of the digit-1 bucket of the k-th key
+  int32_t* stage_idx;   // [d] their coordinates
+  uint32_t* hist;       // [kDigit1Bins] digit-1 histogram of the dense keys
+  uint32_t* hist2;      // [kDigitBins]
+  uint32_t* hist_c;     // [kDigit1Bins] digit-1 histogram of pruned candidates
+  SelectCtl* ctl;
+  uint32_t* bitmap;     // [ceil(d/32)] output bitmap
+  uint32_t* blockcnt;   // [emit_blocks]
+  int64_t emit_blocks;
+};
 constexpr int kSampleMax = 16384;  // sampled estimates for the pruning bound
 constexpr int64_t kPruneMinCells = 2000000;  // d*r below which the full estimate is faster (measured)
 
@@ -141,6 +158,10 @@ inline StateView state_view(const gs_ctx* x) {
   return x->state_layout == GS_STATE_INTERLEAVED ? StateView{1, x->state_stride} : StateView{x->d, 1};
 }
 inline StateView worker_major_view(const gs_ctx* x) { return StateView{x->d, 1}; }
+inline SelectBufs select_bufs(const gs_ctx* x) {
+  return SelectBufs{x->cand_key, x->cand_idx, x->cand_cap, x->keys,   x->stage_idx, x->hist,
+                    x->hist2,    x->hist_c,   x->ctl,      x->bitmap, x->blockcnt,  x->emit_blocks};
+}
 
 constexpr int kStageMarks = 6;  // events per timed step: before stage 0, after stages 0..4
 // Record timing mark t (0..5) of the current step on `s` when timing is active; mark 5
@@ -164,6 +185,15 @@ hipError_t launch_sketch_state(gs_ctx* x, hipStream_t s, const float* merged, fl
 hipError_t launch_gather_reset(const gs_ctx* x, hipStream_t s, const int32_t* idx, int64_t k, float* u, float* v,
                                float* values);
 int64_t emit_blocks_for(int64_t d);
+// The estimate of every coordinate and the top-k over them (the full path of
+// launch_unsketch_topk) on explicit buffers; r = hs.r, 1 <= k <= d.
+hipError_t launch_unsketch_topk_dense(const HashSet& hs, int64_t d, int num_cus, const SelectBufs& b, hipStream_t s,
+                                      const float* merged, int64_t k, float* est, int32_t* idx);
+// Granlund-Montgomery reciprocal of the bucket modulus c (sets hs.c, hs.magic, hs.shift).
+void set_divisor(HashSet& hs, uint32_t c);
+// Message of the last failing context-free call on this thread (gs_create,
+// gs_unsketch_topk_static), returned by gs_last_error(NULL); no heap allocation.
+void set_free_error(const char* msg);
 hipError_t prepare_prune(gs_ctx* x);
 PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int64_t c, int num_cus);
 hipError_t build_pull_lists(gs_ctx* x);

@@ -992,9 +992,10 @@ __global__ void k_hm_out(const SelectCtl* __restrict__ ctl, int64_t* __restrict_
 }
 
 template <int R>
-void launch_unsketch_r(gs_ctx* x, hipStream_t s, const float* merged, float* est, SelectCtl* gate) {
-  hipLaunchKernelGGL(k_unsketch<R>, dim3(grid_for(x->d, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s, x->hs, merged,
-                     x->d, est, x->cand_key, x->hist, x->bitmap, gate);
+void launch_unsketch_r(const HashSet& hs, int64_t d, int num_cus, const SelectBufs& b, hipStream_t s,
+                       const float* merged, float* est, SelectCtl* gate) {
+  hipLaunchKernelGGL(k_unsketch<R>, dim3(grid_for(d, kBlock, 4 * num_cus)), dim3(kBlock), 0, s, hs, merged, d, est,
+                     b.cand_key, b.hist, b.bitmap, gate);
 }
 
 template <int R, bool HM>
@@ -1049,23 +1050,28 @@ hipError_t allow_prune_lds(size_t bytes) {
 
 // digit2 -> select2 -> finalize -> emit over the candidates: the pruned pass's (pruned = 1,
 // unless it fell short of k) or the full estimate's dense ones.
-hipError_t launch_select_tail(gs_ctx* x, hipStream_t s, int64_t k, int pruned, int32_t* idx) {
+hipError_t launch_select_tail(int64_t d, int num_cus, const SelectBufs& b, hipStream_t s, int64_t k, int pruned,
+                              int32_t* idx) {
   // one block per CU for the pruned candidates (a few times k); the full estimate's dense
   // ones (d) get up to eight per CU (a pruned pass's fallback keeps the smaller grid)
-  int g2 = x->num_cus;
-  if (!pruned) g2 = std::max(g2, grid_for(x->d, 8192, 8 * x->num_cus));
-  hipLaunchKernelGGL(k_digit2, dim3(g2), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl, x->cand_cap,
-                     x->d, x->hist_c, x->hist, pruned, (uint32_t)k, x->hist2, x->keys, x->stage_idx);
-  hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, x->ctl, x->hist2, x->keys, x->stage_idx, x->hist_c,
-                     x->hist, pruned, (uint32_t)k);
-  hipLaunchKernelGGL(k_finalize, dim3(4 * x->num_cus), dim3(kBlock), 0, s, x->cand_key, x->cand_idx, x->ctl,
-                     x->cand_cap, x->d, pruned, x->bitmap);
-  const int64_t words = (x->d + 31) / 32;
-  hipLaunchKernelGGL(k_emit_count, dim3((unsigned)x->emit_blocks), dim3(kSelBlock), 0, s, x->bitmap, words,
-                     x->blockcnt);
-  hipLaunchKernelGGL(k_emit_write, dim3((unsigned)x->emit_blocks), dim3(kSelBlock), 0, s, x->bitmap, words,
-                     x->blockcnt, idx, (uint32_t)k);
+  int g2 = num_cus;
+  if (!pruned) g2 = std::max(g2, grid_for(d, 8192, 8 * num_cus));
+  hipLaunchKernelGGL(k_digit2, dim3(g2), dim3(kBlock), 0, s, b.cand_key, b.cand_idx, b.ctl, b.cand_cap, d, b.hist_c,
+                     b.hist, pruned, (uint32_t)k, b.hist2, b.keys, b.stage_idx);
+  hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, b.ctl, b.hist2, b.keys, b.stage_idx, b.hist_c, b.hist,
+                     pruned, (uint32_t)k);
+  hipLaunchKernelGGL(k_finalize, dim3(4 * num_cus), dim3(kBlock), 0, s, b.cand_key, b.cand_idx, b.ctl, b.cand_cap, d,
+                     pruned, b.bitmap);
+  const int64_t words = (d + 31) / 32;
+  hipLaunchKernelGGL(k_emit_count, dim3((unsigned)b.emit_blocks), dim3(kSelBlock), 0, s, b.bitmap, words,
+                     b.blockcnt);
+  hipLaunchKernelGGL(k_emit_write, dim3((unsigned)b.emit_blocks), dim3(kSelBlock), 0, s, b.bitmap, words,
+                     b.blockcnt, idx, (uint32_t)k);
   return hipGetLastError();
+}
+
+hipError_t launch_select_tail(gs_ctx* x, hipStream_t s, int64_t k, int pruned, int32_t* idx) {
+  return launch_select_tail(x->d, x->num_cus, select_bufs(x), s, k, pruned, idx);
 }
 
 }  // namespace
@@ -1129,7 +1135,7 @@ hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, i
 #define GS_R_CASE(RR) \
   case RR:                                            \
     if (prune) launch_prune_r<RR, false>(x, s, merged, k, nullptr);  \
-    launch_unsketch_r<RR>(x, s, merged, est, gate);  \
+    launch_unsketch_r<RR>(x->hs, x->d, x->num_cus, select_bufs(x), s, merged, est, gate);  \
     break;
     GS_R_CASE(1) GS_R_CASE(2) GS_R_CASE(3) GS_R_CASE(4) GS_R_CASE(5) GS_R_CASE(6) GS_R_CASE(7) GS_R_CASE(8)
     GS_R_CASE(9) GS_R_CASE(10) GS_R_CASE(11) GS_R_CASE(12) GS_R_CASE(13) GS_R_CASE(14) GS_R_CASE(15) GS_R_CASE(16)
@@ -1137,6 +1143,19 @@ hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, i
     default: return hipErrorInvalidValue;
   }
   return launch_select_tail(x, s, k, prune ? 1 : 0, idx);
+}
+
+hipError_t launch_unsketch_topk_dense(const HashSet& hs, int64_t d, int num_cus, const SelectBufs& b, hipStream_t s,
+                                      const float* merged, int64_t k, float* est, int32_t* idx) {
+  switch (hs.r) {
+#define GS_R_CASE(RR) \
+  case RR: launch_unsketch_r<RR>(hs, d, num_cus, b, s, merged, est, nullptr); break;
+    GS_R_CASE(1) GS_R_CASE(2) GS_R_CASE(3) GS_R_CASE(4) GS_R_CASE(5) GS_R_CASE(6) GS_R_CASE(7) GS_R_CASE(8)
+    GS_R_CASE(9) GS_R_CASE(10) GS_R_CASE(11) GS_R_CASE(12) GS_R_CASE(13) GS_R_CASE(14) GS_R_CASE(15) GS_R_CASE(16)
+#undef GS_R_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return launch_select_tail(d, num_cus, b, s, k, 0, idx);
 }
 
 hipError_t launch_heavymix_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, const uint32_t* rnd,

@@ -124,3 +124,17 @@ def test_state_layout_conversions():
             assert st[2, 1] == x[1, 2] and torch.all(st[:, P:] == 0)
         assert torch.equal(ctx.from_state(st), x)
     assert gs.state_stride(1) == 4 and gs.state_stride(8) == 8 and gs.state_stride(17) == 20
+
+
+def test_static_selection_rejects_invalid_arguments_before_any_device_call():
+    lib = gs.load_library()
+    fake = ctypes.c_void_p(256)  # never dereferenced: the checks fail first
+    cfg, keep = _cfg(d=gs.GS_STATIC_MAX_D + 1)
+    assert lib.gs_unsketch_topk_static(ctypes.byref(cfg), None, fake, 1, None, fake) == gs.GS_ERR_INVALID_ARG
+    assert b"GS_STATIC_MAX_D" in lib.gs_last_error(None)
+    cfg, keep = _cfg(d=1000)
+    assert lib.gs_unsketch_topk_static(ctypes.byref(cfg), None, fake, 1001, None, fake) == gs.GS_ERR_INVALID_ARG
+    assert lib.gs_unsketch_topk_static(ctypes.byref(cfg), None, None, 1, None, fake) == gs.GS_ERR_INVALID_ARG
+    assert lib.gs_unsketch_topk_static(None, None, fake, 1, None, fake) == gs.GS_ERR_INVALID_ARG
+    cfg, keep = _cfg(a=[0, 2, 3])
+    assert lib.gs_unsketch_topk_static(ctypes.byref(cfg), None, fake, 1, None, fake) == gs.GS_ERR_INVALID_ARG
