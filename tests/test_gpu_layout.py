@@ -38,18 +38,6 @@ def test_interleaved_small_workload_all_steps(name):
     dv.close()
 
 
-def test_interleaved_full_size_benchmark_step():
-    # the benchmark's workload and launch configuration (25.6M x 8, fused step), full oracle
-    w = synth.WORKLOADS["laplace53-d25.6M-P8"]
-    hp = synth.hash_params(w)
-    dv = Dev(w.d, w.P, w.r, w.c, w.k, hp, w.rho, layout=IL)
-    u = np.zeros((w.P, w.d), np.float32)
-    v = np.zeros((w.P, w.d), np.float32)
-    chain_check(dv, synth.gradients(w, 0), u, v, w.k, w.rho, full_tables=True, n_est=200_000, fused=True,
-                label=f"{w.name} interleaved step 0")
-    dv.close()
-
-
 EDGE = [
     # d, P, r, c, k
     (1, 1, 1, 1, 1),

@@ -16,6 +16,7 @@ import numpy as np
 import pytest
 
 import oracle
+import par_oracle
 import synth
 
 pytestmark = pytest.mark.gpu
@@ -130,7 +131,7 @@ def chain_check(dv: Dev, g, u0, v0, k, rho, reset_momentum=True, full_tables=Tru
     tg = host(dv.tables)
     ora_tables = None
     if full_tables:
-        ora_tables = oracle.sketch(v1, hp, c)
+        ora_tables = par_oracle.sketch(v1, hp, c)
         assert_tol(tg, ora_tables, f"{label}: sketch tables")
     else:
         rng = np.random.default_rng(1234)
@@ -157,7 +158,7 @@ def chain_check(dv: Dev, g, u0, v0, k, rho, reset_momentum=True, full_tables=Tru
         sel = np.unique(np.concatenate([np.random.default_rng(99).integers(0, d, n_est), ig]))
         assert np.array_equal(eg[sel], oracle.unsketch_at(mg, hp, sel)), f"{label}: estimates not exact"
     else:
-        assert np.array_equal(eg, oracle.unsketch(mg, hp, d)), f"{label}: estimates not exact"
+        assert np.array_equal(eg, par_oracle.unsketch(mg, hp, d)), f"{label}: estimates not exact"
     check_topk_of(eg, ig, k, label)
     ref_idx = ig
     # without an estimate vector the pruned selection runs: it must give the same set
@@ -165,8 +166,9 @@ def chain_check(dv: Dev, g, u0, v0, k, rho, reset_momentum=True, full_tables=Tru
     dv.ctx.unsketch_topk(dv.merged, k, idx_p)
     assert np.array_equal(host(idx_p), ig), f"{label}: pruned selection differs from the full one"
     n_tie = 0
+    est_o = idx_o = kth = None
     if end_to_end and ora_tables is not None:
-        est_o = oracle.unsketch(ora_merged, hp, d)
+        est_o = par_oracle.unsketch(ora_merged, hp, d)
         idx_o, kth = oracle.topk(est_o, k)
         n_tie = assert_tie_band(ig, idx_o, lambda s: est_o[s], kth, f"{label}: end-to-end top-k")
 
@@ -193,6 +195,16 @@ def chain_check(dv: Dev, g, u0, v0, k, rho, reset_momentum=True, full_tables=Tru
         e2 = host(dv.est)
         assert np.array_equal(host(idx2), jf), f"{label}: fused top-k differs from gs_unsketch_topk on its sketch"
         check_topk_of(e2, jf, k, f"{label} fused")
+        # the fused sketch's estimates are the oracle's estimates of that sketch, bit for bit,
+        # and the fused selection is the oracle's end-to-end set up to the tie band
+        if n_est:
+            sel = np.unique(np.concatenate([np.random.default_rng(98).integers(0, d, n_est), jf]))
+            assert np.array_equal(e2[sel], oracle.unsketch_at(mf, hp, sel)), f"{label}: fused estimates not exact"
+        else:
+            assert np.array_equal(e2, par_oracle.unsketch(mf, hp, d)), f"{label}: fused estimates not exact"
+        if idx_o is not None:
+            n_tie_f = assert_tie_band(jf, idx_o, lambda s: est_o[s], kth, f"{label}: fused end-to-end top-k")
+            _flush(f"[{label}] fused tie-band differences: {n_tie_f}")
         # values: exact tree sums of the accumulated v at the fused selection
         uc, vc = u1.copy(), v1.copy()
         assert np.array_equal(valf, oracle.gather_reset(jf, uc, vc, reset_momentum)), f"{label}: fused values"
@@ -270,34 +282,20 @@ def test_small_workload_free_running_divergence():
 # ---------------------------------------------------------------------------------------
 # Full-size workloads in the fused launch configuration the benchmark times.
 
-@pytest.mark.parametrize("name,step", [("t3scaled-d14.7M-P4", 0), ("t3scaled-d14.7M-P4", 1),
-                                       ("laplace53-d25.6M-P8", 0)])
-def test_full_size_step(name, step):
-    w = synth.WORKLOADS[name]
+def test_full_size_all_steps_worker_major():
+    # the 14.7M x 4 workload, every step, worker-major state, re-synced from the oracle's
+    # state before each step: every table cell, every estimate, the end-to-end selections
+    # (separate calls and fused step) within the tie band, the state bit for bit. The
+    # 25.6M x 8 and 66M x 16 workloads run in the benchmark's (interleaved) state layout in
+    # test_gpu_fullsize.py.
+    w = synth.WORKLOADS["t3scaled-d14.7M-P4"]
     hp = synth.hash_params(w)
     dv = Dev(w.d, w.P, w.r, w.c, w.k, hp, w.rho)
     u = np.zeros((w.P, w.d), np.float32)
     v = np.zeros((w.P, w.d), np.float32)
-    for t in range(step):  # oracle state before `step`, stepping the oracle only
-        oracle.step(synth.gradients(w, t), u, v, hp, w.c, w.k, rho=w.rho, want_tables=False, want_est=False)
-    g = synth.gradients(w, step)
-    chain_check(dv, g, u, v, w.k, w.rho, full_tables=True, n_est=200_000, fused=True,
-                label=f"{name} step {step}")
-    dv.close()
-
-
-def test_full_size_rowsparse_sampled():
-    # 66M coordinates x 16 workers: the oracle checks 4,000 sampled cells per worker, the
-    # estimates at 200,000 sampled coordinates plus the selection, the merge, the top-k
-    # of the GPU's estimates and the reset in full; the fused step (chunked, overlapped
-    # accumulation and sketch) against the separate calls.
-    w = synth.WORKLOADS["rowsparse-d66M-P16"]
-    hp = synth.hash_params(w)
-    dv = Dev(w.d, w.P, w.r, w.c, w.k, hp, w.rho)
-    u = np.zeros((w.P, w.d), np.float32)
-    v = np.zeros((w.P, w.d), np.float32)
-    chain_check(dv, synth.gradients(w, 0), u, v, w.k, w.rho, full_tables=False, ncells=4000, n_est=200_000,
-                end_to_end=False, fused=True, label=f"{w.name} step 0")
+    for t in range(w.steps):
+        u, v = chain_check(dv, synth.gradients(w, t), u, v, w.k, w.rho, full_tables=True, fused=True,
+                           label=f"{w.name} step {t}")
     dv.close()
 
 
@@ -548,4 +546,24 @@ def test_stage_timing_over_ordinary_steps():
         dv.ctx.step_sketch_momentum(g, U, E, w.k, dv.merged, dv.idx, dv.values)
     stages, n = dv.ctx.timing_stop()
     assert n == 2 and all(ms > 0 for ms in stages.values())
+    dv.close()
+
+
+def test_create_out_of_device_memory_then_recovers():
+    # P*r*c just under the configuration limit with c near p: the fp64 cell accumulators
+    # alone would take 8.8 TB, so gs_create's allocation fails (a failed hipMalloc, no kernel
+    # runs): GS_ERR_OUT_OF_MEMORY with a message, nothing left allocated, and the next
+    # context on the device works
+    hp = synth.hash_params(synth.BASE_SEED + 77, 16)
+    with pytest.raises(gs.GsError) as e:
+        gs.GsContext(1000, 32, 16, (1 << 31) - 2, 10, hp)
+    assert e.value.status == gs.GS_ERR_OUT_OF_MEMORY
+    msg = gs.load_library().gs_last_error(None).decode()
+    assert "allocation failed" in msg, msg
+    torch.cuda.synchronize()
+    w = synth.WORKLOADS["t3planted-d65536-P4"]
+    dv = Dev(w.d, w.P, w.r, w.c, w.k, synth.hash_params(w), w.rho)
+    g = synth.gradients(w, 0)
+    z = np.zeros_like(g)
+    chain_check(dv, g, z, z.copy(), w.k, w.rho, label="after an out-of-memory create")
     dv.close()
