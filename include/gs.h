@@ -79,6 +79,12 @@ typedef enum gs_status {
  *                   in every call that takes them (gs_accumulate, gs_sketch's v,
  *                   gs_gather_reset, gs_step, gs_step_heavymix, gs_step_profiled). Other
  *                   values are GS_ERR_INVALID_ARG.
+ *   options         0, or GS_OPT_ROW_COPY: reserve a worker-interleaved [d][PP] fp32 copy
+ *                   (4 PP d bytes) in an interleaved-state context too. A worker-major context
+ *                   always has it (its sketch gathers from it). An interleaved context needs it
+ *                   only for gs_step_sketch_momentum (GS_ERR_UNSUPPORTED without it) and for
+ *                   a v that is not 16-byte aligned (GS_ERR_INVALID_ARG without it; torch
+ *                   allocations are aligned). Other bits are GS_ERR_INVALID_ARG.
  */
 typedef struct gs_config {
   int64_t d;
@@ -93,7 +99,10 @@ typedef struct gs_config {
   const uint32_t* sign_a;
   const uint32_t* sign_b;
   int32_t state_layout;
+  int32_t options;
 } gs_config;
+
+#define GS_OPT_ROW_COPY 1
 
 typedef struct gs_ctx gs_ctx; /* opaque: a copy of the config plus device scratch */
 
@@ -108,10 +117,12 @@ typedef struct gs_ctx gs_ctx; /* opaque: a copy of the config plus device scratc
  * with enough heavy cells) when d*r exceeds 2,000,000 and estimates every coordinate
  * otherwise; GS_SELECT_PATH=pruned or =full fixes that choice (the selected set is the same
  * either way).
- * Device scratch is about (16 + 4 PP + 4.1 r) d + 8 S P r c bytes (PP = P rounded up to 4; S
- * list segments per tile, 1 unless the sketch is small), plus 2 r d bytes while the lists are
- * built: 1.8 GB at d = 25.6M, P = 8, r = 5, c = 256,000 and 95 GB at d = 2^31 - 2, P = 2,
- * r = 3. The atomic form replaces the lists and the interleaved copy with 8 P r c bytes. */
+ * Device scratch is about (16 + 4.1 r) d + 8 S P r c bytes (S list segments per tile, 1
+ * unless the sketch is small), plus the 4 PP d bytes of the interleaved copy (PP = P rounded
+ * up to 4) in a worker-major context or with GS_OPT_ROW_COPY, plus 2 r d bytes while the
+ * lists are built: with the interleaved state and no copy 1.0 GB at d = 25.6M, P = 8, r = 5,
+ * c = 256,000 (1.8 GB worker-major) and 61 GB at d = 2^31 - 2, P = 2, r = 3 (95 GB
+ * worker-major). The atomic form replaces the lists and the copy with 8 P r c bytes. */
 gs_status gs_create(const gs_config* cfg, gs_ctx** out);
 
 /* Free the context's scratch (after synchronizing the device). NULL is accepted. */

@@ -63,7 +63,11 @@ class gs_config(ctypes.Structure):
         ("sign_a", ctypes.POINTER(ctypes.c_uint32)),
         ("sign_b", ctypes.POINTER(ctypes.c_uint32)),
         ("state_layout", ctypes.c_int32),
+        ("options", ctypes.c_int32),
     ]
+
+
+GS_OPT_ROW_COPY = 1
 
 
 _lib = None
@@ -142,7 +146,7 @@ def _stream(stream):
 
 
 def gs_create(d: int, P: int, r: int, c: int, k_max: int, hash_a, hash_b, sign_a, sign_b, rho: float = 0.9,
-              reset_momentum: bool = True, state_layout: int = GS_STATE_WORKER_MAJOR) -> int:
+              reset_momentum: bool = True, state_layout: int = GS_STATE_WORKER_MAJOR, options: int = 0) -> int:
     """Create a context on the current device; returns the opaque handle (an int)."""
     lib = load_library()
     arrs = [np.ascontiguousarray(a, dtype=np.uint32) for a in (hash_a, hash_b, sign_a, sign_b)]
@@ -150,7 +154,7 @@ def gs_create(d: int, P: int, r: int, c: int, k_max: int, hash_a, hash_b, sign_a
         raise ValueError("hash parameter arrays must have r entries")
     u32p = ctypes.POINTER(ctypes.c_uint32)
     cfg = gs_config(d, P, r, c, k_max, rho, int(bool(reset_momentum)), *(a.ctypes.data_as(u32p) for a in arrs),
-                    int(state_layout))
+                    int(state_layout), int(options))
     out = ctypes.c_void_p()
     _check(lib.gs_create(ctypes.byref(cfg), ctypes.byref(out)), None, "gs_create")
     return out.value
@@ -168,7 +172,8 @@ def gs_unsketch_topk_static(d: int, r: int, c: int, hash_params: dict, merged, k
     if any(a.size != r for a in arrs):
         raise ValueError("hash parameter arrays must have r entries")
     u32p = ctypes.POINTER(ctypes.c_uint32)
-    cfg = gs_config(d, 1, r, c, max(1, k), 0.0, 1, *(a.ctypes.data_as(u32p) for a in arrs), GS_STATE_WORKER_MAJOR)
+    cfg = gs_config(d, 1, r, c, max(1, k), 0.0, 1, *(a.ctypes.data_as(u32p) for a in arrs), GS_STATE_WORKER_MAJOR,
+                    0)
     _check(lib.gs_unsketch_topk_static(ctypes.byref(cfg), _stream(stream),
                                        _ptr(merged, torch.float32, r * c, "merged"), k,
                                        _ptr(est, torch.float32, d, "est"), _ptr(idx, torch.int32, k, "idx")),
@@ -249,13 +254,17 @@ class GsContext:
     """A context plus shape/dtype checks on every call."""
 
     def __init__(self, d: int, P: int, r: int, c: int, k_max: int, hash_params: dict, rho: float = 0.9,
-                 reset_momentum: bool = True, state_layout: str = "worker_major"):
+                 reset_momentum: bool = True, state_layout: str = "worker_major", row_copy: bool = False):
+        """row_copy: reserve the interleaved row copy in an interleaved-state context too
+        (GS_OPT_ROW_COPY; needed there by step_sketch_momentum and by v views that are not
+        16-byte aligned)."""
         if state_layout not in STATE_LAYOUTS:
             raise ValueError(f"state_layout must be one of {sorted(STATE_LAYOUTS)}")
         self.d, self.P, self.r, self.c, self.k_max = d, P, r, c, k_max
         self.state_layout = state_layout
         self.handle = gs_create(d, P, r, c, k_max, hash_params["a"], hash_params["b"], hash_params["a2"],
-                                hash_params["b2"], rho, reset_momentum, STATE_LAYOUTS[state_layout])
+                                hash_params["b2"], rho, reset_momentum, STATE_LAYOUTS[state_layout],
+                                GS_OPT_ROW_COPY if row_copy else 0)
 
     @property
     def state_shape(self) -> tuple:

@@ -75,6 +75,15 @@ bool valid_ab(const uint32_t* a, const uint32_t* b, int r) {
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
+// An interleaved v the pull cannot gather directly (16-byte pieces of its rows) goes through
+// the context's interleaved copy, which an interleaved context has only with GS_OPT_ROW_COPY.
+bool unaligned_without_copy(const gs_ctx* x, const float* v) {
+  return x->use_pull && x->state_layout == GS_STATE_INTERLEAVED && x->P <= 16 && ((uintptr_t)v & 15u) != 0 &&
+         x->vI == nullptr;
+}
+constexpr const char* kUnalignedMsg =
+    ": interleaved v is not 16-byte aligned and the context has no row copy (GS_OPT_ROW_COPY)";
+
 }  // namespace
 
 namespace gs {
@@ -134,6 +143,7 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   if ((int64_t)cfg->P * cfg->r * cfg->c > (int64_t)1 << 40) return bad("P*r*c too large");
   if (cfg->state_layout != GS_STATE_WORKER_MAJOR && cfg->state_layout != GS_STATE_INTERLEAVED)
     return bad("state_layout must be GS_STATE_WORKER_MAJOR or GS_STATE_INTERLEAVED");
+  if (cfg->options & ~GS_OPT_ROW_COPY) return bad("options: unknown bits");
 
   gs_ctx* x = new (std::nothrow) gs_ctx();
   if (!x) {
@@ -216,7 +226,10 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
     chk(alloc(&x->bases, x->list_cap / gs::kListGroup));
     chk(alloc(&x->tile_off, (int64_t)x->plan.T + 1));
     chk(alloc(&x->tile_n, (int64_t)x->plan.T));
-    chk(alloc(&x->vI, x->d * x->plan.PP));
+    // the interleaved copy: the worker-major state's sketch gathers from it; an interleaved
+    // context gathers the caller's v and needs the copy only on request (GS_OPT_ROW_COPY)
+    if (x->state_layout == GS_STATE_WORKER_MAJOR || (cfg->options & GS_OPT_ROW_COPY))
+      chk(alloc(&x->vI, x->d * x->plan.PP));
     chk(alloc(&x->partial, (int64_t)x->plan.S * x->r * x->c * x->P));
   } else {
     chk(alloc(&x->acc64, (int64_t)x->P * x->r * x->c));
@@ -265,6 +278,7 @@ gs_status gs_sketch(gs_ctx* x, void* stream, const float* v, float* tables) {
   if (!x) return GS_ERR_INVALID_ARG;
   x->last_error.clear();
   if (!v || !tables) return fail(x, GS_ERR_INVALID_ARG, "gs_sketch: NULL array");
+  if (unaligned_without_copy(x, v)) return fail(x, GS_ERR_INVALID_ARG, std::string("gs_sketch") + kUnalignedMsg);
   hipStream_t s = as_stream(stream);
   hipError_t e;
   if (x->use_pull) {
@@ -350,6 +364,7 @@ gs_status gs_step(gs_ctx* x, void* stream, const float* g, float* u, float* v, i
   x->last_error.clear();
   if (!g || !u || !v || !merged || !idx || !values) return fail(x, GS_ERR_INVALID_ARG, "gs_step: NULL array");
   if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_step: k must satisfy 1 <= k <= k_max");
+  if (unaligned_without_copy(x, v)) return fail(x, GS_ERR_INVALID_ARG, std::string("gs_step") + kUnalignedMsg);
   hipStream_t s = as_stream(stream);
   hipError_t e = launch_sketch_phase(x, s, g, u, v, merged);
   if (e == hipSuccess) e = gs::launch_unsketch_topk(x, s, merged, k, nullptr, idx);
@@ -376,6 +391,8 @@ gs_status gs_step_heavymix(gs_ctx* x, void* stream, const float* g, float* u, fl
   if (!g || !u || !v || !rnd || !merged || !idx || !values)
     return fail(x, GS_ERR_INVALID_ARG, "gs_step_heavymix: NULL array");
   if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_step_heavymix: k must satisfy 1 <= k <= k_max");
+  if (unaligned_without_copy(x, v))
+    return fail(x, GS_ERR_INVALID_ARG, std::string("gs_step_heavymix") + kUnalignedMsg);
   hipStream_t s = as_stream(stream);
   hipError_t e = launch_sketch_phase(x, s, g, u, v, merged);
   if (e == hipSuccess) e = gs::launch_heavymix_topk(x, s, merged, k, rnd, nullptr, idx, n_heavy, nullptr);
@@ -393,6 +410,9 @@ gs_status gs_step_sketch_momentum(gs_ctx* x, void* stream, const float* g, float
     return fail(x, GS_ERR_INVALID_ARG, "gs_step_sketch_momentum: NULL array");
   if (k < 1 || k > x->k_max)
     return fail(x, GS_ERR_INVALID_ARG, "gs_step_sketch_momentum: k must satisfy 1 <= k <= k_max");
+  if (x->use_pull && x->vI == nullptr)
+    return fail(x, GS_ERR_UNSUPPORTED,
+                "gs_step_sketch_momentum: an interleaved-state context needs the row copy (GS_OPT_ROW_COPY)");
   hipStream_t s = as_stream(stream);
   hipError_t e;
   gs::stage_mark(x, s, 0);
@@ -482,6 +502,8 @@ gs_status gs_step_profiled(gs_ctx* x, void* stream, const float* g, float* u, fl
   if (!g || !u || !v || !merged || !idx || !values || !stage_ms)
     return fail(x, GS_ERR_INVALID_ARG, "gs_step_profiled: NULL array");
   if (k < 1 || k > x->k_max) return fail(x, GS_ERR_INVALID_ARG, "gs_step_profiled: k must satisfy 1 <= k <= k_max");
+  if (unaligned_without_copy(x, v))
+    return fail(x, GS_ERR_INVALID_ARG, std::string("gs_step_profiled") + kUnalignedMsg);
   hipStream_t s = as_stream(stream);
   hipEvent_t ev[GS_NUM_STAGES + 1] = {};
   hipError_t e = hipSuccess;

@@ -43,13 +43,13 @@ def test_status_strings():
 
 def _cfg(**over):
     hp = {"a": [1, 2, 3], "b": [0, 5, 7], "a2": [9, 10, 11], "b2": [1, 1, 1]}
-    kw = dict(d=1000, P=4, r=3, c=50, k_max=10, rho=0.9, reset_momentum=1, state_layout=0)
+    kw = dict(d=1000, P=4, r=3, c=50, k_max=10, rho=0.9, reset_momentum=1, state_layout=0, options=0)
     kw.update({k: v for k, v in over.items() if k in kw})
     hp.update({k: v for k, v in over.items() if k in hp})
     keep = [np.ascontiguousarray(hp[k], dtype=np.uint32) for k in ("a", "b", "a2", "b2")]
     u32p = ctypes.POINTER(ctypes.c_uint32)
     cfg = gs.gs_config(kw["d"], kw["P"], kw["r"], kw["c"], kw["k_max"], kw["rho"], kw["reset_momentum"],
-                       *(a.ctypes.data_as(u32p) for a in keep), kw["state_layout"])
+                       *(a.ctypes.data_as(u32p) for a in keep), kw["state_layout"], kw["options"])
     return cfg, keep
 
 
@@ -61,7 +61,7 @@ P31 = (1 << 31) - 1
                                                                          b2=[0] * 17),
     dict(c=0), dict(c=P31), dict(k_max=0), dict(k_max=1001), dict(rho=float("nan")), dict(rho=float("inf")),
     dict(a=[0, 2, 3]), dict(a=[1, P31, 3]), dict(b=[0, P31, 0]), dict(a2=[1, 0, 1]), dict(b2=[P31, 0, 0]),
-    dict(state_layout=2), dict(state_layout=-1),
+    dict(state_layout=2), dict(state_layout=-1), dict(options=2), dict(options=-1),
 ])
 def test_create_rejects_invalid_config_before_any_device_call(over):
     lib = gs.load_library()

@@ -91,8 +91,19 @@ def test_interleaved_padding_untouched_and_misaligned_views(P):
     v0 = rng.standard_normal((P, d)).astype(np.float32)
     ref = oracle.step(g, u0.copy(), v0.copy(), hp, c, k, rho=0.9, want_tables=False)
     kth = float(oracle.topk(ref["est"], k)[1])
-    dv = Dev(d, P, r, c, k, hp, 0.9, layout=IL)
+    # a v view that is not 16-byte aligned needs the context's row copy (GS_OPT_ROW_COPY)
+    plain = Dev(d, P, r, c, k, hp, 0.9, layout=IL)
     PP = gs.state_stride(P)
+    mis = [torch.zeros((d * PP + 1,), dtype=torch.float32, device=DEV)[1:].view(d, PP) for _ in range(2)]
+    with pytest.raises(gs.GsError) as e:
+        plain.ctx.step(to_dev(g), mis[0], mis[1], k, plain.merged, plain.idx, plain.values)
+    assert e.value.status == gs.GS_ERR_INVALID_ARG
+    with pytest.raises(gs.GsError) as e:  # the sketch-space step needs the copy too
+        U = torch.zeros((r, c), dtype=torch.float32, device=DEV)
+        plain.ctx.step_sketch_momentum(to_dev(g), U, U.clone(), k, plain.merged, plain.idx, plain.values)
+    assert e.value.status == gs.GS_ERR_UNSUPPORTED
+    plain.close()
+    dv = Dev(d, P, r, c, k, hp, 0.9, layout=IL, row_copy=True)
     for offset in (0, 1):
         _flush(f"[padding P={P} offset={offset}]")
         bufs = [torch.full((d * PP + offset,), 12345.0, dtype=torch.float32, device=DEV) for _ in range(2)]

@@ -88,10 +88,11 @@ def check_topk_of(est, idx, k, what):
 class Dev:
     """GPU buffers and a context for one workload shape."""
 
-    def __init__(self, d, P, r, c, k, hp, rho=0.9, reset_momentum=True, layout="worker_major"):
+    def __init__(self, d, P, r, c, k, hp, rho=0.9, reset_momentum=True, layout="worker_major", row_copy=False):
         self.d, self.P, self.r, self.c, self.k = d, P, r, c, k
         self.hp = hp
-        self.ctx = gs.GsContext(d, P, r, c, k, hp, rho=rho, reset_momentum=reset_momentum, state_layout=layout)
+        self.ctx = gs.GsContext(d, P, r, c, k, hp, rho=rho, reset_momentum=reset_momentum, state_layout=layout,
+                                row_copy=row_copy)
         f32 = dict(dtype=torch.float32, device=DEV)
         self.tables = torch.empty((P, r, c), **f32)
         self.merged = torch.empty((r, c), **f32)
