@@ -77,6 +77,10 @@ struct PullPlan {
   // coordinates in `list`, position | sign << 15 in `codes`.
   int32_t packed;
   int32_t off_bits;
+  // list build: t / W as (t * w_magic) >> w_shift, 1 / c, bits of a tile index
+  uint32_t w_magic, w_shift;
+  double inv_c;
+  int32_t tile_bits;
 };
 constexpr int kListGroup = 64;
 constexpr int64_t kMaxFillLds = 160 * 1024;  // LDS of the list-fill kernel holds T cursors

@@ -39,16 +39,38 @@ int grid_for(int64_t work_items, int per_block, int cap) {
   return (int)b;
 }
 
+// theta * col mod c for theta < 2^22 and col < c < 2^31: the product is below 2^53, so it
+// and its quotient estimate in double precision are within one of the true quotient.
+__device__ __forceinline__ uint32_t scaled_position(uint32_t theta, uint32_t col, uint32_t c, double inv_c) {
+  const uint64_t prod = (uint64_t)theta * col;
+  const uint64_t q = (uint64_t)((double)prod * inv_c);
+  int64_t rem = (int64_t)(prod - q * (uint64_t)c);
+  if (rem < 0) rem += c;
+  if (rem >= (int64_t)c) rem -= c;
+  return (uint32_t)rem;
+}
+
 // The tile of entry (j, i) and the entry's position in it (the scaled column t = theta_j *
 // col mod c, less the tile's first position), and the sign as a float sign-bit mask.
 __device__ __forceinline__ void tile_of(const HashSet& hs, const PullPlan& pl, int j, uint32_t i, uint32_t& pos,
                                         uint32_t& sflip, uint32_t& tile) {
   uint32_t col;
   hash_ij(hs, j, i, col, sflip);
-  const uint32_t t = (uint32_t)(((uint64_t)pl.theta[j] * col) % hs.c);
-  const uint32_t k = t / (uint32_t)pl.W;
+  const uint32_t t = scaled_position(pl.theta[j], col, hs.c, pl.inv_c);
+  const uint32_t k = (uint32_t)(((uint64_t)t * pl.w_magic) >> pl.w_shift);  // t / W
   tile = (uint32_t)j * pl.tiles_per_row + k;
   pos = t - k * (uint32_t)pl.W;
+}
+
+// Lanes of the wave whose `t` equals this lane's (t < 2^nbits), by one ballot per bit.
+__device__ __forceinline__ uint64_t same_value_lanes(uint32_t t, bool valid, int nbits) {
+  uint64_t m = __ballot(valid);
+  for (int b = 0; b < nbits; ++b) {
+    const bool bit = (t >> b) & 1u;
+    const uint64_t ones = __ballot(valid && bit);
+    m &= bit ? ones : ~ones;
+  }
+  return m;
 }
 
 // Work item of pull workgroup b (of n): the workgroups of one round (`slots` resident at a
@@ -70,18 +92,31 @@ __device__ __forceinline__ uint32_t column_at(const HashSet& hs, const PullPlan&
 // ------------------------------------------------------------------------------------
 // Static list build (gs_create).
 
-// counts[b][t]: entries of build chunk b that fall in tile t.
+// counts[b][t]: entries of build chunk b that fall in tile t (every t written). The chunk's
+// counts are an LDS histogram; consecutive coordinates mostly share a tile, so the lanes of
+// a wave add per distinct tile, once (a ballot per tile).
 __global__ void __launch_bounds__(kBlock) k_build_count(HashSet hs, PullPlan pl, int64_t d,
                                                         uint32_t* __restrict__ counts) {
+  extern __shared__ uint32_t h[];  // [T]
   const int64_t b = blockIdx.x;
+  for (int64_t t = threadIdx.x; t < pl.T; t += kBlock) h[t] = 0u;
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const uint64_t below = (1ull << lane) - 1ull;
   const int64_t lo = b * pl.chunk, hi = min(d, lo + pl.chunk);
-  for (int64_t i = lo + threadIdx.x; i < hi; i += kBlock) {
+  for (int64_t i0 = lo; i0 < hi; i0 += kBlock) {  // block-uniform
+    const int64_t i = i0 + threadIdx.x;
+    const bool valid = i < hi;
     for (int j = 0; j < hs.r; ++j) {
-      uint32_t pos, sflip, t;
-      tile_of(hs, pl, j, (uint32_t)i, pos, sflip, t);
-      atomicAdd(&counts[b * pl.T + t], 1u);
+      uint32_t pos = 0, sflip = 0, t = 0;
+      if (valid) tile_of(hs, pl, j, (uint32_t)i, pos, sflip, t);
+      // the first lane of each distinct tile adds the tile's lane count (distinct addresses)
+      const uint64_t same = same_value_lanes(t, valid, pl.tile_bits);
+      if (valid && (same & below) == 0ull) atomicAdd(&h[t], (uint32_t)__popcll(same));
     }
   }
+  __syncthreads();
+  for (int64_t t = threadIdx.x; t < pl.T; t += kBlock) counts[b * pl.T + t] = h[t];
 }
 
 // Per tile: exclusive prefix of counts over chunks (in place) and the tile total.
@@ -90,6 +125,7 @@ __global__ void __launch_bounds__(kBlock) k_build_prefix(PullPlan pl, uint32_t* 
   const int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x;
   if (t >= pl.T) return;
   uint32_t run = 0;
+#pragma unroll 8
   for (int64_t b = 0; b < pl.NB; ++b) {
     const uint32_t cnt = counts[b * pl.T + t];
     counts[b * pl.T + t] = run;
@@ -159,9 +195,11 @@ __global__ void __launch_bounds__(kBlock) k_build_pack(uint32_t* __restrict__ li
   if (bad) atomicOr(flag, 1u);
 }
 
-// In-order fill: one wave per build chunk walks its coordinates in ascending order; lanes
-// take their list slots one after another (lane order = coordinate order), so every
-// tile's list comes out sorted by coordinate.
+// In-order fill: one wave per build chunk walks its coordinates in ascending order, 64 at
+// a time (lane order = coordinate order). The lanes whose entry falls in one tile take
+// consecutive slots in lane order: per distinct tile of the wave, its first lane advances
+// the tile's cursor by the number of such lanes and each lane adds its rank among them. So
+// every tile's list comes out sorted by coordinate.
 __global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int64_t d,
                                                    const uint32_t* __restrict__ prefix,
                                                    const int64_t* __restrict__ off, uint32_t* __restrict__ list,
@@ -171,6 +209,7 @@ __global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int6
   const int lane = threadIdx.x;
   for (int64_t t = lane; t < pl.T; t += 64) cursor[t] = prefix[b * pl.T + t];
   __syncthreads();
+  const uint64_t below = (1ull << lane) - 1ull;
   const int64_t lo = b * pl.chunk, hi = min(d, lo + pl.chunk);
   for (int64_t base = lo; base < hi; base += 64) {
     const int64_t i = base + lane;
@@ -178,14 +217,18 @@ __global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int6
     for (int j = 0; j < hs.r; ++j) {
       uint32_t pos = 0, sflip = 0, t = 0;
       if (valid) tile_of(hs, pl, j, (uint32_t)i, pos, sflip, t);
-      uint32_t slot = 0;
-      for (int l = 0; l < 64; ++l) {
-        if (lane == l && valid) {
-          slot = cursor[t];
-          cursor[t] = slot + 1;
-        }
-        __builtin_amdgcn_wave_barrier();
+      // per distinct tile, its first lane advances the cursor by the tile's lane count (the
+      // leaders hold distinct tiles, so their reads and writes do not collide) and every lane
+      // adds its rank among the tile's lanes
+      const uint64_t same = same_value_lanes(t, valid, pl.tile_bits);
+      const int leader = same ? __builtin_ctzll(same) : lane;
+      uint32_t start = 0;
+      if (valid && leader == lane) {
+        start = cursor[t];
+        cursor[t] = start + (uint32_t)__popcll(same);
       }
+      start = __shfl(start, leader, 64);
+      const uint32_t slot = start + (uint32_t)__popcll(same & below);
       if (valid) {
         list[off[t] + slot] = (uint32_t)i;
         codes[off[t] + slot] = (uint16_t)(pos | (sflip >> 16));  // position < 2^15; sign in bit 15
@@ -685,6 +728,18 @@ PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int6
   }
   pl.tiles_per_row = (int32_t)((c + W - 1) / W);
   pl.T = r * pl.tiles_per_row;
+  {
+    // t / W for t < c < 2^31 by a reciprocal multiply (as the bucket modulus), c's
+    // reciprocal for theta * col mod c, and the bits of a tile index
+    uint32_t l = 0;
+    while ((1ull << l) < (uint64_t)W) ++l;
+    pl.w_shift = 31 + l;
+    pl.w_magic = (uint32_t)(((1ull << (31 + l)) + (uint64_t)W - 1) / (uint64_t)W);
+    pl.inv_c = 1.0 / (double)c;
+    int tb = 1;
+    while ((1ll << tb) < (int64_t)pl.T) ++tb;
+    pl.tile_bits = tb;
+  }
   // small sketches: split each tile's list into segments so every CU gets work, at most one
   // round of workgroups (T * S <= slots: a second round would hold only the leftovers)
   int64_t S = slots / pl.T;
@@ -695,8 +750,12 @@ PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int6
   if (S > per_tile / 16384) S = per_tile / 16384;
   if (S < 1) S = 1;
   pl.S = (int32_t)S;
-  // build chunks: 64 Ki coordinates each
-  pl.chunk = 65536;
+  // build chunks (one fill wave each): 16 Ki coordinates, so that the fill has several waves
+  // per CU, or more for large d, so that there are at most 4,096 chunks (the per-chunk
+  // counts, NB * T words, stay small and the per-tile prefix over chunks short)
+  int64_t chunk = 16384;
+  if ((d + chunk - 1) / chunk > 4096) chunk = ((d + 4095) / 4096 + 255) / 256 * 256;
+  pl.chunk = chunk;
   pl.NB = (int32_t)((d + pl.chunk - 1) / pl.chunk);
   return pl;
 }
@@ -721,6 +780,9 @@ hipError_t build_pull_lists(gs_ctx* x) {
   const size_t fill_lds = (size_t)pl.T * sizeof(uint32_t);
   hipError_t ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_build_fill),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)fill_lds);
+  if (ea == hipSuccess)
+    ea = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_build_count),
+                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)fill_lds);
   if (ea != hipSuccess) return ea;
   ea = prepare_pull_kernels(x);
   if (ea != hipSuccess) return ea;
@@ -730,10 +792,9 @@ hipError_t build_pull_lists(gs_ctx* x) {
   hipError_t e = hipMalloc(reinterpret_cast<void**>(&counts), (size_t)pl.NB * pl.T * sizeof(uint32_t));
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&total), (size_t)pl.T * sizeof(uint32_t));
   if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void**>(&flag), sizeof(uint32_t));
-  if (e == hipSuccess) e = hipMemset(counts, 0, (size_t)pl.NB * pl.T * sizeof(uint32_t));
   if (e == hipSuccess) e = hipMemset(flag, 0, sizeof(uint32_t));
   if (e == hipSuccess) {
-    hipLaunchKernelGGL(k_build_count, dim3(pl.NB), dim3(kBlock), 0, 0, x->hs, pl, x->d, counts);
+    hipLaunchKernelGGL(k_build_count, dim3(pl.NB), dim3(kBlock), fill_lds, 0, x->hs, pl, x->d, counts);
     hipLaunchKernelGGL(k_build_prefix, dim3((pl.T + kBlock - 1) / kBlock), dim3(kBlock), 0, 0, pl, counts, total);
     hipLaunchKernelGGL(k_build_offsets, dim3(1), dim3(1024), 0, 0, pl, total, x->tile_off, x->tile_n);
     hipLaunchKernelGGL(k_build_fill, dim3(pl.NB), dim3(64), (size_t)pl.T * sizeof(uint32_t), 0, x->hs, pl, x->d,

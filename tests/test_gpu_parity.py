@@ -568,3 +568,22 @@ def test_create_out_of_device_memory_then_recovers():
     z = np.zeros_like(g)
     chain_check(dv, g, z, z.copy(), w.k, w.rho, label="after an out-of-memory create")
     dv.close()
+
+
+@pytest.mark.parametrize("layout", ["worker_major", "interleaved"])
+@pytest.mark.parametrize("d,P,r,c", [(300_007, 8, 5, 2_999), (1_000_003, 3, 7, 20_011), (65_536, 16, 3, 4_096),
+                                     (200_000, 5, 4, 200_000)])
+def test_sketch_exact_on_integer_state(layout, d, P, r, c):
+    # integer-valued state (|v| < 2^12, at most d/c + slack entries per cell): every cell sum
+    # is exact in fp32, so the per-worker tables equal the oracle's bit for bit. A tile list
+    # that missed, repeated or misplaced an entry, or carried a wrong sign, would change a
+    # cell: this pins the static lists built by gs_create (several build chunks of 65,536
+    # coordinates, packed and unpacked forms)
+    hp = synth.hash_params(synth.BASE_SEED + 13 * d + P, r)
+    rng = np.random.default_rng(d ^ P)
+    v = rng.integers(-2048, 2048, (P, d)).astype(np.float32)
+    dv = Dev(d, P, r, c, 1, hp, layout=layout)
+    tables = torch.empty((P, r, c), dtype=torch.float32, device=DEV)
+    dv.ctx.sketch(dv.state(v), tables)
+    assert np.array_equal(host(tables), par_oracle.sketch(v, hp, c)), "tables of an integer state not exact"
+    dv.close()
