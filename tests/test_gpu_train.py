@@ -98,3 +98,63 @@ def test_apply_update_rejects_invalid_arguments():
         assert e.value.status == gs.GS_ERR_INVALID_ARG
     assert not host(w).any()
     ctx.close()
+
+
+def test_optimizer_hook_on_a_module_matches_the_oracle_every_step():
+    # a small MLP regressing a fixed random teacher (synthetic data, no dataset), P = 4
+    # simulated workers on their own micro-batches, the warm-up schedule; at every step the
+    # parameters after the update equal oracle.apply_update on the flat parameters before
+    # it with the step's selection and values, bit for bit, and the step itself equals the
+    # oracle's step from the same state (selection within the tie band, values and state
+    # bit for bit)
+    from paper_2108_06004_amd.train import GlobalSketchOptimizer
+
+    torch.manual_seed(11)
+    P, r, c, batch = 4, 5, 2048, 32
+    model = torch.nn.Sequential(torch.nn.Linear(64, 256), torch.nn.Tanh(), torch.nn.Linear(256, 32)).to(DEV)
+    teacher = torch.nn.Sequential(torch.nn.Linear(64, 32)).to(DEV)
+    hp = synth.hash_params(synth.BASE_SEED + 94, r)
+    sched = DensitySchedule(0.01, 0.05, [(0.25, 0.05), (0.05, 0.05)])
+    opt = GlobalSketchOptimizer(model.parameters(), P, r, c, hp, sched, rho=0.9)
+    d = opt.d
+    assert d == sum(p.numel() for p in model.parameters()) == 64 * 256 + 256 + 256 * 32 + 32
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(3)
+    losses = []
+    for t in range(12):
+        opt.set_epoch(t // 4)
+        total = 0.0
+        for q in range(P):
+            x = torch.randn(batch, 64, device=DEV, generator=gen)
+            with torch.no_grad():
+                y = teacher(x)
+            loss = ((model(x) - y) ** 2).mean()
+            loss.backward()
+            opt.collect(q)
+            total += float(loss)
+        losses.append(total / P)
+        g = host(opt.grads).copy()
+        u0, v0 = opt.ctx.from_state(opt.u).cpu().numpy(), opt.ctx.from_state(opt.v).cpu().numpy()
+        w0 = host(opt.flat).copy()
+        opt.step()
+        k = opt.last_k
+        lr = sched.at(t // 4)[1]
+        idx, vals = host(opt.idx)[:k].copy(), host(opt.values)[:k].copy()
+        want = w0.copy()
+        oracle.apply_update(want, idx, vals, lr / P)
+        assert np.array_equal(host(opt.flat), want), f"step {t}: update not bit-exact"
+        assert torch.equal(torch.cat([p.detach().reshape(-1) for p in model.parameters()]), opt.flat)
+        # the compression step from the same state
+        uo, vo = u0.copy(), v0.copy()
+        ref = oracle.step(g, uo, vo, hp, c, k, rho=0.9)
+        kth = np.sort(np.abs(ref["est"]).astype(np.float64))[::-1][k - 1]
+        sd = np.setxor1d(idx, ref["idx"])
+        assert np.all(np.abs(np.abs(ref["est"][sd].astype(np.float64)) - kth) <= 1e-6 * kth), f"step {t}: selection"
+        common, gi, oi = np.intersect1d(idx, ref["idx"], return_indices=True)
+        assert np.array_equal(vals[gi], ref["values"][oi]), f"step {t}: values"
+        if sd.size == 0:
+            assert np.array_equal(opt.ctx.from_state(opt.u).cpu().numpy(), uo), f"step {t}: u"
+            assert np.array_equal(opt.ctx.from_state(opt.v).cpu().numpy(), vo), f"step {t}: v"
+    print(f"optimizer hook: loss {losses[0]:.4f} -> {losses[-1]:.4f}", flush=True)
+    assert losses[-1] < losses[0]
+    opt.close()
