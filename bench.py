@@ -14,8 +14,13 @@ Prints one JSON line with
                many further steps after the timed region, which carries no events inside a
                step) against MI355X's 8 TB/s HBM peak
   cpu_baseline the plain CPU oracle (single thread) timed on a bounded sample
-Algorithmic bytes per step: B = 20*P*d + 8*P*r*c + 8*r*c + 12*P*k + 8*k (vector state); with
---state sketch (momentum and error kept in the sketch) B = 4*P*d + 8*P*r*c + 28*r*c + 8*k.
+Algorithmic bytes per step: B = 20*P*d + 8*r*c + 12*P*k + 8*k (vector state; the fused step
+never writes the P per-worker tables); with --state sketch (momentum and error kept in the
+sketch) B = 4*P*d + 24*r*c + 8*k.
+
+The roofline object names the dominant kernel: of the stages within 10% of the longest one,
+the one furthest below the HBM peak in algorithmic bytes. It also carries every such
+co-dominant stage and the whole step's fraction (B / time per step / 8 TB/s).
 """
 from __future__ import annotations
 
@@ -43,18 +48,52 @@ def stage_bytes(w, state: str = "vector") -> dict:
     if state == "sketch":
         return {
             "interleave": 0,                      # implementation only (g is read by the sketch)
-            "sketch": 4 * P * d + 4 * P * r * c,  # read g, write the P tables
-            "merge": 4 * P * r * c + 4 * r * c,   # read the P tables, write the merged one
+            "sketch": 4 * P * d + 4 * r * c,      # read g, write the merged table (merged in the tiles)
+            "merge": 0,                           # no kernel
             "select": 4 * r * c + 16 * r * c + 4 * r * c + 4 * k,  # read S; U, E read+written; E read
             "state_update": 8 * k,                # values and the correction of touched cells
         }
+    # the fused step never writes the P per-worker tables: its tiles merge their own cells
     return {
         "accumulate": 20 * P * d,            # read g, u, v; write u, v
-        "sketch": 4 * P * d + 4 * P * r * c, # read v, write the P tables (v is not re-read once fused)
-        "merge": 4 * P * r * c + 4 * r * c,  # read the P tables, write the merged one
+        "sketch": 4 * P * d + 4 * r * c,     # read v once, write the merged table
+        "merge": 0,                          # no kernel: merged inside the sketch's tiles
         "select": 4 * r * c + 4 * k,         # read the merged table, write k indices
         "gather_reset": 12 * P * k + 4 * k,  # read v, zero u and v at k coordinates; write k values
     }
+
+
+def step_bytes(w, state: str = "vector") -> int:
+    """Algorithmic bytes of one fused step. Vector state: read g, u, v and write u, v
+    (20 P d); the merged table written and read (8 r c); at the k selected coordinates v
+    read, u and v zeroed (12 P k); idx and values written (8 k). The P per-worker tables
+    never reach memory in the fused step, so they are not counted. Sketch state: read g
+    (4 P d); merged written (4 r c); U, E read and written (16 r c); E read for the
+    estimates (4 r c); idx and values (8 k)."""
+    P, d, r, c, k = w.P, w.d, w.r, w.c, w.k
+    if state == "sketch":
+        return 4 * P * d + 4 * r * c + 16 * r * c + 4 * r * c + 8 * k
+    return 20 * P * d + 8 * r * c + 12 * P * k + 8 * k
+
+
+def roofline_of(stages: list, step_bytes_: int, step_ms: float):
+    """The roofline object of the bench line. `stages`: per stage {stage, kernel, mean_ms,
+    bytes_per_launch, achieved, frac, traffic, traffic_frac}. The dominant kernel is, among
+    the stages within 10% of the longest one (co-dominant), the one furthest below the HBM
+    peak in algorithmic bytes per second; every co-dominant stage and the whole step's
+    fraction are reported beside it."""
+    if not stages:
+        return None
+    longest = max(e["mean_ms"] for e in stages)
+    co_dominant = [e for e in stages if e["mean_ms"] >= 0.9 * longest]
+    p = min(co_dominant, key=lambda e: e["frac"])
+    t = step_ms * 1e-3
+    return {"bound": "hbm", "kernel": p["kernel"], "stage": p["stage"], "achieved": p["achieved"],
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": p["frac"], "traffic": p["traffic"],
+            "traffic_unit": "bytes per launch", "bytes_per_launch": p["bytes_per_launch"], "mean_ms": p["mean_ms"],
+            "co_dominant": co_dominant,
+            "step": {"bytes": step_bytes_, "ms": step_ms, "achieved": step_bytes_ / t / 1e9,
+                     "frac": step_bytes_ / t / 1e9 / HBM_PEAK_GBS}}
 
 
 def log(msg):
@@ -196,7 +235,11 @@ def main():
     idx = torch.empty(w.k, dtype=torch.int32, device=dev)
     vals = torch.empty(w.k, dtype=torch.float32, device=dev)
     layout = args.state_layout if args.state == "vector" else "worker_major"
+    torch.cuda.synchronize()
+    c_t0 = time.perf_counter()
     ctx = gs.GsContext(w.d, w.P, w.r, w.c, w.k, hp, rho=w.rho, state_layout=layout)
+    torch.cuda.synchronize()
+    create_ms = (time.perf_counter() - c_t0) * 1e3  # gs_create: scratch and the static tile lists
     u = torch.zeros(ctx.state_shape, dtype=torch.float32, device=dev)
     v = torch.zeros_like(u)
     if args.state == "sketch":
@@ -264,8 +307,16 @@ def main():
         stage_ms = {"interleave": stage_ms["accumulate"], "sketch": stage_ms["sketch"], "merge": stage_ms["merge"],
                     "select": stage_ms["select"], "state_update": stage_ms["gather_reset"]}
     sb = stage_bytes(w, args.state)
-    dom = max(stage_ms, key=lambda s_: stage_ms[s_]) if n_timed else "sketch"
-    achieved = sb[dom] / (stage_ms[dom] * 1e-3) / 1e9 if stage_ms[dom] > 0 else 0.0
+    kern = stage_kernels(w, layout)
+    stages = []
+    for st, st_ms in stage_ms.items():
+        if n_timed == 0 or st_ms <= 0 or sb.get(st, 0) <= 0:
+            continue
+        ach = sb[st] / (st_ms * 1e-3) / 1e9
+        tr = measured_traffic(w, st, layout) if args.state == "vector" else None
+        stages.append({"stage": st, "kernel": " + ".join(kern.get(st, [st])), "mean_ms": st_ms,
+                       "bytes_per_launch": sb[st], "achieved": ach, "frac": ach / HBM_PEAK_GBS, "traffic": tr,
+                       "traffic_frac": (tr / (st_ms * 1e-3) / 1e9 / HBM_PEAK_GBS) if tr else None})
     ctx.close()
     del u, v
 
@@ -304,13 +355,9 @@ def main():
     copy_gbs = 2 * src.numel() * 4 / (c0.elapsed_time(c1) / ncopy * 1e-3) / 1e9
     del dst
 
-    if args.state == "sketch":
-        # read g; write and read the P tables; merged written; U, E read and written; E read
-        # again for the estimates; idx and values written
-        B = 4 * w.P * w.d + 8 * w.P * w.r * w.c + 4 * w.r * w.c + 16 * w.r * w.c + 4 * w.r * w.c + 8 * w.k
-    else:
-        B = 20 * w.P * w.d + 8 * w.P * w.r * w.c + 8 * w.r * w.c + 12 * w.P * w.k + 8 * w.k
+    B = step_bytes(w, args.state)
     t = ms * 1e-3
+    roofline = roofline_of(stages, B, ms)
     out = {
         "metric": METRIC,
         "value": w.P * w.d / t,
@@ -339,10 +386,8 @@ def main():
         "wall_s_timed": wall,
         "stage_ms": stage_ms,
         "stage_ms_from": f"HIP events recorded between the stages of {n_timed} further steps after the timed region",
-        "roofline": {"bound": "hbm", "kernel": " + ".join(stage_kernels(w, layout).get(dom, [dom])), "stage": dom,
-                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": measured_traffic(w, dom, layout), "traffic_unit": "bytes per launch",
-                     "bytes_per_launch": sb[dom], "mean_ms": stage_ms[dom]},
+        "roofline": roofline,
+        "create_ms": create_ms,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

@@ -98,3 +98,27 @@ def test_cpu_baseline_runs_whole_steps_within_its_bounds():
     assert r["kind"] == "oracle" and r["cores"] == 1 and r["steps"] >= 1
     assert 0.2 <= r["seconds"] <= 5.0
     assert r["value"] == pytest.approx(r["steps"] * w.P * w.d / r["seconds"], rel=1e-2)
+
+
+def test_roofline_names_the_co_dominant_stage_furthest_below_peak():
+    # two stages within 10% of each other: the one with the lower algorithmic fraction is the
+    # dominant kernel, both are listed, and the step fraction is B / t / 8 TB/s
+    st = [
+        {"stage": "accumulate", "kernel": "a", "mean_ms": 0.66, "bytes_per_launch": 4.096e9, "achieved": 6206.0,
+         "frac": 0.776, "traffic": None, "traffic_frac": None},
+        {"stage": "sketch", "kernel": "p", "mean_ms": 0.645, "bytes_per_launch": 0.824e9, "achieved": 1277.0,
+         "frac": 0.160, "traffic": None, "traffic_frac": None},
+        {"stage": "select", "kernel": "s", "mean_ms": 0.14, "bytes_per_launch": 5.2e6, "achieved": 37.0,
+         "frac": 0.005, "traffic": None, "traffic_frac": None},
+    ]
+    r = bench.roofline_of(st, 4_000_000_000, 1.25)
+    assert r["stage"] == "sketch" and r["frac"] == 0.160
+    assert [e["stage"] for e in r["co_dominant"]] == ["accumulate", "sketch"]
+    assert abs(r["step"]["frac"] - 4e9 / 1.25e-3 / 1e9 / 8000.0) < 1e-12
+    assert bench.roofline_of([], 1, 1.0) is None
+
+
+def test_step_bytes_leave_out_the_tables_the_fused_step_never_writes():
+    w = synth.WORKLOADS["laplace53-d25.6M-P8"]
+    assert bench.step_bytes(w) == 20 * w.P * w.d + 8 * w.r * w.c + 12 * w.P * w.k + 8 * w.k
+    assert bench.stage_bytes(w)["merge"] == 0
