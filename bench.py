@@ -122,13 +122,17 @@ def kernel_source_file(name: str):
 def stage_kernels(w, layout: str = "interleaved") -> dict:
     """The kernels each stage of the fused step launches (names as rocprofv3 reports them)."""
     acc = [f"k_accumulate_il<{w.P // 4}>"] if layout == "interleaved" else [f"k_vi_il<{w.P}, true>"]
+    tail = ["k_digit2", "k_select2", "k_finalize", "k_emit_count", "k_emit_write"]
+    if w.d * w.r > 2_000_000:  # pruned selection (the library's choice above 2,000,000 cells of d*r)
+        select = [f"k_sample<{w.r}, false>", "k_heavy", f"k_pruned<{w.r}, false, 0>", f"k_survivors<{w.r}, false>",
+                  f"k_unsketch<{w.r}>"] + tail
+    else:  # every coordinate estimated
+        select = [f"k_unsketch<{w.r}>"] + tail
     return {
         "accumulate": acc,
         "sketch": [f"k_pull<{w.P}, {4 if w.P <= 4 else 6}, true>"],  # packed lists (the library's choice here)
         "merge": [f"k_merge_partials<{w.P}>"],
-        "select": [f"k_sample<{w.r}, false>", "k_heavy", f"k_pruned<{w.r}, false, 0>",
-                   f"k_survivors<{w.r}, false>", f"k_unsketch<{w.r}>", "k_digit2", "k_select2", "k_finalize",
-                   "k_emit_count", "k_emit_write"],
+        "select": select,
         "gather_reset": [f"k_gather_reset<{w.P}>"],
     }
 
