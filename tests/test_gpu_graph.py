@@ -2,7 +2,7 @@
 allocates, synchronizes or clears memory with a memset node, so every replay must equal the
 same step run eagerly. Replays are interleaved with unrelated eager work and host
 synchronizations, and each is checked. Covered: gs_step (both state layouts),
-gs_step_heavymix and gs_step_sketch_momentum."""
+gs_step_heavymix, gs_step_sketch_momentum and gs_unsketch_topk_static."""
 import numpy as np
 import pytest
 import torch
@@ -95,4 +95,42 @@ def test_graph_replays_equal_eager_steps(name, entry, layout):
             assert torch.equal(got[k], ref[t][k]), f"{entry}/{layout} replay {t}: {k} differs from the eager step"
     del graph
     ctx.close()
+    assert np.isfinite(noise.sum().item())
+
+
+def test_graph_replays_of_the_static_selection():
+    # gs_unsketch_topk_static (no context, no allocation) captured once, after its first call
+    # on the device looked up the scratch array, and replayed on new sketches: every replay
+    # equals the eager call on the same sketch
+    d, r, c, k = 270_000, 5, 27_000, 2_700
+    hp = synth.hash_params(synth.BASE_SEED + 55, r)
+    rng = np.random.default_rng(55)
+    tables = [torch.from_numpy((np.round(rng.laplace(0.0, 1.0, (r, c)) * 64.0) / 64.0).astype(np.float32))
+              for _ in range(STEPS)]
+    m = torch.empty((r, c), dtype=torch.float32, device=DEV)
+    est = torch.empty(d, dtype=torch.float32, device=DEV)
+    idx = torch.empty(k, dtype=torch.int32, device=DEV)
+    ref = []
+    for t in range(STEPS):
+        m.copy_(tables[t])
+        gs.gs_unsketch_topk_static(d, r, c, hp, m, k, est, idx)
+        torch.cuda.synchronize()
+        ref.append((est.clone(), idx.clone()))
+    m.copy_(tables[0])
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        gs.gs_unsketch_topk_static(d, r, c, hp, m, k, est, idx)
+    torch.cuda.synchronize()
+    noise = torch.empty(1 << 20, dtype=torch.float32, device=DEV)
+    for t in range(STEPS):
+        m.copy_(tables[t])
+        noise.normal_()
+        gs.gs_unsketch_topk_static(1000, 3, 97, synth.hash_params(synth.BASE_SEED + 56, 3), m[:3, :97].contiguous(),
+                                   10, None, torch.empty(10, dtype=torch.int32, device=DEV))  # other eager use
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(est, ref[t][0]) and torch.equal(idx, ref[t][1]), f"static selection replay {t}"
+    del graph
     assert np.isfinite(noise.sum().item())
