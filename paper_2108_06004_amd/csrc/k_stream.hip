@@ -24,11 +24,38 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
+// Each wave takes U = 4 consecutive chunks of 64 quads (4 KB of each array) per pass, all
+// its loads in flight together, and every load and store is non-temporal (the streams are
+// read and written once): as the interleaved accumulation, which these settings brought to
+// the part's stream rate; the quads past the last whole group go one per lane.
 __global__ void __launch_bounds__(kBlock) k_accumulate4(const f4* __restrict__ g, f4* __restrict__ u,
                                                         f4* __restrict__ v, int64_t n4, float rho) {
+  constexpr int U = 4;
+  const int lane = threadIdx.x & 63;
+  const int64_t ngr = n4 / (64 * U);
+  const int64_t wstride = (int64_t)gridDim.x * (kBlock / 64);
+  const int64_t w0 = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
+  for (int64_t gr = w0; gr < ngr; gr += wstride) {
+    f4 gg[U], uu[U], vv[U];
+#pragma unroll
+    for (int m = 0; m < U; ++m) {
+      const int64_t t = (gr * U + m) * 64 + lane;
+      gg[m] = __builtin_nontemporal_load(g + t);
+      uu[m] = __builtin_nontemporal_load(u + t);
+      vv[m] = __builtin_nontemporal_load(v + t);
+    }
+#pragma unroll
+    for (int m = 0; m < U; ++m) {
+      const int64_t t = (gr * U + m) * 64 + lane;
+      uu[m] = rho * uu[m] + gg[m];
+      vv[m] = vv[m] + uu[m];
+      __builtin_nontemporal_store(uu[m], u + t);
+      __builtin_nontemporal_store(vv[m], v + t);
+    }
+  }
   const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n4; t += stride) {
-    const f4 gg = __builtin_nontemporal_load(g + t);
+  for (int64_t t = ngr * U * 64 + (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n4; t += stride) {
+    const f4 gg = g[t];
     f4 uu = u[t], vv = v[t];
     uu = rho * uu + gg;
     vv = vv + uu;
@@ -314,9 +341,11 @@ hipError_t launch_accumulate(const gs_ctx* x, hipStream_t s, const float* g, flo
   if (aligned16(g) && aligned16(u) && aligned16(v)) {
     const int64_t n4 = n / 4;
     if (n4 > 0) {
-      hipLaunchKernelGGL(k_accumulate4, dim3(grid_for(n4, kBlock, 4 * x->num_cus * 2)), dim3(kBlock), 0, s,
-                         reinterpret_cast<const f4*>(g), reinterpret_cast<f4*>(u),
-                         reinterpret_cast<f4*>(v), n4, x->rho);
+      // one group of four 64-quad chunks per wave and pass, up to 64 workgroups per CU
+      const int64_t groups = n4 / (64 * 4);
+      const int blocks = grid_for(groups > 0 ? groups : 1, kBlock / 64, 64 * x->num_cus);
+      hipLaunchKernelGGL(k_accumulate4, dim3(blocks), dim3(kBlock), 0, s, reinterpret_cast<const f4*>(g),
+                         reinterpret_cast<f4*>(u), reinterpret_cast<f4*>(v), n4, x->rho);
     }
     if (4 * n4 < n) hipLaunchKernelGGL(k_accumulate1, dim3(1), dim3(kBlock), 0, s, g, u, v, 4 * n4, n, x->rho);
   } else {
