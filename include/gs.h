@@ -73,8 +73,8 @@ typedef enum gs_status {
  *   rho      momentum factor of the accumulation u <- rho*u + g (finite)
  *   reset_momentum  1: the reset after selection zeroes u as well as v; 0: only v
  *   hash_a, hash_b  HOST arrays [r]: bucket hash h_j(i) = ((a_j*i + b_j) mod p) mod c
- *   sign_a, sign_b  HOST arrays [r]: sign s_j(i) = +1 if ((a_j*i + b_j) mod p) is odd, else -1
- *                   with 1 <= a < p and 0 <= b < p for all four; copied by gs_create.
+ *   sign_a, sign_b  HOST arrays [r]: sign s_j(i) = +1 if ((sign_a_j*i + sign_b_j) mod p) is odd,
+ *                   else -1; 1 <= a < p and 0 <= b < p for all four arrays; copied by gs_create.
  *   state_layout    GS_STATE_WORKER_MAJOR (0) or GS_STATE_INTERLEAVED: the layout of u and v
  *                   in every call that takes them (gs_accumulate, gs_sketch's v,
  *                   gs_gather_reset, gs_step, gs_step_heavymix, gs_step_profiled). Other
