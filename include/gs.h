@@ -81,10 +81,12 @@ typedef enum gs_status {
  *                   values are GS_ERR_INVALID_ARG.
  *   options         0, or GS_OPT_ROW_COPY: reserve a worker-interleaved [d][PP] fp32 copy
  *                   (4 PP d bytes) in an interleaved-state context too. A worker-major context
- *                   always has it (its sketch gathers from it). An interleaved context needs it
- *                   only for gs_step_sketch_momentum (GS_ERR_UNSUPPORTED without it) and for
- *                   a v that is not 16-byte aligned (GS_ERR_INVALID_ARG without it; torch
- *                   allocations are aligned). Other bits are GS_ERR_INVALID_ARG.
+ *                   with P > 1 always has it (its sketch gathers from it); with P = 1 the
+ *                   state [1][d] is a plain vector that the sketch gathers directly. An
+ *                   interleaved context with P > 1 needs it only for gs_step_sketch_momentum
+ *                   (GS_ERR_UNSUPPORTED without it) and for a v that is not 16-byte aligned
+ *                   (GS_ERR_INVALID_ARG without it; torch allocations are aligned). Other
+ *                   bits are GS_ERR_INVALID_ARG.
  */
 typedef struct gs_config {
   int64_t d;
@@ -119,7 +121,7 @@ typedef struct gs_ctx gs_ctx; /* opaque: a copy of the config plus device scratc
  * either way).
  * Device scratch is about (16 + 4.1 r) d + 8 S P r c bytes (S list segments per tile, 1
  * unless the sketch is small), plus the 4 PP d bytes of the interleaved copy (PP = P rounded
- * up to 4) in a worker-major context or with GS_OPT_ROW_COPY, plus 2 r d bytes while the
+ * up to 4) in a worker-major context with P > 1 or with GS_OPT_ROW_COPY, plus 2 r d bytes while the
  * lists are built: with the interleaved state and no copy 1.0 GB at d = 25.6M, P = 8, r = 5,
  * c = 256,000 (1.8 GB worker-major) and 61 GB at d = 2^31 - 2, P = 2, r = 3 (95 GB
  * worker-major). The atomic form replaces the lists and the copy with 8 P r c bytes. */

@@ -226,9 +226,10 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
     chk(alloc(&x->bases, x->list_cap / gs::kListGroup));
     chk(alloc(&x->tile_off, (int64_t)x->plan.T + 1));
     chk(alloc(&x->tile_n, (int64_t)x->plan.T));
-    // the interleaved copy: the worker-major state's sketch gathers from it; an interleaved
-    // context gathers the caller's v and needs the copy only on request (GS_OPT_ROW_COPY)
-    if (x->state_layout == GS_STATE_WORKER_MAJOR || (cfg->options & GS_OPT_ROW_COPY))
+    // the interleaved copy: the worker-major state's sketch gathers from it (with more than
+    // one worker: one worker's state is a plain vector the pull gathers directly); an
+    // interleaved context gathers the caller's v and needs the copy only on request
+    if ((x->state_layout == GS_STATE_WORKER_MAJOR && x->P > 1) || (cfg->options & GS_OPT_ROW_COPY))
       chk(alloc(&x->vI, x->d * x->plan.PP));
     chk(alloc(&x->partial, (int64_t)x->plan.S * x->r * x->c * x->P));
   } else {
@@ -281,7 +282,10 @@ gs_status gs_sketch(gs_ctx* x, void* stream, const float* v, float* tables) {
   if (unaligned_without_copy(x, v)) return fail(x, GS_ERR_INVALID_ARG, std::string("gs_sketch") + kUnalignedMsg);
   hipStream_t s = as_stream(stream);
   hipError_t e;
-  if (x->use_pull) {
+  if (x->use_pull && gs::flat_state(x)) {
+    e = gs::launch_pull_flat(x, s, v, nullptr, tables);
+    if (e == hipSuccess) e = gs::launch_merge_partials(x, s, nullptr, tables);
+  } else if (x->use_pull) {
     const float* rows = x->vI;
     if (x->state_layout == GS_STATE_INTERLEAVED)
       rows = gs::pull_rows_of_state(x, s, v, &e);
@@ -330,15 +334,19 @@ static hipError_t launch_sketch_phase(gs_ctx* x, hipStream_t s, const float* g, 
   mark(0);
   if (x->use_pull) {
     const float* rows = x->vI;
+    const bool flat = gs::flat_state(x);
     if (x->state_layout == GS_STATE_INTERLEAVED) {
       // the caller's v rows are what the pull gathers: no interleaved copy
       e = gs::launch_accumulate(x, s, g, u, v);
       if (e == hipSuccess) rows = gs::pull_rows_of_state(x, s, v, &e);
+    } else if (flat) {
+      e = gs::launch_accumulate(x, s, g, u, v);  // one worker: v itself is gathered
     } else {
       e = gs::launch_accumulate_vi(x, s, g, u, v);
     }
     mark(1);
-    if (e == hipSuccess) e = gs::launch_pull(x, s, rows, merged, nullptr);
+    if (e == hipSuccess) e = flat ? gs::launch_pull_flat(x, s, v, merged, nullptr)
+                                  : gs::launch_pull(x, s, rows, merged, nullptr);
     mark(2);
     if (e == hipSuccess) e = gs::launch_merge_partials(x, s, merged, nullptr);
   } else {
@@ -410,13 +418,18 @@ gs_status gs_step_sketch_momentum(gs_ctx* x, void* stream, const float* g, float
     return fail(x, GS_ERR_INVALID_ARG, "gs_step_sketch_momentum: NULL array");
   if (k < 1 || k > x->k_max)
     return fail(x, GS_ERR_INVALID_ARG, "gs_step_sketch_momentum: k must satisfy 1 <= k <= k_max");
-  if (x->use_pull && x->vI == nullptr)
+  if (x->use_pull && x->P > 1 && x->vI == nullptr)
     return fail(x, GS_ERR_UNSUPPORTED,
                 "gs_step_sketch_momentum: an interleaved-state context needs the row copy (GS_OPT_ROW_COPY)");
   hipStream_t s = as_stream(stream);
   hipError_t e;
   gs::stage_mark(x, s, 0);
-  if (x->use_pull) {
+  if (x->use_pull && x->P == 1) {  // one worker's gradient [1][d] is a plain vector: gathered directly
+    gs::stage_mark(x, s, 1);
+    e = gs::launch_pull_flat(x, s, g, merged, nullptr);
+    gs::stage_mark(x, s, 2);
+    if (e == hipSuccess) e = gs::launch_merge_partials(x, s, merged, nullptr);
+  } else if (x->use_pull) {
     e = gs::launch_interleave(x, s, g);
     gs::stage_mark(x, s, 1);
     if (e == hipSuccess) e = gs::launch_pull(x, s, x->vI, merged, nullptr);

@@ -209,6 +209,11 @@ hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v);
 // merged sketch (non-null outputs) and launch_merge_partials has nothing left to do; pass
 // the same outputs to both.
 hipError_t launch_pull(const gs_ctx* x, hipStream_t s, const float* rows, float* merged, float* tables);
+// One worker (P = 1): the pull gathers the plain vector v[d] (4 bytes per coordinate), with
+// no interleaved copy; the worker-major state of one worker is such a vector.
+hipError_t launch_pull_flat(const gs_ctx* x, hipStream_t s, const float* v, float* merged, float* tables);
+// A worker-major state with one worker is gathered directly (no interleaved copy).
+inline bool flat_state(const gs_ctx* x) { return x->P == 1 && x->state_layout == GS_STATE_WORKER_MAJOR; }
 bool pull_merges(const gs_ctx* x);
 // Rows for the pull from the caller's state array v (GS_STATE_INTERLEAVED): v itself when it
 // is 16-byte aligned, otherwise a copy enqueued into x->vI.

@@ -30,6 +30,9 @@ constexpr int kBlock = 256;
 // takes an entry, P <= 4; 6 otherwise).
 constexpr int kPullBlock = 512;
 constexpr int pull_unroll(int P) { return P <= 4 ? 4 : 6; }
+// Whether a pass fetches the next pass's list words while its own rows are in flight (see
+// k_pull): the one-worker plain-vector gather and four lanes per entry (P >= 13).
+constexpr bool pull_pipelined(int P, bool flat) { return flat || P >= 13; }
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 int grid_for(int64_t work_items, int per_block, int cap) {
@@ -395,7 +398,24 @@ __device__ __forceinline__ void segment_bounds(int64_t lo, int64_t n, int64_t s,
   e1 = s + 1 == S ? lo + n : lo + (n * (s + 1) / S) / g * g;
 }
 
-template <int P, int U, bool PK>
+// Workers 4 sub .. 4 sub + 3 of coordinate i: one 16-byte load of an interleaved row (rows of
+// PP floats, 16-byte aligned), or, with FLAT (one worker: the state [1][d] is a plain vector),
+// the coordinate's one value.
+template <int P, bool FLAT>
+__device__ __forceinline__ f4 load_quad(const float* __restrict__ v, uint32_t i, int sub) {
+  constexpr int PP = (P + 3) & ~3;
+  if constexpr (FLAT) {
+    static_assert(P == 1, "a flat state holds one worker");
+    f4 x;
+    x.x = v[i];
+    x.y = x.z = x.w = 0.f;
+    return x;
+  } else {
+    return reinterpret_cast<const f4*>(v + (int64_t)i * PP)[sub];
+  }
+}
+
+template <int P, int U, bool PK, bool FLAT>
 __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, const uint32_t* __restrict__ list,
                                                      const uint16_t* __restrict__ codes,
                                                      const uint32_t* __restrict__ bases,
@@ -428,28 +448,63 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   // when L does not divide the block (L = 3: 85 groups of 3 lanes), the last lane has no
   // group: it takes no entry (its would be the next pass's first)
   int64_t eb = tid0 < B ? e0 + tid : e1;
-  for (; eb + (U - 1) * B < e1; eb += U * B) {
-    uint32_t i[U], pos[U], sg[U];
+  // The list words of a pass's U entries (and their group bases). Pipelined (PIPE), a pass
+  // fetches the next pass's words while its own rows are in flight, so it waits on one memory
+  // round trip (the rows), not two (words, then rows): measured faster where a pass moves
+  // little (one worker's 4-byte values: 0.39 -> 0.30 ms at d = 25.6M) or where the miss
+  // latency is long (66M x 16: 6.10 -> 5.71 ms), slower at 25.6M x 8 (0.66 -> 0.73 ms).
+  constexpr bool PIPE = pull_pipelined(P, FLAT);
+  uint32_t wn[U], an[U];
+  auto fetch = [&](int64_t ebx) {
 #pragma unroll
     for (int m = 0; m < U; ++m) {
-      const int64_t e = eb + m * B;
-      const uint32_t w = list[e];
-      uint32_t aux;
+      const int64_t e = ebx + m * B;
+      wn[m] = list[e];
       if constexpr (PK && (L == 1 || L == 2 || L == 4)) {
         static_assert(B % kListGroup == 0 && kListGroup % (64 / L) == 0, "a wave's entries must share a group");
         // e0 is group-aligned, B is a multiple of kListGroup and a wave's lanes take 64 / L
         // consecutive entries of an aligned run (permuted within it): every lane active in
         // this pass needs the same group base, so the wave loads it once, as a scalar. The
         // tail loop below cannot do this (its lanes may be one pass apart).
-        aux = bases[__builtin_amdgcn_readfirstlane((uint32_t)(e / kListGroup))];
+        an[m] = bases[__builtin_amdgcn_readfirstlane((uint32_t)(e / kListGroup))];
       } else {
-        aux = PK ? bases[e / kListGroup] : (uint32_t)codes[e];
+        an[m] = PK ? bases[e / kListGroup] : (uint32_t)codes[e];
       }
-      decode_entry<PK>(w, aux, pl.off_bits, i[m], pos[m], sg[m]);
     }
+  };
+  if (PIPE && eb + (U - 1) * B < e1) {
+    fetch(eb);
+    for (;;) {
+      uint32_t i[U], pos[U], sg[U];
+#pragma unroll
+      for (int m = 0; m < U; ++m) decode_entry<PK>(wn[m], an[m], pl.off_bits, i[m], pos[m], sg[m]);
+      f4 x[U];
+#pragma unroll
+      for (int m = 0; m < U; ++m) x[m] = load_quad<P, FLAT>(vI, i[m], sub);
+      const int64_t ebn = eb + U * B;
+      const bool more = ebn + (U - 1) * B < e1;
+      if (more) fetch(ebn);
+#pragma unroll
+      for (int m = 0; m < U; ++m) {
+        double* cell = mycol + pos[m];
+        const uint32_t sflip = sg[m];
+        const float xs[4] = {x[m].x, x[m].y, x[m].z, x[m].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (P % 4 == 0 || 4 * sub + q < P) atomicAdd(cell + q * wt, (double)apply_sign(xs[q], sflip));
+      }
+      eb = ebn;
+      if (!more) break;
+    }
+  }
+  for (; !PIPE && eb + (U - 1) * B < e1; eb += U * B) {
+    fetch(eb);
+    uint32_t i[U], pos[U], sg[U];
+#pragma unroll
+    for (int m = 0; m < U; ++m) decode_entry<PK>(wn[m], an[m], pl.off_bits, i[m], pos[m], sg[m]);
     f4 x[U];
 #pragma unroll
-    for (int m = 0; m < U; ++m) x[m] = reinterpret_cast<const f4*>(vI + (int64_t)i[m] * PP)[sub];
+    for (int m = 0; m < U; ++m) x[m] = load_quad<P, FLAT>(vI, i[m], sub);
 #pragma unroll
     for (int m = 0; m < U; ++m) {
       double* cell = mycol + pos[m];
@@ -463,7 +518,7 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   for (; eb < e1; eb += B) {
     uint32_t i, pos, sflip;
     decode_entry<PK>(list[eb], PK ? bases[eb / kListGroup] : (uint32_t)codes[eb], pl.off_bits, i, pos, sflip);
-    const f4 x = reinterpret_cast<const f4*>(vI + (int64_t)i * PP)[sub];
+    const f4 x = load_quad<P, FLAT>(vI, i, sub);
     double* cell = mycol + pos;
     const float xs[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
@@ -608,25 +663,25 @@ hipError_t launch_vi_il_p(const gs_ctx* x, hipStream_t s, const float* g, float*
   return hipGetLastError();
 }
 
-template <int P>
+template <int P, bool FLAT = false>
 void launch_pull_p(const gs_ctx* x, hipStream_t s, const float* rows, float* merged, float* tables) {
   const PullPlan& pl = x->plan;
   const dim3 grid((unsigned)((int64_t)pl.T * pl.S)), block(kPullBlock);
   const size_t lds = (size_t)pl.W * pl.P * sizeof(double);
   if (pl.packed)
-    hipLaunchKernelGGL((k_pull<P, pull_unroll(P), true>), grid, block, lds, s, x->hs, pl, x->list, x->codes, x->bases,
-                       x->tile_off, x->tile_n, rows, x->partial, merged, tables);
+    hipLaunchKernelGGL((k_pull<P, pull_unroll(P), true, FLAT>), grid, block, lds, s, x->hs, pl, x->list, x->codes,
+                       x->bases, x->tile_off, x->tile_n, rows, x->partial, merged, tables);
   else
-    hipLaunchKernelGGL((k_pull<P, pull_unroll(P), false>), grid, block, lds, s, x->hs, pl, x->list, x->codes,
+    hipLaunchKernelGGL((k_pull<P, pull_unroll(P), false, FLAT>), grid, block, lds, s, x->hs, pl, x->list, x->codes,
                        x->bases, x->tile_off, x->tile_n, rows, x->partial, merged, tables);
 }
 
-template <int P>
+template <int P, bool FLAT = false>
 hipError_t allow_pull_lds(size_t bytes) {
-  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull<P, pull_unroll(P), true>),
+  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull<P, pull_unroll(P), true, FLAT>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
   if (e != hipSuccess) return e;
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull<P, pull_unroll(P), false>),
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_pull<P, pull_unroll(P), false, FLAT>),
                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
 }
 
@@ -765,7 +820,12 @@ hipError_t prepare_pull_kernels(const gs_ctx* x) {
   switch (x->P) {
 #define GS_ALLOW_CASE(PP) \
   case PP: return allow_pull_lds<PP>(bytes);
-    GS_ALLOW_CASE(1) GS_ALLOW_CASE(2) GS_ALLOW_CASE(3) GS_ALLOW_CASE(4) GS_ALLOW_CASE(5) GS_ALLOW_CASE(6)
+    case 1: {
+      const hipError_t e = allow_pull_lds<1, true>(bytes);
+      if (e != hipSuccess) return e;
+      return allow_pull_lds<1>(bytes);
+    }
+    GS_ALLOW_CASE(2) GS_ALLOW_CASE(3) GS_ALLOW_CASE(4) GS_ALLOW_CASE(5) GS_ALLOW_CASE(6)
     GS_ALLOW_CASE(7) GS_ALLOW_CASE(8) GS_ALLOW_CASE(9) GS_ALLOW_CASE(10) GS_ALLOW_CASE(11) GS_ALLOW_CASE(12)
     GS_ALLOW_CASE(13) GS_ALLOW_CASE(14) GS_ALLOW_CASE(15) GS_ALLOW_CASE(16)
 #undef GS_ALLOW_CASE
@@ -858,6 +918,12 @@ hipError_t launch_interleave(const gs_ctx* x, hipStream_t s, const float* v) {
   const int64_t n = (int64_t)x->P * x->d;
   hipLaunchKernelGGL(k_accumulate_vi_any, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, nullptr,
                      nullptr, src, x->vI, x->d, x->P, x->plan.PP, x->rho, 0, (int64_t)0);
+  return hipGetLastError();
+}
+
+hipError_t launch_pull_flat(const gs_ctx* x, hipStream_t s, const float* v, float* merged, float* tables) {
+  if (x->P != 1) return hipErrorInvalidValue;
+  launch_pull_p<1, true>(x, s, v, merged, tables);
   return hipGetLastError();
 }
 

@@ -587,3 +587,37 @@ def test_sketch_exact_on_integer_state(layout, d, P, r, c):
     dv.ctx.sketch(dv.state(v), tables)
     assert np.array_equal(host(tables), par_oracle.sketch(v, hp, c)), "tables of an integer state not exact"
     dv.close()
+
+
+def test_one_worker_state_gathered_in_place_at_any_alignment():
+    # one worker: the worker-major state [1][d] is a plain vector, gathered by the sketch with
+    # 4-byte loads and no interleaved copy, so views starting one float into their buffers
+    # work for the fused step and gs_sketch alike
+    d, P, r, c, k = 300_007, 1, 5, 30_011, 400
+    hp = synth.hash_params(synth.BASE_SEED + 67, r)
+    rng = np.random.default_rng(67)
+    g = rng.laplace(0, 1e-2, (P, d)).astype(np.float32)
+    u0 = rng.standard_normal((P, d)).astype(np.float32)
+    v0 = rng.standard_normal((P, d)).astype(np.float32)
+    dv = Dev(d, P, r, c, k, hp, 0.9)
+    bufs = [torch.zeros(d + 1, dtype=torch.float32, device=DEV) for _ in range(3)]
+    gv, uv, vv = (b_[1:] for b_ in bufs)
+    gv.copy_(to_dev(g).reshape(-1))
+    uv.copy_(to_dev(u0).reshape(-1))
+    vv.copy_(to_dev(v0).reshape(-1))
+    dv.ctx.step(gv, uv, vv, k, dv.merged, dv.idx, dv.values)
+    u1, v1 = u0.copy(), v0.copy()
+    ref = oracle.step(g, u1, v1, hp, c, k, rho=0.9)
+    assert_tol(host(dv.merged), ref["merged"], "one worker: merged sketch")
+    jf = host(dv.idx)
+    kth = float(oracle.topk(ref["est"], k)[1])
+    assert_tie_band(jf, ref["idx"], lambda s_: ref["est"][s_], kth, "one worker: selection")
+    uc, vc = u0.copy(), v0.copy()
+    oracle.accumulate(g, uc, vc, 0.9)
+    assert np.array_equal(host(dv.values), oracle.gather_reset(jf, uc, vc, True)), "one worker: values"
+    assert np.array_equal(host(uv).reshape(P, d), uc) and np.array_equal(host(vv).reshape(P, d), vc)
+    # gs_sketch on a misaligned v: the per-worker table
+    tables = torch.empty((P, r, c), dtype=torch.float32, device=DEV)
+    dv.ctx.sketch(vv, tables)
+    assert_tol(host(tables), par_oracle.sketch(vc, hp, c), "one worker: table of a misaligned v")
+    dv.close()

@@ -105,6 +105,7 @@ EDGE = [
     (10_007, 7, 7, 211, 500, False),  # momentum kept
     (3001, 17, 5, 97, 60, True),     # P beyond the unrolled instances
     (65_536, 2, 16, 4096, 655, True),  # maximum r
+    (200_003, 1, 5, 20_011, 300, True),  # one worker: its gradient vector is gathered directly
 ]
 
 
@@ -149,4 +150,19 @@ def test_sketch_state_atomic_sketch_path(monkeypatch):
     for t in range(3):
         g = rng.standard_normal((P, d)).astype(np.float32)
         U, E = state_step(ctx, g, U, E, hp, k, 0.9, True, f"atomic sketch state t={t}")
+    ctx.close()
+
+
+def test_sketch_state_one_worker_interleaved_context():
+    # with one worker the gradient [1][d] is a plain vector the pull gathers, so an
+    # interleaved-state context runs the sketch-space step without the row copy
+    d, P, r, c, k = 100_003, 1, 5, 10_007, 200
+    hp = synth.hash_params(synth.BASE_SEED + 61, r)
+    rng = np.random.default_rng(61)
+    ctx = gs.GsContext(d, P, r, c, k, hp, rho=0.9, state_layout="interleaved")
+    U = np.zeros((r, c), np.float32)
+    E = np.zeros((r, c), np.float32)
+    for t in range(2):
+        g = rng.laplace(0, 1e-2, (P, d)).astype(np.float32)
+        U, E = state_step(ctx, g, U, E, hp, k, 0.9, True, f"one worker interleaved t={t}")
     ctx.close()
