@@ -121,7 +121,12 @@ def kernel_source_file(name: str):
 
 def stage_kernels(w, layout: str = "interleaved") -> dict:
     """The kernels each stage of the fused step launches (names as rocprofv3 reports them)."""
-    acc = [f"k_accumulate_il<{w.P // 4}>"] if layout == "interleaved" else [f"k_vi_il<{w.P}, true>"]
+    if layout == "interleaved":
+        acc = [f"k_accumulate_il<{w.P // 4}>"]
+    elif w.P == 1:
+        acc = ["k_accumulate4"]
+    else:
+        acc = [f"k_vi_il<{w.P}, true>"]
     tail = ["k_digit2", "k_select2", "k_finalize", "k_emit_count", "k_emit_write"]
     if w.d * w.r > 2_000_000:  # pruned selection (the library's choice above 2,000,000 cells of d*r)
         select = [f"k_sample<{w.r}, false>", "k_heavy", f"k_pruned<{w.r}, false, 0>", f"k_survivors<{w.r}, false>",
@@ -130,7 +135,10 @@ def stage_kernels(w, layout: str = "interleaved") -> dict:
         select = [f"k_unsketch<{w.r}>"] + tail
     return {
         "accumulate": acc,
-        "sketch": [f"k_pull<{w.P}, {4 if w.P <= 4 else 6}, true>"],  # packed lists (the library's choice here)
+        # packed lists (the library's choice here); one worker in the worker-major layout: its
+        # plain state vector gathered directly (the last template argument)
+        "sketch": [f"k_pull<{w.P}, {4 if w.P <= 4 else 6}, true, "
+                   f"{'true' if w.P == 1 and layout == 'worker_major' else 'false'}>"],
         "merge": [f"k_merge_partials<{w.P}>"],
         "select": select,
         "gather_reset": [f"k_gather_reset<{w.P}>"],
