@@ -127,7 +127,7 @@ def stage_kernels(w, layout: str = "interleaved") -> dict:
         acc = ["k_accumulate4"]
     else:
         acc = [f"k_vi_il<{w.P}, true>"]
-    tail = ["k_digit2", "k_select2", "k_finalize", "k_emit_count", "k_emit_write"]
+    tail = ["k_digit2", "k_select2", "k_mark", "k_emit"]
     if w.d * w.r > 2_000_000:  # pruned selection (the library's choice above 2,000,000 cells of d*r)
         select = [f"k_sample<{w.r}, false>", "k_heavy", f"k_pruned<{w.r}, false, 0>", f"k_survivors<{w.r}, false>",
                   f"k_unsketch<{w.r}>"] + tail

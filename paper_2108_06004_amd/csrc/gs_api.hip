@@ -37,7 +37,7 @@ hipError_t alloc(T** p, int64_t count) {
 
 void free_scratch(gs_ctx* x) {
   void* ptrs[] = {x->keys,     x->hist,     x->hist2,       x->hist_s, x->hist_c, x->ctl,     x->stage_idx,
-                  x->cand_key, x->cand_idx, x->bitmap,      x->blockcnt, x->acc64, x->list,  x->codes,
+                  x->cand_key, x->cand_idx, x->bitmap,      x->emit_flags, x->acc64, x->list,  x->codes,
                   x->bases,    x->tile_off, x->tile_n,      x->vI,     x->partial, x->sample_keys,
                   x->heavy,    x->l2buf,    x->coarse};
   for (void* p : ptrs)
@@ -52,7 +52,7 @@ void free_scratch(gs_ctx* x) {
   x->cand_key = nullptr;
   x->cand_idx = nullptr;
   x->bitmap = nullptr;
-  x->blockcnt = nullptr;
+  x->emit_flags = nullptr;
   x->acc64 = nullptr;
   x->list = nullptr;
   x->codes = nullptr;
@@ -197,9 +197,10 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   chk(alloc(&x->cand_key, x->cand_cap));
   chk(alloc(&x->cand_idx, x->cand_cap));
   chk(alloc(&x->bitmap, words));
-  chk(alloc(&x->blockcnt, x->emit_blocks));
+  chk(alloc(&x->emit_flags, x->emit_blocks));
   chk(alloc(&x->sample_keys, gs::kSampleMax));
-  chk(alloc(&x->heavy, ((int64_t)x->r * x->c + 63) / 64 * 2));
+  x->heavy_row = (x->c + 63) / 64 * 64;
+  chk(alloc(&x->heavy, (int64_t)x->r * x->heavy_row / 32));
   {
     const int64_t npad = gs::l2_pad(x->c);
     x->l2_half = (int64_t)x->r * (npad > 2048 ? npad / 2048 : 1);

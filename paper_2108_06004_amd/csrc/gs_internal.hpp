@@ -30,6 +30,8 @@ struct SelectCtl {
   double theta;         // HEAVYMIX: heavy threshold l2sq / k
   unsigned long long n_heavy;  // HEAVYMIX: |H|
   uint32_t n_stage2;    // keys of the digit-1 bucket b1 staged for the digit-3 pass
+  uint32_t n_staged;    // n_stage2 as k_select2 found it, for the emit (n_stage2 is reset there)
+  uint32_t emit_ticket; // order in which the emit's workgroups start (their look-back order)
 };
 // Buffers of the dense selection (every coordinate a candidate) and of its radix tail: the
 // context's scratch for gs_unsketch_topk and friends, or the static scratch of
@@ -45,7 +47,7 @@ struct SelectBufs {
   uint32_t* hist_c;     // [kDigit1Bins] digit-1 histogram of pruned candidates
   SelectCtl* ctl;
   uint32_t* bitmap;     // [ceil(d/32)] output bitmap
-  uint32_t* blockcnt;   // [emit_blocks]
+  unsigned long long* emit_flags;  // [emit_blocks] look-back words of the emit (zero before it)
   int64_t emit_blocks;
 };
 constexpr int kSampleMax = 16384;  // sampled estimates for the pruning bound
@@ -117,16 +119,16 @@ struct gs_ctx {
   int32_t* cand_idx = nullptr;    // [cand_cap]
   int64_t cand_cap = 0;
   uint32_t* bitmap = nullptr;     // [ceil(d/32)]
-  uint32_t* blockcnt = nullptr;   // [emit blocks]
+  unsigned long long* emit_flags = nullptr;  // [emit blocks] look-back words of the emit
   uint32_t* sample_keys = nullptr;  // [kSampleMax]
-  uint32_t* heavy = nullptr;        // [ceil(r*c/64)*2] heavy-cell bitmap
+  uint32_t* heavy = nullptr;        // [r * heavy_row / 32] heavy-cell bitmap, rows padded to heavy_row bits
+  int64_t heavy_row = 0;            // c rounded up to a multiple of 64: bit j * heavy_row + col is cell (j, col)
   int64_t prune_map_words = 0;      // words of the heavy bitmap
   int prune_map_in_lds = 0;         // 1: the pruned pass keeps a bitmap in LDS (fine, or coarse below)
   int prune_coarse_log2 = 0;        // > 0: LDS holds the coarse map, one bit per 2^this cells
   uint32_t* coarse = nullptr;       // coarse heavy-cell map (bit = OR of its cells' heavy bits)
   int64_t prune_coarse_words = 0;
   int prune_buf_cap = 0;            // LDS candidate buffer entries of the pruned pass
-  size_t prune_lds = 0;             // dynamic LDS bytes of the pruned pass
   int64_t emit_blocks = 0;
   // selections without an estimate vector prune when d*r exceeds this (0: always); below it
   // the full estimate takes fewer launches than the pruned pass's chain
@@ -164,7 +166,7 @@ inline StateView state_view(const gs_ctx* x) {
 inline StateView worker_major_view(const gs_ctx* x) { return StateView{x->d, 1}; }
 inline SelectBufs select_bufs(const gs_ctx* x) {
   return SelectBufs{x->cand_key, x->cand_idx, x->cand_cap, x->keys,   x->stage_idx, x->hist,
-                    x->hist2,    x->hist_c,   x->ctl,      x->bitmap, x->blockcnt,  x->emit_blocks};
+                    x->hist2,    x->hist_c,   x->ctl,      x->bitmap, x->emit_flags, x->emit_blocks};
 }
 
 constexpr int kStageMarks = 6;  // events per timed step: before stage 0, after stages 0..4

@@ -17,17 +17,17 @@ constexpr int64_t kMaxD = GS_STATIC_MAX_D;
 constexpr int64_t kAlignWords = 64;  // 256-byte alignment of every region
 constexpr int64_t up(int64_t n) { return (n + kAlignWords - 1) / kAlignWords * kAlignWords; }
 constexpr int64_t kCtlWords = up((int64_t)((sizeof(gs::SelectCtl) + 3) / 4));
-constexpr int64_t kBlockCntWords = 64;  // emit blocks of kMaxD coordinates: 32 (checked at set-up)
+constexpr int64_t kFlagWords = 64;  // look-back words of the emit, 2 per emit block: 32 at kMaxD (checked per call)
 
 // Layout of the array in 32-bit words.
 constexpr int64_t kCandKey = 0;                            // [kMaxD] key of coordinate t
 constexpr int64_t kStageKey = kCandKey + up(kMaxD);        // [kMaxD] staged keys
 constexpr int64_t kStageIdx = kStageKey + up(kMaxD);       // [kMaxD] their coordinates
 constexpr int64_t kBitmap = kStageIdx + up(kMaxD);         // [kMaxD / 32] output bitmap
-constexpr int64_t kBlockCnt = kBitmap + up((kMaxD + 31) / 32);
+constexpr int64_t kFlags = kBitmap + up((kMaxD + 31) / 32);
 // Cleared at the start of every call (the selection needs them zero and leaves them zero,
 // but a call that was never completed, or one overlapping on another stream, may not have).
-constexpr int64_t kZero = kBlockCnt + kBlockCntWords;
+constexpr int64_t kZero = kFlags + kFlagWords;
 constexpr int64_t kHist = kZero;                           // [kDigit1Bins]
 constexpr int64_t kHist2 = kHist + gs::kDigit1Bins;        // [kDigitBins]
 constexpr int64_t kHistC = kHist2 + gs::kDigitBins;        // [kDigit1Bins] (not read: dense candidates)
@@ -116,7 +116,7 @@ extern "C" gs_status gs_unsketch_topk_static(const gs_config* cfg, void* stream,
   hipError_t e = scratch_of_current_device(&base, &num_cus);
   if (e != hipSuccess) return device_error("scratch set-up", e);
   const int64_t d = cfg->d;
-  if (gs::emit_blocks_for(d) > kBlockCntWords) return device_error("scratch layout", hipErrorInvalidValue);
+  if (2 * gs::emit_blocks_for(d) > kFlagWords) return device_error("scratch layout", hipErrorInvalidValue);
   const gs::SelectBufs bufs{base + kCandKey,
                             reinterpret_cast<int32_t*>(base + kStageIdx),  // candidates are dense: never read
                             d,
@@ -127,7 +127,7 @@ extern "C" gs_status gs_unsketch_topk_static(const gs_config* cfg, void* stream,
                             base + kHistC,
                             reinterpret_cast<gs::SelectCtl*>(base + kCtl),
                             base + kBitmap,
-                            base + kBlockCnt,
+                            reinterpret_cast<unsigned long long*>(base + kFlags),
                             gs::emit_blocks_for(d)};
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   e = gs::launch_fill_zero(s, reinterpret_cast<float*>(base + kZero), kZeroWords);  // a kernel, not a memset

@@ -12,14 +12,15 @@
 //      digit-1 histogram), or every coordinate, from the full estimate (k_unsketch /
 //      k_unsketch_hm), which also runs whenever the pruned candidates fall short of k;
 //   2. k_digit2 (many blocks): each block finds the digit-1 bucket (bits 31..20) of the
-//      k-th key in the candidates' histogram; digit 2 (bits 19..10) of that bucket's keys,
-//      and the bucket compacted (keys and coordinates);
+//      k-th key in the candidates' histogram; candidates in higher buckets are all taken and
+//      set their bit in the output bitmap; digit 2 (bits 19..10) of the bucket's keys, and
+//      the bucket compacted (keys and coordinates);
 //   3. k_select2 (one block): digit 3 (bits 9..0) of the bucket gives the k-th key tau and
 //      how many keys equal to tau are taken; if not all of them, the largest coordinate iota
 //      taken among them (lowest coordinates win), by rank or by three index digits;
-//   4. k_finalize: candidates with key > tau, or key == tau and index <= iota, set their bit;
-//   5. emit: the bitmap is turned into ascending indices (per-block popcounts, then a
-//      block-local scan offset by the preceding blocks' totals).
+//   4. k_mark: the bucket's keys > tau, or == tau with index <= iota, set their bit;
+//   5. k_emit: the bitmap is turned into ascending indices in one pass (each block counts
+//      its words and takes its offset from the blocks before it by a decoupled look-back).
 #include <algorithm>
 #include <cmath>
 #include <type_traits>
@@ -201,7 +202,7 @@ __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ 
                                                    const uint32_t* __restrict__ hist_c,
                                                    const uint32_t* __restrict__ hist, int pruned, uint32_t k,
                                                    uint32_t* __restrict__ hist2, uint32_t* __restrict__ stage_key,
-                                                   int32_t* __restrict__ stage_idx) {
+                                                   int32_t* __restrict__ stage_idx, uint32_t* __restrict__ bitmap) {
   __shared__ uint32_t h[kDigitBins];
   __shared__ uint32_t bkey[kStageBuf];
   __shared__ int32_t bidx[kStageBuf];
@@ -233,7 +234,12 @@ __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ 
 #pragma unroll
     for (int m = 0; m < V; ++m) {
       const int64_t t = c0 + (int64_t)m * kBlock + threadIdx.x;
-      const bool take = t < hi && (key[m] >> kDigit1Shift) == b1;
+      const uint32_t d1 = key[m] >> kDigit1Shift;
+      if (t < hi && d1 > b1) {  // above the k-th key's bucket: taken
+        const uint32_t ix = dense ? (uint32_t)t : (uint32_t)cand_idx[t];
+        atomicOr(&bitmap[ix >> 5], 1u << (ix & 31u));
+      }
+      const bool take = t < hi && d1 == b1;
       hist_add(h, take, (key[m] >> 10) & 1023u);
       const uint64_t bal = __ballot(take);
       uint32_t wbase = 0u;
@@ -273,7 +279,8 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(SelectCtl* __restrict__ c
                                                        const uint32_t* __restrict__ stage_key,
                                                        const int32_t* __restrict__ stage_idx,
                                                        uint32_t* __restrict__ hist_c, uint32_t* __restrict__ hist,
-                                                       int pruned, uint32_t k) {
+                                                       int pruned, uint32_t k, unsigned long long* __restrict__ flags,
+                                                       int64_t emit_blocks) {
   __shared__ uint32_t h[2048];
   __shared__ uint32_t shw[kSelBlock / 64];
   __shared__ uint32_t res[2];
@@ -292,6 +299,7 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(SelectCtl* __restrict__ c
     for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) hist_c[b] = 0u;
   if (dense)
     for (int b = threadIdx.x; b < kDigit1Bins; b += kSelBlock) hist[b] = 0u;
+  for (int64_t b = threadIdx.x; b < emit_blocks; b += kSelBlock) flags[b] = 0ull;  // the emit's look-back words
   __syncthreads();
   find_bucket<kSelBlock, kDigitBins>(h, true, need1, shw, res);
   const uint32_t pre2 = (b1 << 10) | res[0];
@@ -399,25 +407,26 @@ __global__ void __launch_bounds__(kSelBlock) k_select2(SelectCtl* __restrict__ c
   if (threadIdx.x == 0) {
     ctl->tau = tau;
     ctl->iota = iota;
+    ctl->n_staged = (uint32_t)n2;
     ctl->n_stage2 = 0u;
+    ctl->emit_ticket = 0u;
   }
 }
 
 // ------------------------------------------------------------------------------------
-// Step 4: mark the selected candidates.
+// Step 4: mark the taken keys of the staged digit-1 bucket (the candidates above it set
+// their bits in k_digit2).
 
-__global__ void __launch_bounds__(kBlock) k_finalize(const uint32_t* __restrict__ cand_key,
-                                                     const int32_t* __restrict__ cand_idx,
-                                                     const SelectCtl* __restrict__ ctl, int64_t cap, int64_t d,
-                                                     int pruned, uint32_t* __restrict__ bitmap) {
-  const bool dense = dense_cands(ctl, pruned);
-  const int64_t n = dense ? d : (ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap);
+__global__ void __launch_bounds__(kBlock) k_mark(const uint32_t* __restrict__ stage_key,
+                                                 const int32_t* __restrict__ stage_idx,
+                                                 const SelectCtl* __restrict__ ctl, uint32_t* __restrict__ bitmap) {
+  const int64_t n2 = ctl->n_staged;
   const uint32_t tau = ctl->tau, iota = ctl->iota;
   const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n; t += stride) {
-    const uint32_t key = cand_key[t];
+  for (int64_t t = (int64_t)blockIdx.x * kBlock + threadIdx.x; t < n2; t += stride) {
+    const uint32_t key = stage_key[t];
     if (key < tau) continue;
-    const uint32_t ix = dense ? (uint32_t)t : (uint32_t)cand_idx[t];
+    const uint32_t ix = (uint32_t)stage_idx[t];
     if (key > tau || ix <= iota) atomicOr(&bitmap[ix >> 5], 1u << (ix & 31u));
   }
 }
@@ -508,14 +517,16 @@ __device__ uint32_t sampled_bound(const uint32_t* __restrict__ sample, int M, ui
   return (pre << 10) | res[0];
 }
 
-// Heavy-cell bitmap: bit e of the flat [r][c] sketch is |merged[e]| >= tau0, or (HEAVYMIX,
+// Heavy-cell bitmap: bit j * hrow + col (rows padded to hrow bits, a multiple of 64, so a
+// row starts on a word) is |merged[j][col]| >= tau0, or (HEAVYMIX,
 // hm = 1) merged[e]^2 >= theta in fp64 (one ballot per 64 cells); with hm the sampled fill
 // bound tau0 is still found here, for the pruned pass. A coordinate with
 // est^2 >= theta has ceil(r/2) cells with |cell| >= |est| (see the pruned pass), and the
 // squares of fp32 values are exact in fp64, so those cells pass the same test.
 // Every block first finds tau0 itself (the sampled keys are read from L2; block 0 records
 // it and resets the selection counters), so no single-block kernel runs in between.
-__global__ void __launch_bounds__(kSelBlock) k_heavy(const float* __restrict__ merged, int64_t rc,
+__global__ void __launch_bounds__(kSelBlock) k_heavy(const float* __restrict__ merged, int64_t c, int64_t hrow,
+                                                  int r,
                                                   SelectCtl* __restrict__ ctl, uint32_t* __restrict__ heavy,
                                                   int hm, const uint32_t* __restrict__ sample, int M,
                                                   uint32_t rho, uint32_t k, const uint32_t* __restrict__ hist_s) {
@@ -532,11 +543,13 @@ __global__ void __launch_bounds__(kSelBlock) k_heavy(const float* __restrict__ m
   }
   const double theta = ctl->theta;
   const int64_t stride = (int64_t)gridDim.x * kSelBlock;
-  for (int64_t base = ((int64_t)blockIdx.x * kSelBlock + threadIdx.x) & ~63ll; base < rc; base += stride) {
-    const int64_t e = base + (threadIdx.x & 63);
+  const int64_t n = (int64_t)r * hrow;  // bits of the padded map; hrow is a multiple of 64
+  for (int64_t base = ((int64_t)blockIdx.x * kSelBlock + threadIdx.x) & ~63ll; base < n; base += stride) {
+    const int64_t j = base / hrow;  // one row per wave (64-bit aligned bases)
+    const int64_t col = base - j * hrow + (threadIdx.x & 63);
     bool hv = false;
-    if (e < rc) {
-      const float x = merged[e];
+    if (col < c) {
+      const float x = merged[j * c + col];
       hv = hm ? (double)x * (double)x >= theta : abs_key(x) >= tau0;
     }
     const uint64_t m = __ballot(hv);
@@ -587,18 +600,34 @@ constexpr int kMapCoarse = 1;  // a coarse map in LDS (one bit per 2^coarse_log2
                                // in global memory, so the count equals the fine map's
 constexpr int kMapGlobal = 2;  // the fine map read from global memory
 
+constexpr int kPruneLdsWords = 160 * 1024 / 4;  // the whole LDS of a CU (one workgroup per CU)
+
+template <int MAP>
+__device__ __forceinline__ int64_t map_words_in_lds(int64_t map_words) {
+  return MAP == kMapGlobal ? 0 : map_words;
+}
+
+// Bit e & 31 of word w (the hardware takes the low five bits of the offset).
+__device__ __forceinline__ uint32_t bit_at(uint32_t w, uint32_t e) { return __builtin_amdgcn_ubfe(w, e, 1u); }
+
 template <int R, bool HM, int MAP>
 __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, SelectCtl* __restrict__ ctl,
                                                    const uint32_t* __restrict__ heavy,
                                                    const uint32_t* __restrict__ lmap, int64_t map_words,
-                                                   int coarse_log2, int buf_cap, uint32_t* __restrict__ queue,
+                                                   int64_t hrow, int coarse_log2, int buf_cap,
+                                                   uint32_t* __restrict__ queue,
                                                    uint32_t* __restrict__ bitmap, const uint32_t* __restrict__ rnd,
                                                    uint32_t* __restrict__ hist_s) {
-  constexpr int U = 4;  // coordinates per lane per pass: independent hash chains in flight
+  // coordinates per lane per pass: independent hash chains in flight (two registers each per
+  // row, so fewer with many rows, where four would spill)
+  constexpr int U = R <= 8 ? 4 : R <= 12 ? 2 : 1;
   // flat cell index j*c + col; below 2^32 whenever a map fits in LDS
   using Cell = typename std::conditional<MAP == kMapGlobal, uint64_t, uint32_t>::type;
-  extern __shared__ uint32_t sm[];
-  __shared__ uint32_t bn, gbase;
+  // LDS: [map words][buf_cap queue entries][2 counters], one static array, so a lookup's
+  // address is known at compile time to need no base added
+  __shared__ uint32_t sm[kPruneLdsWords];
+  uint32_t& bn = sm[map_words_in_lds<MAP>(map_words) + buf_cap];
+  uint32_t& gbase = sm[map_words_in_lds<MAP>(map_words) + buf_cap + 1];
   if (blockIdx.x == 0)  // the samples' histogram, read by k_heavy, cleared for the next call
     for (int b = threadIdx.x; b < kDigit1Bins; b += kPruneBlock) hist_s[b] = 0u;
   uint32_t* buf = sm;
@@ -628,14 +657,39 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
   __syncthreads();
   const int64_t stride = (int64_t)gridDim.x * kPruneBlock * U;
   const int64_t base0 = (int64_t)blockIdx.x * kPruneBlock * U;
-  uint32_t hb[R][U], db[R];  // raw bucket hashes of this lane's U coordinates, per-stride steps
+  // Raw bucket hashes and columns of this lane's U coordinates, advanced by one stride per
+  // pass without a multiply: the raw hash moves by db = (a * stride) mod p, less p when it
+  // passes p, so the column moves by dc1 = db mod c, or by dc2 = (db - p) mod c after such a
+  // wrap, and is brought back below c by one subtraction. The raw hash is kept biased by
+  // kBias = 2^32 - p, so that passing p is the carry out of the 32-bit add.
+  constexpr uint32_t kBias = 0x80000001u;
+  uint32_t hb[R][U], cb[R][U], db[R], dc1[R], dc2[R];
+  const uint32_t pc = mod_c(kMersenne, kr[0].c, kr[0].magic, kr[0].shift);  // p mod c
 #pragma unroll
   for (int j = 0; j < R; ++j) {
     db[j] = mod_mersenne_affine(kr[j].a, 0u, (uint32_t)stride);
+    dc1[j] = mod_c(db[j], kr[j].c, kr[j].magic, kr[j].shift);
+    dc2[j] = dc1[j] >= pc ? dc1[j] - pc : dc1[j] + (kr[j].c - pc);
+    // the select between the two steps takes one operand from a vector register: keep both
+    // there for the whole kernel rather than copying them in every pass
+    asm volatile("" : "+v"(dc1[j]), "+v"(dc2[j]));
 #pragma unroll
-    for (int m = 0; m < U; ++m)
-      hb[j][m] = mod_mersenne_affine(kr[j].a, kr[j].b, (uint32_t)(base0 + threadIdx.x + (int64_t)m * kPruneBlock));
+    for (int m = 0; m < U; ++m) {
+      const uint32_t raw =
+          mod_mersenne_affine(kr[j].a, kr[j].b, (uint32_t)(base0 + threadIdx.x + (int64_t)m * kPruneBlock));
+      hb[j][m] = raw + kBias;  // < 2^32: raw < p
+      cb[j][m] = mod_c(raw, kr[j].c, kr[j].magic, kr[j].shift);
+    }
   }
+  auto advance = [&](int j, int m) {
+    const uint32_t t = hb[j][m] + db[j];
+    const bool wrap = t < db[j];  // carry out: raw + db >= p
+    hb[j][m] = wrap ? t + kBias : t;  // on a carry t is the new raw hash itself
+    const uint32_t cn = cb[j][m] + (wrap ? dc2[j] : dc1[j]);
+    cb[j][m] = min(cn, cn - kr[j].c);  // cn < 2c: one subtraction, unsigned
+  };
+  // byte offset of row j's map words (rows padded to hrow bits, hrow a multiple of 64)
+  const uint32_t hrow32 = (uint32_t)(hrow >> 5);
   for (int64_t base = base0; base < d; base += stride) {  // block-uniform
     // HEAVYMIX: the draws are loaded first, so their memory latency overlaps the lookups
     uint32_t fill[U];
@@ -657,11 +711,11 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
         uint32_t cset = 0u, nset = 0u;
 #pragma unroll
         for (int j = 0; j < R; ++j) {
-          const uint32_t col = mod_c(hb[j][m], kr[j].c, kr[j].magic, kr[j].shift);
-          hb[j][m] = add_mod_mersenne(hb[j][m], db[j]);
-          ev[j] = (Cell)j * kr[j].c + col;
+          const uint32_t col = cb[j][m];
+          advance(j, m);
+          ev[j] = (Cell)j * (Cell)hrow + col;
           const uint32_t cb = ev[j] >> coarse_log2;
-          const uint32_t bit = (sm[cb >> 5] >> (cb & 31)) & 1u;
+          const uint32_t bit = bit_at(sm[cb >> 5], cb);
           cset |= bit << j;
           nset += bit;
         }
@@ -675,19 +729,22 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
             }
           }
         }
+      } else if constexpr (MAP == kMapFine) {
+#pragma unroll
+        for (int j = 0; j < R; ++j) {
+          const uint32_t col = cb[j][m];
+          advance(j, m);
+          cnt[m] += bit_at(sm[(uint32_t)j * hrow32 + (col >> 5)], col);
+        }
       } else {
 #pragma unroll
         for (int j = 0; j < R; ++j) {
-          const uint32_t col = mod_c(hb[j][m], kr[j].c, kr[j].magic, kr[j].shift);
-          hb[j][m] = add_mod_mersenne(hb[j][m], db[j]);
-          const Cell e = (Cell)j * kr[j].c + col;
-          if constexpr (MAP == kMapFine) {
-            cnt[m] += (sm[e >> 5] >> (e & 31)) & 1u;
-          } else {
-            // global reads are the cost here (L2 requests): skip a row once the coordinate
-            // cannot reach `need` with the rows left, which leaves the keep decision unchanged
-            if (cnt[m] + (uint32_t)(R - j) >= (uint32_t)need) cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
-          }
+          const uint32_t col = cb[j][m];
+          advance(j, m);
+          const Cell e = (Cell)j * (Cell)hrow + col;
+          // global reads are the cost here (L2 requests): skip a row once the coordinate
+          // cannot reach `need` with the rows left, which leaves the keep decision unchanged
+          if (cnt[m] + (uint32_t)(R - j) >= (uint32_t)need) cnt[m] += (heavy[e >> 5] >> (e & 31)) & 1u;
         }
       }
     }
@@ -814,28 +871,40 @@ __global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* _
 // ------------------------------------------------------------------------------------
 // Step 5: bitmap -> ascending index list.
 
-__global__ void __launch_bounds__(kSelBlock) k_emit_count(const uint32_t* __restrict__ bitmap, int64_t words,
-                                                          uint32_t* __restrict__ blockcnt) {
-  __shared__ uint32_t shw[kSelBlock / 64];
-  const int64_t w0 = (int64_t)blockIdx.x * kEmitWordsPerBlock + (int64_t)threadIdx.x * kEmitWordsPerThread;
-  uint32_t cnt = 0;
-#pragma unroll
-  for (int m = 0; m < kEmitWordsPerThread; ++m)
-    if (w0 + m < words) cnt += __popc(bitmap[w0 + m]);
-  uint32_t total;
-  block_scan_incl<kSelBlock>(cnt, shw, total);
-  if (threadIdx.x == 0) blockcnt[blockIdx.x] = total;
+// Look-back word of emit block b: 0 until published, then kFlagAgg | (the block's own count),
+// then kFlagIncl | (the count of blocks 0..b together). The count is all a word carries, so
+// relaxed device-scope loads and stores of the word suffice (no fence orders other data).
+constexpr unsigned long long kFlagAgg = 1ull << 62, kFlagIncl = 2ull << 62;
+constexpr unsigned long long kFlagCount = 0xffffffffull;
+// Polls of a window of predecessors' words before the block counts the bitmap words before
+// its own directly (the blocks start in ticket order, so a predecessor is running and
+// publishes without waiting on later blocks; the bound makes every wait finite regardless).
+constexpr int kEmitSpin = 1 << 20;
+
+__device__ __forceinline__ unsigned long long flag_load(const unsigned long long* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void flag_store(unsigned long long* p, unsigned long long v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__global__ void __launch_bounds__(kSelBlock) k_emit_write(const uint32_t* __restrict__ bitmap, int64_t words,
-                                                          const uint32_t* __restrict__ blockcnt,
-                                                          int32_t* __restrict__ idx, uint32_t k) {
+// Bitmap -> ascending index list in one pass. Block b (by ticket, i.e. in start order) owns
+// words [b W, (b + 1) W): it counts its bits, publishes the count, adds the counts of the
+// blocks before it (walking back until a block that has published its inclusive count),
+// publishes its own inclusive count and writes its indices from that offset.
+__global__ void __launch_bounds__(kSelBlock) k_emit(const uint32_t* __restrict__ bitmap, int64_t words,
+                                                    SelectCtl* __restrict__ ctl,
+                                                    unsigned long long* __restrict__ flags,
+                                                    int32_t* __restrict__ idx, uint32_t k) {
   __shared__ uint32_t shw[kSelBlock / 64];
-  uint32_t before = 0;
-  for (int b = threadIdx.x; b < (int)blockIdx.x; b += kSelBlock) before += blockcnt[b];
-  uint32_t base;
-  block_scan_incl<kSelBlock>(before, shw, base);
-  const int64_t w0 = (int64_t)blockIdx.x * kEmitWordsPerBlock + (int64_t)threadIdx.x * kEmitWordsPerThread;
+  __shared__ uint32_t sb, sexcl, sdirect;
+  if (threadIdx.x == 0) {
+    sb = atomicAdd(&ctl->emit_ticket, 1u);
+    sdirect = 0u;
+  }
+  __syncthreads();
+  const int64_t b = sb;
+  const int64_t w0 = b * kEmitWordsPerBlock + (int64_t)threadIdx.x * kEmitWordsPerThread;
   uint32_t wv[kEmitWordsPerThread];
   uint32_t cnt = 0;
 #pragma unroll
@@ -844,13 +913,61 @@ __global__ void __launch_bounds__(kSelBlock) k_emit_write(const uint32_t* __rest
     cnt += __popc(wv[m]);
   }
   uint32_t total;
-  uint32_t pos = base + block_scan_incl<kSelBlock>(cnt, shw, total) - cnt;
+  const uint32_t incl = block_scan_incl<kSelBlock>(cnt, shw, total);
+  if (threadIdx.x < 64) {  // the first wave publishes and looks back, 64 predecessors at a time
+    const int lane = threadIdx.x;
+    if (lane == 0) flag_store(&flags[b], (b == 0 ? kFlagIncl : kFlagAgg) | total);
+    uint32_t excl = 0;
+    bool direct = false;
+    for (int64_t top = b - 1; top >= 0; top -= 64) {
+      const int64_t j = top - lane;  // lane 0 is the nearest predecessor
+      unsigned long long f = j >= 0 ? flag_load(&flags[j]) : kFlagIncl;  // before block 0: 0
+      uint64_t incl_lanes, need;
+      for (int spin = 0;; ++spin) {
+        incl_lanes = __ballot((f & kFlagIncl) != 0ull);
+        // lanes up to the nearest inclusive word must have published
+        need = incl_lanes ? ((2ull << __builtin_ctzll(incl_lanes)) - 1ull) : ~0ull;
+        if ((__ballot(f == 0ull) & need) == 0ull) break;
+        if (spin == kEmitSpin) {
+          direct = true;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        if (f == 0ull) f = flag_load(&flags[j]);
+      }
+      if (direct) break;
+      uint32_t part = ((need >> lane) & 1ull) ? (uint32_t)(f & kFlagCount) : 0u;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) part += __shfl_xor(part, o, 64);
+      excl += part;
+      if (incl_lanes) break;
+    }
+    if (lane == 0) {
+      sdirect = direct ? 1u : 0u;
+      if (b > 0 && !direct) flag_store(&flags[b], kFlagIncl | (excl + total));
+      sexcl = excl;
+    }
+  }
+  __syncthreads();
+  if (sdirect) {  // every word before this block's, counted by the whole block
+    uint32_t before = 0;
+    for (int64_t w = threadIdx.x; w < b * kEmitWordsPerBlock; w += kSelBlock) before += __popc(bitmap[w]);
+    uint32_t all;
+    (void)block_scan_incl<kSelBlock>(before, shw, all);
+    if (threadIdx.x == 0) {
+      sexcl = all;
+      flag_store(&flags[b], kFlagIncl | (all + total));
+    }
+    __syncthreads();
+  }
+  uint32_t pos = sexcl + incl - cnt;
+  const int64_t wb = b * kEmitWordsPerBlock + (int64_t)threadIdx.x * kEmitWordsPerThread;
 #pragma unroll
   for (int m = 0; m < kEmitWordsPerThread; ++m) {
     uint32_t w = wv[m];
     while (w) {
       const int bit = __ffs(w) - 1;
-      if (pos < k) idx[pos] = (int32_t)((w0 + m) * 32 + bit);
+      if (pos < k) idx[pos] = (int32_t)((wb + m) * 32 + bit);
       ++pos;
       w &= w - 1u;
     }
@@ -1008,47 +1125,34 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
   if (rho_d < 1) rho_d = 1;
   hipLaunchKernelGGL((k_sample<R, HM>), dim3((M + kBlock - 1) / kBlock), dim3(kBlock), 0, s, x->hs, merged, x->d, M,
                      rnd, x->sample_keys, x->hist_s);
-  const int64_t rc = (int64_t)x->r * x->c;
-  hipLaunchKernelGGL(k_heavy, dim3(grid_for(rc, kSelBlock, x->num_cus)), dim3(kSelBlock), 0, s, merged, rc, x->ctl,
+  const int64_t nbits = (int64_t)x->r * x->heavy_row;  // heavy-cell map bits (padded rows)
+  hipLaunchKernelGGL(k_heavy, dim3(grid_for(nbits, kSelBlock, x->num_cus)), dim3(kSelBlock), 0, s, merged, x->c,
+                     x->heavy_row, x->r, x->ctl,
                      x->heavy, HM ? 1 : 0, x->sample_keys, M, (uint32_t)rho_d, (uint32_t)k, x->hist_s);
   // with the bitmap in LDS one block fits a CU: launch one per CU so the map is loaded once
   const int pgrid = grid_for(x->d, 4 * kPruneBlock, x->prune_map_in_lds ? x->num_cus : 2 * x->num_cus);
   const dim3 pb(kPruneBlock);
   if (!x->prune_map_in_lds) {
-    hipLaunchKernelGGL((k_pruned<R, HM, kMapGlobal>), dim3(pgrid), pb, x->prune_lds, s, x->hs, x->d, x->ctl,
-                       x->heavy, x->heavy, x->prune_map_words, 0, x->prune_buf_cap, x->keys, x->bitmap, rnd,
-                       x->hist_s);
+    hipLaunchKernelGGL((k_pruned<R, HM, kMapGlobal>), dim3(pgrid), pb, 0, s, x->hs, x->d, x->ctl,
+                       x->heavy, x->heavy, x->prune_map_words, x->heavy_row, 0, x->prune_buf_cap, x->keys,
+                       x->bitmap, rnd, x->hist_s);
   } else if (x->prune_coarse_log2 > 0) {
     hipLaunchKernelGGL(k_coarse, dim3(grid_for(x->prune_coarse_words, kBlock, 4 * x->num_cus)), dim3(kBlock), 0, s,
-                       x->heavy, (rc + 63) / 64 * 2, x->prune_coarse_log2, x->coarse, x->prune_coarse_words);
-    hipLaunchKernelGGL((k_pruned<R, HM, kMapCoarse>), dim3(pgrid), pb, x->prune_lds, s, x->hs, x->d, x->ctl,
-                       x->heavy, x->coarse, x->prune_map_words, x->prune_coarse_log2, x->prune_buf_cap, x->keys,
+                       x->heavy, nbits / 32, x->prune_coarse_log2, x->coarse, x->prune_coarse_words);
+    hipLaunchKernelGGL((k_pruned<R, HM, kMapCoarse>), dim3(pgrid), pb, 0, s, x->hs, x->d, x->ctl,
+                       x->heavy, x->coarse, x->prune_map_words, x->heavy_row, x->prune_coarse_log2,
+                       x->prune_buf_cap, x->keys,
                        x->bitmap, rnd, x->hist_s);
   } else {
-    hipLaunchKernelGGL((k_pruned<R, HM, kMapFine>), dim3(pgrid), pb, x->prune_lds, s, x->hs, x->d, x->ctl,
-                       x->heavy, x->heavy, x->prune_map_words, 0, x->prune_buf_cap, x->keys, x->bitmap, rnd,
-                       x->hist_s);
+    hipLaunchKernelGGL((k_pruned<R, HM, kMapFine>), dim3(pgrid), pb, 0, s, x->hs, x->d, x->ctl,
+                       x->heavy, x->heavy, x->prune_map_words, x->heavy_row, 0, x->prune_buf_cap, x->keys,
+                       x->bitmap, rnd, x->hist_s);
   }
   hipLaunchKernelGGL((k_survivors<R, HM>), dim3(x->num_cus), dim3(kBlock), 0, s, x->hs, merged, x->ctl, x->keys,
                      x->cand_key, x->cand_idx, x->cand_cap, rnd, x->hist_c);
 }
 
-template <int R>
-hipError_t allow_prune_lds(size_t bytes) {
-  const void* fns[] = {reinterpret_cast<const void*>(&k_pruned<R, false, kMapFine>),
-                       reinterpret_cast<const void*>(&k_pruned<R, true, kMapFine>),
-                       reinterpret_cast<const void*>(&k_pruned<R, false, kMapCoarse>),
-                       reinterpret_cast<const void*>(&k_pruned<R, true, kMapCoarse>),
-                       reinterpret_cast<const void*>(&k_pruned<R, false, kMapGlobal>),
-                       reinterpret_cast<const void*>(&k_pruned<R, true, kMapGlobal>)};
-  for (const void* f : fns) {
-    const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
-}
-
-// digit2 -> select2 -> finalize -> emit over the candidates: the pruned pass's (pruned = 1,
+// digit2 -> select2 -> mark -> emit over the candidates: the pruned pass's (pruned = 1,
 // unless it fell short of k) or the full estimate's dense ones.
 hipError_t launch_select_tail(int64_t d, int num_cus, const SelectBufs& b, hipStream_t s, int64_t k, int pruned,
                               int32_t* idx) {
@@ -1057,16 +1161,13 @@ hipError_t launch_select_tail(int64_t d, int num_cus, const SelectBufs& b, hipSt
   int g2 = num_cus;
   if (!pruned) g2 = std::max(g2, grid_for(d, 8192, 8 * num_cus));
   hipLaunchKernelGGL(k_digit2, dim3(g2), dim3(kBlock), 0, s, b.cand_key, b.cand_idx, b.ctl, b.cand_cap, d, b.hist_c,
-                     b.hist, pruned, (uint32_t)k, b.hist2, b.keys, b.stage_idx);
+                     b.hist, pruned, (uint32_t)k, b.hist2, b.keys, b.stage_idx, b.bitmap);
   hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, b.ctl, b.hist2, b.keys, b.stage_idx, b.hist_c, b.hist,
-                     pruned, (uint32_t)k);
-  hipLaunchKernelGGL(k_finalize, dim3(4 * num_cus), dim3(kBlock), 0, s, b.cand_key, b.cand_idx, b.ctl, b.cand_cap, d,
-                     pruned, b.bitmap);
+                     pruned, (uint32_t)k, b.emit_flags, b.emit_blocks);
+  hipLaunchKernelGGL(k_mark, dim3(num_cus), dim3(kBlock), 0, s, b.keys, b.stage_idx, b.ctl, b.bitmap);
   const int64_t words = (d + 31) / 32;
-  hipLaunchKernelGGL(k_emit_count, dim3((unsigned)b.emit_blocks), dim3(kSelBlock), 0, s, b.bitmap, words,
-                     b.blockcnt);
-  hipLaunchKernelGGL(k_emit_write, dim3((unsigned)b.emit_blocks), dim3(kSelBlock), 0, s, b.bitmap, words,
-                     b.blockcnt, idx, (uint32_t)k);
+  hipLaunchKernelGGL(k_emit, dim3((unsigned)b.emit_blocks), dim3(kSelBlock), 0, s, b.bitmap, words, b.ctl,
+                     b.emit_flags, idx, (uint32_t)k);
   return hipGetLastError();
 }
 
@@ -1082,8 +1183,8 @@ int64_t emit_blocks_for(int64_t d) {
 }
 
 hipError_t prepare_prune(gs_ctx* x) {
-  const int64_t rc = (int64_t)x->r * x->c;
-  const int64_t words = (rc + 63) / 64 * 2;
+  const int64_t rc = (int64_t)x->r * x->heavy_row;  // bits of the heavy-cell map (padded rows)
+  const int64_t words = rc / 32;
   const int64_t lds_max = 160 * 1024 - 256;
   // the fine map in LDS if it fits beside a 512-entry queue buffer; else the coarsest-needed
   // coarse map (2 .. 32 cells per bit); else the fine map from global memory
@@ -1101,7 +1202,6 @@ hipError_t prepare_prune(gs_ctx* x) {
     x->prune_coarse_log2 = log2g;
     x->prune_map_words = map_words;
     x->prune_buf_cap = (int)buf;
-    x->prune_lds = (size_t)(map_words * 4 + buf * 4);
     if (log2g > 0) {
       x->prune_coarse_words = map_words;
       const hipError_t e = hipMalloc(reinterpret_cast<void**>(&x->coarse), (size_t)map_words * sizeof(uint32_t));
@@ -1112,16 +1212,11 @@ hipError_t prepare_prune(gs_ctx* x) {
     x->prune_coarse_log2 = 0;
     x->prune_map_words = words;
     x->prune_buf_cap = 8192;
-    x->prune_lds = 8192 * 4;
   }
-  switch (x->r) {
-#define GS_R_CASE(RR) \
-  case RR: return allow_prune_lds<RR>(x->prune_lds);
-    GS_R_CASE(1) GS_R_CASE(2) GS_R_CASE(3) GS_R_CASE(4) GS_R_CASE(5) GS_R_CASE(6) GS_R_CASE(7) GS_R_CASE(8)
-    GS_R_CASE(9) GS_R_CASE(10) GS_R_CASE(11) GS_R_CASE(12) GS_R_CASE(13) GS_R_CASE(14) GS_R_CASE(15) GS_R_CASE(16)
-#undef GS_R_CASE
-    default: return hipErrorInvalidValue;
-  }
+  // the map (when in LDS), the queue buffer and two counters share the pass's LDS array
+  if ((x->prune_map_in_lds ? x->prune_map_words : 0) + x->prune_buf_cap + 2 > kPruneLdsWords)
+    return hipErrorInvalidValue;
+  return hipSuccess;
 }
 
 hipError_t launch_unsketch_topk(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, float* est, int32_t* idx) {
