@@ -119,8 +119,10 @@ def kernel_source_file(name: str):
     return None
 
 
-def stage_kernels(w, layout: str = "interleaved") -> dict:
-    """The kernels each stage of the fused step launches (names as rocprofv3 reports them)."""
+def stage_kernels(w, layout: str = "interleaved", plan: dict = None) -> dict:
+    """The kernels each stage of the fused step launches (names as rocprofv3 reports them).
+    `plan` is the context's gs_describe; without it the library's size rule is assumed (list
+    segments only for small sketches)."""
     if layout == "interleaved":
         acc = [f"k_accumulate_il<{w.P // 4}>"]
     elif w.P == 1:
@@ -133,13 +135,16 @@ def stage_kernels(w, layout: str = "interleaved") -> dict:
                   f"k_unsketch<{w.r}>"] + tail
     else:  # every coordinate estimated
         select = [f"k_unsketch<{w.r}>"] + tail
+    segmented = plan["segments"] > 1 if plan is not None else w.d <= 1_000_000
     return {
         "accumulate": acc,
         # packed lists (the library's choice here); one worker in the worker-major layout: its
         # plain state vector gathered directly (the last template argument)
         "sketch": [f"k_pull<{w.P}, {4 if w.P <= 4 else 6}, true, "
                    f"{'true' if w.P == 1 and layout == 'worker_major' else 'false'}>"],
-        "merge": [f"k_merge_partials<{w.P}>"],
+        # the tiles merge their own cells; small sketches' tiles, split into list segments,
+        # are summed here
+        "merge": [f"k_merge_partials<{w.P}>"] if segmented else [],
         "select": select,
         "gather_reset": [f"k_gather_reset<{w.P}>"],
     }
@@ -252,6 +257,7 @@ def main():
     ctx = gs.GsContext(w.d, w.P, w.r, w.c, w.k, hp, rho=w.rho, state_layout=layout)
     torch.cuda.synchronize()
     create_ms = (time.perf_counter() - c_t0) * 1e3  # gs_create: scratch and the static tile lists
+    plan = ctx.describe()
     u = torch.zeros(ctx.state_shape, dtype=torch.float32, device=dev)
     v = torch.zeros_like(u)
     if args.state == "sketch":
@@ -319,7 +325,7 @@ def main():
         stage_ms = {"interleave": stage_ms["accumulate"], "sketch": stage_ms["sketch"], "merge": stage_ms["merge"],
                     "select": stage_ms["select"], "state_update": stage_ms["gather_reset"]}
     sb = stage_bytes(w, args.state)
-    kern = stage_kernels(w, layout)
+    kern = stage_kernels(w, layout, plan)
     stages = []
     for st, st_ms in stage_ms.items():
         if n_timed == 0 or st_ms <= 0 or sb.get(st, 0) <= 0:
@@ -400,6 +406,7 @@ def main():
         "stage_ms_from": f"HIP events recorded between the stages of {n_timed} further steps after the timed region",
         "roofline": roofline,
         "create_ms": create_ms,
+        "plan": plan,
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:

@@ -263,6 +263,28 @@ gs_status gs_timing_stop(gs_ctx* ctx, float* stage_ms, int32_t* n_steps);
 gs_status gs_unsketch_topk_static(const gs_config* cfg, void* stream, const float* merged, int64_t k, float* est,
                                   int32_t* idx);
 
+/* The form a context computes in, fixed by gs_create (for tests and benchmark reports).
+ *   sketch            GS_SKETCH_GATHER: LDS tiles gather their listed coordinates (Sec. III-A,
+ *                     S(g) = C g, cell by cell); GS_SKETCH_ATOMIC: fp64 device atomics
+ *   tile_width        columns per tile (gather), tiles = r * tiles per row, segments = list
+ *                     segments per tile (tiles split so that small sketches fill the GPU)
+ *   packed_lists      1: one 32-bit word per list entry (coordinate offset, position, sign)
+ *   prune             1: selections without an estimate vector prune (d * r > 2,000,000)
+ *   row_copy          1: the context holds the interleaved copy of v ([d][PP] floats)
+ * Errors: GS_ERR_INVALID_ARG for a NULL argument. */
+#define GS_SKETCH_GATHER 0
+#define GS_SKETCH_ATOMIC 1
+typedef struct gs_plan {
+  int32_t sketch;
+  int32_t tile_width;
+  int32_t tiles;
+  int32_t segments;
+  int32_t packed_lists;
+  int32_t prune;
+  int32_t row_copy;
+} gs_plan;
+gs_status gs_describe(const gs_ctx* ctx, gs_plan* out);
+
 /* Static description of a status code. */
 const char* gs_status_string(gs_status status);
 

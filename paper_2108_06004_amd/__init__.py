@@ -25,7 +25,7 @@ GS_MAX_ROWS = 16
 EXPORTED = ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
             "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_sketch_momentum",
             "gs_apply_update", "gs_step_profiled", "gs_timing_start", "gs_timing_stop", "gs_unsketch_topk_static",
-            "gs_status_string", "gs_last_error")
+            "gs_describe", "gs_status_string", "gs_last_error")
 GS_STATIC_MAX_D = 4194304  # largest d of gs_unsketch_topk_static (its fixed scratch array)
 GS_NUM_STAGES = 5
 STAGES = ("accumulate", "sketch", "merge", "select", "gather_reset")
@@ -68,6 +68,13 @@ class gs_config(ctypes.Structure):
 
 
 GS_OPT_ROW_COPY = 1
+GS_SKETCH_GATHER, GS_SKETCH_ATOMIC = 0, 1  # gs_plan.sketch
+
+
+class gs_plan(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32) for name in
+                ("sketch", "tile_width", "tiles", "segments", "packed_lists", "prune",
+                 "row_copy")]
 
 
 _lib = None
@@ -98,6 +105,7 @@ def load_library():
     lib.gs_timing_start.argtypes = [vp, ctypes.c_int32]
     lib.gs_timing_stop.argtypes = [vp, vp, vp]
     lib.gs_unsketch_topk_static.argtypes = [ctypes.POINTER(gs_config), vp, vp, i64, vp, vp]
+    lib.gs_describe.argtypes = [vp, ctypes.POINTER(gs_plan)]
     for name in ("gs_create", "gs_destroy", "gs_accumulate", "gs_sketch", "gs_merge", "gs_unsketch_topk",
                  "gs_gather_reset", "gs_step", "gs_heavymix_topk", "gs_step_heavymix", "gs_step_sketch_momentum",
                  "gs_apply_update", "gs_step_profiled", "gs_timing_start", "gs_timing_stop",
@@ -116,6 +124,12 @@ def _check(status: int, ctx=None, what: str = ""):
         lib = load_library()
         detail = lib.gs_last_error(ctx).decode() if lib.gs_last_error(ctx) is not None else ""
         raise GsError(status, f"{what}: {lib.gs_status_string(status).decode()}: {detail}")
+
+
+def gs_describe(ctx) -> dict:
+    plan = gs_plan()
+    _check(load_library().gs_describe(ctx, ctypes.byref(plan)), ctx, "gs_describe")
+    return {name: getattr(plan, name) for name, _ in gs_plan._fields_}
 
 
 def _ptr(t, dtype=None, numel=None, name="tensor"):
@@ -265,6 +279,10 @@ class GsContext:
         self.handle = gs_create(d, P, r, c, k_max, hash_params["a"], hash_params["b"], hash_params["a2"],
                                 hash_params["b2"], rho, reset_momentum, STATE_LAYOUTS[state_layout],
                                 GS_OPT_ROW_COPY if row_copy else 0)
+
+    def describe(self) -> dict:
+        """gs_describe: the form this context computes in (sketch form, tiles, write-out buckets, ...)."""
+        return gs_describe(self.handle)
 
     @property
     def state_shape(self) -> tuple:

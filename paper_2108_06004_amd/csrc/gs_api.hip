@@ -256,6 +256,20 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
   return GS_OK;
 }
 
+gs_status gs_describe(const gs_ctx* x, gs_plan* out) {
+  if (!x || !out) return GS_ERR_INVALID_ARG;
+  gs_plan p{};
+  p.sketch = x->use_pull ? GS_SKETCH_GATHER : GS_SKETCH_ATOMIC;
+  p.tile_width = x->use_pull ? x->plan.W : 0;
+  p.tiles = x->use_pull ? x->plan.T : 0;
+  p.segments = x->use_pull ? x->plan.S : 0;
+  p.packed_lists = x->use_pull ? x->plan.packed : 0;
+  p.prune = x->d * x->r > x->prune_min_cells ? 1 : 0;
+  p.row_copy = x->vI != nullptr ? 1 : 0;
+  *out = p;
+  return GS_OK;
+}
+
 gs_status gs_destroy(gs_ctx* x) {
   if (!x) return GS_OK;
   hipError_t e = hipDeviceSynchronize();

@@ -408,6 +408,24 @@ def test_unpacked_lists(monkeypatch, d, P, r, c, k):
     dv.close()
 
 
+def test_describe_reports_the_form_in_use(monkeypatch):
+    monkeypatch.delenv("GS_SELECT_PATH", raising=False)  # the library's own size rule for pruning
+    hp = synth.hash_params(synth.BASE_SEED + 44, 5)
+    big = gs.GsContext(1_000_000, 8, 5, 100_000, 100, hp, state_layout="interleaved").describe()
+    assert big["sketch"] == gs.GS_SKETCH_GATHER and big["packed_lists"] == 1 and big["prune"] == 1
+    assert big["segments"] == 1 and big["row_copy"] == 0 and big["tiles"] % 5 == 0
+    assert big["tile_width"] * (big["tiles"] // 5) >= 100_000  # the tiles of a row cover its columns
+    small = gs.GsContext(10_000, 4, 5, 1000, 10, hp).describe()  # worker-major: the interleaved copy
+    assert small["prune"] == 0 and small["row_copy"] == 1 and small["segments"] >= 1
+    monkeypatch.setenv("GS_SELECT_PATH", "pruned")
+    assert gs.GsContext(10_000, 4, 5, 1000, 10, hp).describe()["prune"] == 1
+    monkeypatch.setenv("GS_SKETCH_PATH", "atomic")
+    atomic = gs.GsContext(10_000, 4, 5, 1000, 10, hp).describe()
+    assert atomic["sketch"] == gs.GS_SKETCH_ATOMIC and atomic["tiles"] == 0
+    monkeypatch.setenv("GS_SKETCH_PATH", "unpacked")
+    assert gs.GsContext(10_000, 4, 5, 1000, 10, hp).describe()["packed_lists"] == 0
+
+
 def test_single_huge_coordinate():
     d, P, r, c, k = 200_000, 4, 5, 2000, 10
     hp = synth.hash_params(synth.BASE_SEED + 6, r)
