@@ -118,7 +118,9 @@ typedef struct gs_ctx gs_ctx; /* opaque: a copy of the config plus device scratc
  * tolerance). A selection without an estimate vector prunes (estimates only coordinates
  * with enough heavy cells) when d*r exceeds 2,000,000 and estimates every coordinate
  * otherwise; GS_SELECT_PATH=pruned or =full fixes that choice (the selected set is the same
- * either way).
+ * either way); GS_EMIT_SPIN=n bounds how long the selection's last kernel waits on the
+ * counts of its earlier workgroups before counting their bitmap words itself (0 or negative:
+ * sooner or always; the same indices either way, for tests).
  * Device scratch is about (16 + 4.1 r) d + 8 S P r c bytes (S list segments per tile, 1
  * unless the sketch is small), plus the 4 PP d bytes of the interleaved copy (PP = P rounded
  * up to 4) in a worker-major context with P > 1 or with GS_OPT_ROW_COPY, plus 2 r d bytes while the

@@ -219,6 +219,10 @@ gs_status gs_create(const gs_config* cfg, gs_ctx** out) {
     const char* sel = std::getenv("GS_SELECT_PATH");
     if (sel && std::strcmp(sel, "pruned") == 0) x->prune_min_cells = 0;
     if (sel && std::strcmp(sel, "full") == 0) x->prune_min_cells = INT64_MAX;
+    // GS_EMIT_SPIN=n bounds the emit's look-back polls (0: count directly as soon as a
+    // predecessor has not published; negative: always count directly), for tests
+    const char* spin = std::getenv("GS_EMIT_SPIN");
+    if (spin) x->emit_spin = std::atoi(spin);
   }
   if (x->use_pull) {
     x->list_cap = (int64_t)x->r * x->d + (int64_t)gs::kListGroup * x->plan.T;

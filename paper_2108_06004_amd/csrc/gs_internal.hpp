@@ -49,7 +49,9 @@ struct SelectBufs {
   uint32_t* bitmap;     // [ceil(d/32)] output bitmap
   unsigned long long* emit_flags;  // [emit_blocks] look-back words of the emit (zero before it)
   int64_t emit_blocks;
+  int emit_spin;        // polls of the emit's look-back before counting directly (< 0: never look back)
 };
+constexpr int kEmitSpinDefault = 1 << 20;
 constexpr int kSampleMax = 16384;  // sampled estimates for the pruning bound
 constexpr int64_t kPruneMinCells = 2000000;  // d*r below which the full estimate is faster (measured)
 
@@ -130,6 +132,7 @@ struct gs_ctx {
   int64_t prune_coarse_words = 0;
   int prune_buf_cap = 0;            // LDS candidate buffer entries of the pruned pass
   int64_t emit_blocks = 0;
+  int emit_spin = gs::kEmitSpinDefault;  // diagnostic override: GS_EMIT_SPIN
   // selections without an estimate vector prune when d*r exceeds this (0: always); below it
   // the full estimate takes fewer launches than the pruned pass's chain
   int64_t prune_min_cells = 0;
@@ -166,7 +169,8 @@ inline StateView state_view(const gs_ctx* x) {
 inline StateView worker_major_view(const gs_ctx* x) { return StateView{x->d, 1}; }
 inline SelectBufs select_bufs(const gs_ctx* x) {
   return SelectBufs{x->cand_key, x->cand_idx, x->cand_cap, x->keys,   x->stage_idx, x->hist,
-                    x->hist2,    x->hist_c,   x->ctl,      x->bitmap, x->emit_flags, x->emit_blocks};
+                    x->hist2,    x->hist_c,   x->ctl,      x->bitmap, x->emit_flags, x->emit_blocks,
+                    x->emit_spin};
 }
 
 constexpr int kStageMarks = 6;  // events per timed step: before stage 0, after stages 0..4

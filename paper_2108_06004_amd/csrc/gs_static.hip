@@ -128,7 +128,8 @@ extern "C" gs_status gs_unsketch_topk_static(const gs_config* cfg, void* stream,
                             reinterpret_cast<gs::SelectCtl*>(base + kCtl),
                             base + kBitmap,
                             reinterpret_cast<unsigned long long*>(base + kFlags),
-                            gs::emit_blocks_for(d)};
+                            gs::emit_blocks_for(d),
+                            gs::kEmitSpinDefault};
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   e = gs::launch_fill_zero(s, reinterpret_cast<float*>(base + kZero), kZeroWords);  // a kernel, not a memset
   if (e == hipSuccess) e = gs::launch_unsketch_topk_dense(hs, d, num_cus, bufs, s, merged, k, est, idx);

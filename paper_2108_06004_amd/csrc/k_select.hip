@@ -876,10 +876,10 @@ __global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* _
 // relaxed device-scope loads and stores of the word suffice (no fence orders other data).
 constexpr unsigned long long kFlagAgg = 1ull << 62, kFlagIncl = 2ull << 62;
 constexpr unsigned long long kFlagCount = 0xffffffffull;
-// Polls of a window of predecessors' words before the block counts the bitmap words before
-// its own directly (the blocks start in ticket order, so a predecessor is running and
-// publishes without waiting on later blocks; the bound makes every wait finite regardless).
-constexpr int kEmitSpin = 1 << 20;
+// A block polls a window of predecessors' words at most spin_max times before it counts the
+// bitmap words before its own directly (the blocks start in ticket order, so a predecessor is
+// running and publishes without waiting on later blocks; the bound makes every wait finite
+// regardless). spin_max < 0: every block counts directly.
 
 __device__ __forceinline__ unsigned long long flag_load(const unsigned long long* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -895,7 +895,7 @@ __device__ __forceinline__ void flag_store(unsigned long long* p, unsigned long 
 __global__ void __launch_bounds__(kSelBlock) k_emit(const uint32_t* __restrict__ bitmap, int64_t words,
                                                     SelectCtl* __restrict__ ctl,
                                                     unsigned long long* __restrict__ flags,
-                                                    int32_t* __restrict__ idx, uint32_t k) {
+                                                    int32_t* __restrict__ idx, uint32_t k, int spin_max) {
   __shared__ uint32_t shw[kSelBlock / 64];
   __shared__ uint32_t sb, sexcl, sdirect;
   if (threadIdx.x == 0) {
@@ -918,8 +918,8 @@ __global__ void __launch_bounds__(kSelBlock) k_emit(const uint32_t* __restrict__
     const int lane = threadIdx.x;
     if (lane == 0) flag_store(&flags[b], (b == 0 ? kFlagIncl : kFlagAgg) | total);
     uint32_t excl = 0;
-    bool direct = false;
-    for (int64_t top = b - 1; top >= 0; top -= 64) {
+    bool direct = spin_max < 0 && b > 0;
+    for (int64_t top = direct ? -1 : b - 1; top >= 0; top -= 64) {
       const int64_t j = top - lane;  // lane 0 is the nearest predecessor
       unsigned long long f = j >= 0 ? flag_load(&flags[j]) : kFlagIncl;  // before block 0: 0
       uint64_t incl_lanes, need;
@@ -928,7 +928,7 @@ __global__ void __launch_bounds__(kSelBlock) k_emit(const uint32_t* __restrict__
         // lanes up to the nearest inclusive word must have published
         need = incl_lanes ? ((2ull << __builtin_ctzll(incl_lanes)) - 1ull) : ~0ull;
         if ((__ballot(f == 0ull) & need) == 0ull) break;
-        if (spin == kEmitSpin) {
+        if (spin >= spin_max) {
           direct = true;
           break;
         }
@@ -1167,7 +1167,7 @@ hipError_t launch_select_tail(int64_t d, int num_cus, const SelectBufs& b, hipSt
   hipLaunchKernelGGL(k_mark, dim3(num_cus), dim3(kBlock), 0, s, b.keys, b.stage_idx, b.ctl, b.bitmap);
   const int64_t words = (d + 31) / 32;
   hipLaunchKernelGGL(k_emit, dim3((unsigned)b.emit_blocks), dim3(kSelBlock), 0, s, b.bitmap, words, b.ctl,
-                     b.emit_flags, idx, (uint32_t)k);
+                     b.emit_flags, idx, (uint32_t)k, b.emit_spin);
   return hipGetLastError();
 }
 

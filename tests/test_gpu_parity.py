@@ -408,6 +408,22 @@ def test_unpacked_lists(monkeypatch, d, P, r, c, k):
     dv.close()
 
 
+@pytest.mark.parametrize("spin", ["0", "-1"])
+def test_emit_counts_earlier_words_itself(monkeypatch, spin):
+    # the emit's workgroups take their output offset from the counts their predecessors
+    # publish; with GS_EMIT_SPIN=0 a workgroup whose predecessors have not published yet, and
+    # with -1 every workgroup, counts the earlier bitmap words itself: the same indices
+    monkeypatch.setenv("GS_EMIT_SPIN", spin)
+    d, P, r, c, k = 4_200_000, 2, 3, 150_000, 9_000  # 33 emit workgroups
+    hp = synth.hash_params(synth.BASE_SEED + 45, r)
+    rng = np.random.default_rng(45)
+    dv = Dev(d, P, r, c, k, hp, 0.9)
+    g = rng.laplace(0, 1e-2, (P, d)).astype(np.float32)
+    z = np.zeros_like(g)
+    chain_check(dv, g, z, z.copy(), k, 0.9, label=f"emit spin {spin}")
+    dv.close()
+
+
 def test_describe_reports_the_form_in_use(monkeypatch):
     monkeypatch.delenv("GS_SELECT_PATH", raising=False)  # the library's own size rule for pruning
     hp = synth.hash_params(synth.BASE_SEED + 44, 5)
