@@ -519,7 +519,7 @@ __device__ uint32_t sampled_bound(const uint32_t* __restrict__ sample, int M, ui
 
 // Heavy-cell bitmap: bit j * hrow + col (rows padded to hrow bits, a multiple of 64, so a
 // row starts on a word) is |merged[j][col]| >= tau0, or (HEAVYMIX,
-// hm = 1) merged[e]^2 >= theta in fp64 (one ballot per 64 cells); with hm the sampled fill
+// hm = 1) merged[j][col]^2 >= theta in fp64 (one ballot per 64 cells); with hm the sampled fill
 // bound tau0 is still found here, for the pruned pass. A coordinate with
 // est^2 >= theta has ceil(r/2) cells with |cell| >= |est| (see the pruned pass), and the
 // squares of fp32 values are exact in fp64, so those cells pass the same test.
@@ -621,7 +621,7 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
   // coordinates per lane per pass: independent hash chains in flight (two registers each per
   // row, so fewer with many rows, where four would spill)
   constexpr int U = R <= 8 ? 4 : R <= 12 ? 2 : 1;
-  // flat cell index j*c + col; below 2^32 whenever a map fits in LDS
+  // map index j * hrow + col of a cell; below 2^32 whenever a map fits in LDS
   using Cell = typename std::conditional<MAP == kMapGlobal, uint64_t, uint32_t>::type;
   // LDS: [map words][buf_cap queue entries][2 counters], one static array, so a lookup's
   // address is known at compile time to need no base added
@@ -688,7 +688,7 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
     const uint32_t cn = cb[j][m] + (wrap ? dc2[j] : dc1[j]);
     cb[j][m] = min(cn, cn - kr[j].c);  // cn < 2c: one subtraction, unsigned
   };
-  // byte offset of row j's map words (rows padded to hrow bits, hrow a multiple of 64)
+  // words per map row (rows padded to hrow bits, hrow a multiple of 64)
   const uint32_t hrow32 = (uint32_t)(hrow >> 5);
   for (int64_t base = base0; base < d; base += stride) {  // block-uniform
     // HEAVYMIX: the draws are loaded first, so their memory latency overlaps the lookups
@@ -714,8 +714,8 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
           const uint32_t col = cb[j][m];
           advance(j, m);
           ev[j] = (Cell)j * (Cell)hrow + col;
-          const uint32_t cb = ev[j] >> coarse_log2;
-          const uint32_t bit = bit_at(sm[cb >> 5], cb);
+          const uint32_t cbit = ev[j] >> coarse_log2;
+          const uint32_t bit = bit_at(sm[cbit >> 5], cbit);
           cset |= bit << j;
           nset += bit;
         }
