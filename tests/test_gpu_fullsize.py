@@ -8,7 +8,8 @@ the oracle's k-th |estimate|, the gathered values and the reset state bit for bi
   * d = 25.6M, P = 8, r = 5, c = 256,000, k = 25,600: all 5 steps, the GPU re-synced from
     the oracle's state before each step; then the fused step run free for all 5 steps next
     to the oracle run on its own (the selections' differences are reported and bounded).
-  * d = 66M, P = 16, r = 7, c = 1,320,000, k = 66,000: step 0 (about 50 GB of host memory).
+  * d = 66M, P = 16, r = 7, c = 1,320,000, k = 66,000: all 3 steps, re-synced from the oracle's
+    state before each step (about 50 GB of host memory).
 """
 import numpy as np
 import pytest
@@ -59,11 +60,13 @@ def test_benchmark_workload_free_running_interleaved():
     dv.close()
 
 
-def test_rowsparse_workload_step0_interleaved_full():
+def test_rowsparse_workload_all_steps_interleaved():
     w = synth.WORKLOADS["rowsparse-d66M-P16"]
     hp = synth.hash_params(w)
     dv = Dev(w.d, w.P, w.r, w.c, w.k, hp, w.rho, layout=IL)
-    z = np.zeros((w.P, w.d), np.float32)
-    chain_check(dv, synth.gradients(w, 0), z, z.copy(), w.k, w.rho, full_tables=True, fused=True,
-                label=f"{w.name} interleaved step 0")
+    u = np.zeros((w.P, w.d), np.float32)
+    v = np.zeros((w.P, w.d), np.float32)
+    for t in range(w.steps):
+        u, v = chain_check(dv, synth.gradients(w, t), u, v, w.k, w.rho, full_tables=True, fused=True,
+                           label=f"{w.name} interleaved step {t}")
     dv.close()
