@@ -124,7 +124,8 @@ def stage_kernels(w, layout: str = "interleaved", plan: dict = None) -> dict:
     `plan` is the context's gs_describe; without it the library's size rule is assumed (list
     segments only for small sketches)."""
     if layout == "interleaved":
-        acc = [f"k_accumulate_il<{w.P // 4}>"]
+        ragged = "true" if w.d % (64 // (w.P // 4)) else "false"  # the last chunk of 64 / G coordinates
+        acc = [f"k_accumulate_il<{w.P // 4}, {ragged}>"]
     elif w.P == 1:
         acc = ["k_accumulate4"]
     else:

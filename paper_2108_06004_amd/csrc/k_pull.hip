@@ -250,8 +250,9 @@ __global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int6
 // l/G and piece h = l%G (workers 4h .. 4h+3). So the worker-major loads and stores are 4
 // bytes per lane and 4*CW contiguous bytes per worker row and instruction, and the vI
 // stores 16 bytes per lane, 16*CW*G contiguous bytes per instruction. Each pass a wave takes
-// U consecutive chunks, all in flight together. Workers past P read nothing and write 0 into
-// vI. Full chunks only; the tail goes to k_accumulate_vi_any.
+// U consecutive chunks, all in flight together; the chunks past the last such group, the
+// ragged last one included (lanes past d take no coordinate), run one at a time. Workers past
+// P read nothing and write 0 into vI.
 template <int P, bool ACC>
 __global__ void __launch_bounds__(kBlock) k_vi_il(const float* __restrict__ g, float* __restrict__ u,
                                                   float* __restrict__ v, float* __restrict__ vI, int64_t d,
@@ -264,11 +265,11 @@ __global__ void __launch_bounds__(kBlock) k_vi_il(const float* __restrict__ g, f
   if (lane >= CW * G) return;  // G = 3: one idle lane per wave (no barrier below)
   const int h = lane % G;
   const int64_t sub = lane / G;
-  const int64_t nch = d / CW;
-  const int64_t ngr = nch / U;
+  const int64_t nch = (d + CW - 1) / CW;
+  const int64_t ngr = (d / CW) / U;  // groups of U full chunks
   const int64_t wstride = (int64_t)gridDim.x * (kBlock / 64);
   const int64_t w0 = (int64_t)blockIdx.x * (kBlock / 64) + (threadIdx.x >> 6);
-  // one pass over n consecutive chunks starting at chunk c0
+  // one pass over n consecutive chunks starting at chunk c0 (this lane's coordinate in each)
   auto pass = [&](int64_t c0, auto n_const) {
     constexpr int N = decltype(n_const)::value;
     float x[N][4], uu[N][4], gg[N][4];
@@ -314,7 +315,8 @@ __global__ void __launch_bounds__(kBlock) k_vi_il(const float* __restrict__ g, f
     }
   };
   for (int64_t gr = w0; gr < ngr; gr += wstride) pass(gr * U, std::integral_constant<int, U>());
-  for (int64_t ch = ngr * U + w0; ch < nch; ch += wstride) pass(ch, std::integral_constant<int, 1>());
+  for (int64_t ch = ngr * U + w0; ch < nch; ch += wstride)
+    if (ch * CW + sub < d) pass(ch, std::integral_constant<int, 1>());
 }
 
 // Generic (any P, any d, any alignment): one lane per (coordinate, worker).
@@ -645,21 +647,13 @@ __global__ void __launch_bounds__(kBlock) k_merge_partials_any(const double* __r
   }
 }
 
-// k_vi_il over the full chunks, then k_accumulate_vi_any for the rest; g and u only with ACC.
+// k_vi_il over every chunk (the last one may be ragged); g and u only with ACC.
 template <int P, bool ACC>
 hipError_t launch_vi_il_p(const gs_ctx* x, hipStream_t s, const float* g, float* u, float* v) {
   constexpr int CW = 64 / (((P + 3) & ~3) / 4);
-  const int64_t nch = x->d / CW;
-  if (nch > 0) {
-    const dim3 grid(grid_for(nch, 4 * (kBlock / 64), 64 * x->num_cus)), block(kBlock);
-    hipLaunchKernelGGL((k_vi_il<P, ACC>), grid, block, 0, s, g, u, v, x->vI, x->d, x->rho);
-  }
-  const int64_t done = nch * CW;
-  if (done < x->d) {
-    const int64_t n = (int64_t)P * (x->d - done);
-    hipLaunchKernelGGL(k_accumulate_vi_any, dim3(grid_for(n, kBlock, 8 * x->num_cus)), dim3(kBlock), 0, s, g, u, v,
-                       x->vI, x->d, P, x->plan.PP, x->rho, ACC ? 1 : 0, done);
-  }
+  const int64_t nch = (x->d + CW - 1) / CW;
+  const dim3 grid(grid_for(nch, 4 * (kBlock / 64), 64 * x->num_cus)), block(kBlock);
+  hipLaunchKernelGGL((k_vi_il<P, ACC>), grid, block, 0, s, g, u, v, x->vI, x->d, x->rho);
   return hipGetLastError();
 }
 

@@ -525,6 +525,7 @@ __device__ uint32_t sampled_bound(const uint32_t* __restrict__ sample, int M, ui
 // squares of fp32 values are exact in fp64, so those cells pass the same test.
 // Every block first finds tau0 itself (the sampled keys are read from L2; block 0 records
 // it and resets the selection counters), so no single-block kernel runs in between.
+constexpr int kHeavyUnroll = 8;  // 64-cell groups per wave and pass of k_heavy
 __global__ void __launch_bounds__(kSelBlock) k_heavy(const float* __restrict__ merged, int64_t c, int64_t hrow,
                                                   int r,
                                                   SelectCtl* __restrict__ ctl, uint32_t* __restrict__ heavy,
@@ -542,20 +543,34 @@ __global__ void __launch_bounds__(kSelBlock) k_heavy(const float* __restrict__ m
     ctl->fallback = 0u;
   }
   const double theta = ctl->theta;
-  const int64_t stride = (int64_t)gridDim.x * kSelBlock;
-  const int64_t n = (int64_t)r * hrow;  // bits of the padded map; hrow is a multiple of 64
-  for (int64_t base = ((int64_t)blockIdx.x * kSelBlock + threadIdx.x) & ~63ll; base < n; base += stride) {
-    const int64_t j = base / hrow;  // one row per wave (64-bit aligned bases)
-    const int64_t col = base - j * hrow + (threadIdx.x & 63);
-    bool hv = false;
-    if (col < c) {
-      const float x = merged[j * c + col];
-      hv = hm ? (double)x * (double)x >= theta : abs_key(x) >= tau0;
+  // The map in groups of 64 cells (one ballot, two words each; hrow is a multiple of 64, so a
+  // group lies in one row). A wave takes UH consecutive groups per pass with all their loads
+  // in flight together. r <= 16 and hrow <= 2^31 keep group indices below 2^29.
+  constexpr int UH = kHeavyUnroll;
+  const uint32_t gpr = (uint32_t)(hrow >> 6);  // groups per row
+  const int64_t ng = ((int64_t)r * hrow) >> 6;
+  const int lane = threadIdx.x & 63;
+  const int64_t wv = ((int64_t)blockIdx.x * kSelBlock + threadIdx.x) >> 6;
+  const int64_t nwv = ((int64_t)gridDim.x * kSelBlock) >> 6;
+  for (int64_t g0 = wv * UH; g0 < ng; g0 += nwv * UH) {
+    float x[UH];
+    bool in[UH];
+#pragma unroll
+    for (int q = 0; q < UH; ++q) {
+      const uint32_t gi = (uint32_t)(g0 + q);
+      const uint32_t j = gi / gpr;
+      const int64_t col = (int64_t)(gi - j * gpr) * 64 + lane;
+      in[q] = g0 + q < ng && col < c;
+      x[q] = in[q] ? merged[(int64_t)j * c + col] : 0.f;
     }
-    const uint64_t m = __ballot(hv);
-    if ((threadIdx.x & 63) == 0) {
-      heavy[(base >> 5)] = (uint32_t)m;
-      heavy[(base >> 5) + 1] = (uint32_t)(m >> 32);
+#pragma unroll
+    for (int q = 0; q < UH; ++q) {
+      const bool hv = in[q] && (hm ? (double)x[q] * (double)x[q] >= theta : abs_key(x[q]) >= tau0);
+      const uint64_t m = __ballot(hv);
+      if (lane == 0 && g0 + q < ng) {
+        heavy[2 * (g0 + q)] = (uint32_t)m;
+        heavy[2 * (g0 + q) + 1] = (uint32_t)(m >> 32);
+      }
     }
   }
 }
@@ -1126,7 +1141,7 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
   hipLaunchKernelGGL((k_sample<R, HM>), dim3((M + kBlock - 1) / kBlock), dim3(kBlock), 0, s, x->hs, merged, x->d, M,
                      rnd, x->sample_keys, x->hist_s);
   const int64_t nbits = (int64_t)x->r * x->heavy_row;  // heavy-cell map bits (padded rows)
-  hipLaunchKernelGGL(k_heavy, dim3(grid_for(nbits, kSelBlock, x->num_cus)), dim3(kSelBlock), 0, s, merged, x->c,
+  hipLaunchKernelGGL(k_heavy, dim3(grid_for(nbits, kSelBlock * kHeavyUnroll, x->num_cus)), dim3(kSelBlock), 0, s, merged, x->c,
                      x->heavy_row, x->r, x->ctl,
                      x->heavy, HM ? 1 : 0, x->sample_keys, M, (uint32_t)rho_d, (uint32_t)k, x->hist_s);
   // with the bitmap in LDS one block fits a CU: launch one per CU so the map is loaded once

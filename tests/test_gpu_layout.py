@@ -47,6 +47,9 @@ EDGE = [
     (5_003, 12, 5, 300, 50),     # P = 12: three 16-byte groups per row (one idle lane per wave)
     (6_007, 11, 3, 257, 33),     # P = 11: rows padded to 12 (generic accumulation, masked pull lanes)
     (4_097, 16, 3, 128, 40),     # P = 16: four groups, ragged tail of the 16-coordinate chunks
+    (5, 8, 3, 7, 2),             # P = 8: d below one 32-coordinate chunk (only the ragged one)
+    (100_003, 8, 5, 5_003, 300), # P = 8: groups of four chunks, single chunks, then the ragged one
+    (63, 4, 5, 17, 9),           # P = 4: d below one 64-coordinate chunk
     (3001, 17, 5, 97, 60),       # P beyond the unrolled pulls (rows of 20)
     (65_536, 4, 16, 4096, 655),  # P = 4: one group per coordinate, maximum r
 ]
