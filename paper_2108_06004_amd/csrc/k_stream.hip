@@ -79,20 +79,23 @@ __global__ void __launch_bounds__(kBlock) k_accumulate1(const float* __restrict_
 // the 16-byte group h = l%G of its row (workers 4h..4h+3), so consecutive lanes read and
 // write consecutive 16-byte pieces of u and v; the four gradient values come from four
 // worker rows of g (4-byte loads, 4*CW bytes contiguous per row and wave). Each pass a wave
-// takes four consecutive chunks, all in flight together, so when CW*4 bytes is less than a
-// 128-byte line (G = 3, 4) the rest of the line is read by the wave's next instruction.
-// The chunks past the last group of four run one at a time, and with RAGGED (d not a multiple
+// takes U consecutive chunks (four, eight for G = 4), all in flight together, so when CW*4
+// bytes is less than a 128-byte line (G = 3, 4) the rest of the line is read by the wave's
+// next instruction.
+// The chunks past the last group run one at a time, and with RAGGED (d not a multiple
 // of CW) the first wave then takes the partial last chunk, whose lanes past d take no
 // coordinate. The non-ragged form is kept free of that code: the compiler schedules this loop
 // differently when it is there, and the schedule it picks for G = 2 without it measured 2%
-// faster (0.650 against 0.662 ms at d = 25.6M x 8). For G = 4 the loads of a group are issued
-// before any arithmetic (a scheduling barrier): 3.92 against 3.97 ms at d = 66M x 16.
+// faster (0.650 against 0.662 ms at d = 25.6M x 8). For G = 4 a group is eight chunks, and its
+// loads are all issued before any arithmetic (a scheduling barrier): at d = 66M x 16 the
+// barrier took 3.97 to 3.89 ms and the eight chunks a further 1-2% (3.38 to 3.34 ms on a
+// faster part); eight chunks for G = 1, 2, or the barrier there, measured slower.
 template <int G, bool RAGGED>
 __global__ void __launch_bounds__(kBlock) k_accumulate_il(const float* __restrict__ g, float* __restrict__ u,
                                                           float* __restrict__ v, int64_t d, float rho) {
   constexpr int CW = 64 / G;
   constexpr int PP = 4 * G;
-  constexpr int U = 4;
+  constexpr int U = G == 4 ? 8 : 4;
   const int lane = threadIdx.x & 63;
   if (lane >= CW * G) return;  // G = 3: one idle lane per wave (no barrier below)
   const int h = lane % G;
