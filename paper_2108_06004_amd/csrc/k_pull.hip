@@ -250,9 +250,9 @@ __global__ void __launch_bounds__(64) k_build_fill(HashSet hs, PullPlan pl, int6
 // l/G and piece h = l%G (workers 4h .. 4h+3). So the worker-major loads and stores are 4
 // bytes per lane and 4*CW contiguous bytes per worker row and instruction, and the vI
 // stores 16 bytes per lane, 16*CW*G contiguous bytes per instruction. Each pass a wave takes
-// U consecutive chunks, all in flight together; the chunks past the last such group, the
-// ragged last one included (lanes past d take no coordinate), run one at a time. Workers past
-// P read nothing and write 0 into vI.
+// U consecutive chunks (U below), all in flight together; the chunks past the last such
+// group, the ragged last one included (lanes past d take no coordinate), run one at a time.
+// Workers past P read nothing and write 0 into vI.
 template <int P, bool ACC>
 __global__ void __launch_bounds__(kBlock) k_vi_il(const float* __restrict__ g, float* __restrict__ u,
                                                   float* __restrict__ v, float* __restrict__ vI, int64_t d,
@@ -260,7 +260,10 @@ __global__ void __launch_bounds__(kBlock) k_vi_il(const float* __restrict__ g, f
   constexpr int PP = (P + 3) & ~3;
   constexpr int G = PP / 4;
   constexpr int CW = 64 / G;
-  constexpr int U = 4;
+  // chunks per wave and pass: eight with the accumulation for P > 4 (worker-major step at
+  // d = 25.6M x 8: 0.947 -> 0.916 ms with the scheduling barrier below, 66M x 16: 6.61 ->
+  // 5.90 ms), else four (the interleave alone, and P <= 4, measured no better with eight)
+  constexpr int U = ACC && P > 4 ? 8 : 4;
   const int lane = threadIdx.x & 63;
   if (lane >= CW * G) return;  // G = 3: one idle lane per wave (no barrier below)
   const int h = lane % G;
@@ -292,6 +295,9 @@ __global__ void __launch_bounds__(kBlock) k_vi_il(const float* __restrict__ g, f
         }
       }
     }
+    // P = 5..8: every load of the pass issued before any arithmetic (measured faster there,
+    // slower for P = 16)
+    if constexpr (ACC && P > 4 && P <= 8) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int m = 0; m < N; ++m) {
       const int64_t i = (c0 + m) * CW + sub;

@@ -1141,9 +1141,9 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
   hipLaunchKernelGGL((k_sample<R, HM>), dim3((M + kBlock - 1) / kBlock), dim3(kBlock), 0, s, x->hs, merged, x->d, M,
                      rnd, x->sample_keys, x->hist_s);
   const int64_t nbits = (int64_t)x->r * x->heavy_row;  // heavy-cell map bits (padded rows)
-  hipLaunchKernelGGL(k_heavy, dim3(grid_for(nbits, kSelBlock * kHeavyUnroll, x->num_cus)), dim3(kSelBlock), 0, s, merged, x->c,
-                     x->heavy_row, x->r, x->ctl,
-                     x->heavy, HM ? 1 : 0, x->sample_keys, M, (uint32_t)rho_d, (uint32_t)k, x->hist_s);
+  hipLaunchKernelGGL(k_heavy, dim3(grid_for(nbits, kSelBlock * kHeavyUnroll, x->num_cus)), dim3(kSelBlock), 0, s,
+                     merged, x->c, x->heavy_row, x->r, x->ctl, x->heavy, HM ? 1 : 0, x->sample_keys, M,
+                     (uint32_t)rho_d, (uint32_t)k, x->hist_s);
   // with the bitmap in LDS one block fits a CU: launch one per CU so the map is loaded once
   const int pgrid = grid_for(x->d, 4 * kPruneBlock, x->prune_map_in_lds ? x->num_cus : 2 * x->num_cus);
   const dim3 pb(kPruneBlock);
