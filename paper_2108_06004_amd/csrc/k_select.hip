@@ -550,18 +550,23 @@ __global__ void __launch_bounds__(kSelBlock) k_heavy(const float* __restrict__ m
   const uint32_t gpr = (uint32_t)(hrow >> 6);  // groups per row
   const int64_t ng = ((int64_t)r * hrow) >> 6;
   const int lane = threadIdx.x & 63;
-  const int64_t wv = ((int64_t)blockIdx.x * kSelBlock + threadIdx.x) >> 6;
+  // wave index, the same in every lane (a scalar)
+  const int64_t wv = __builtin_amdgcn_readfirstlane((uint32_t)(((int64_t)blockIdx.x * kSelBlock + threadIdx.x) >> 6));
   const int64_t nwv = ((int64_t)gridDim.x * kSelBlock) >> 6;
   for (int64_t g0 = wv * UH; g0 < ng; g0 += nwv * UH) {
     float x[UH];
     bool in[UH];
+    // row j and group-in-row rr of group g0 + q, advanced one group at a time
+    uint32_t j = (uint32_t)g0 / gpr, rr = (uint32_t)g0 - j * gpr;
 #pragma unroll
     for (int q = 0; q < UH; ++q) {
-      const uint32_t gi = (uint32_t)(g0 + q);
-      const uint32_t j = gi / gpr;
-      const int64_t col = (int64_t)(gi - j * gpr) * 64 + lane;
+      const int64_t col = (int64_t)rr * 64 + lane;
       in[q] = g0 + q < ng && col < c;
       x[q] = in[q] ? merged[(int64_t)j * c + col] : 0.f;
+      if (++rr == gpr) {
+        rr = 0;
+        ++j;
+      }
     }
 #pragma unroll
     for (int q = 0; q < UH; ++q) {
