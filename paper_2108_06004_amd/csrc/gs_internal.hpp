@@ -85,6 +85,9 @@ struct PullPlan {
   uint32_t w_magic, w_shift;
   double inv_c;
   int32_t tile_bits;
+  // LDS cell of position t in row j's tiles: t ^ ((t >> swz[j]) & 31) when swz[j] > 0, else t
+  // (see tile_cell); a worker's column of cells is W rounded up to 32, plus 6, long.
+  int32_t swz[kMaxRows];
 };
 constexpr int kListGroup = 64;
 constexpr int64_t kMaxFillLds = 160 * 1024;  // LDS of the list-fill kernel holds T cursors

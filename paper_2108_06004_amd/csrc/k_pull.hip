@@ -92,6 +92,15 @@ __device__ __forceinline__ uint32_t column_at(const HashSet& hs, const PullPlan&
   return (uint32_t)(((uint64_t)pl.theta_inv[j] * (uint64_t)(k * pl.W + pos)) % hs.c);
 }
 
+// LDS cell of tile position t. A row whose common step between consecutive coordinates is a
+// multiple of 2^s (s >= 5) would put a run's cells t, t + step, ... in one LDS bank;
+// XOR-ing the low five bits with bits s .. s + 4 (which advance by an odd amount each step)
+// spreads them over all banks. Only the low five bits change, each by higher bits alone, so
+// the map is a bijection on every aligned block of 32 cells.
+__device__ __forceinline__ uint32_t tile_cell(uint32_t t, int swz) {
+  return swz ? t ^ ((t >> swz) & 31u) : t;
+}
+
 // ------------------------------------------------------------------------------------
 // Static list build (gs_create).
 
@@ -448,11 +457,15 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   const int j = (int)(t / pl.tiles_per_row);
   const int64_t kt = t - (int64_t)j * pl.tiles_per_row;
   const int64_t wt = min((int64_t)pl.W, (int64_t)hs.c - kt * pl.W);
-  for (int64_t e = threadIdx.x; e < wt * P; e += kPullBlock) acc[e] = 0.0;
+  // column stride: whole blocks of 32 cells (for the swizzle) plus 6, so that the two or four
+  // workers' columns one wave instruction adds into start in different banks
+  const int64_t ws = ((wt + 31) & ~31ll) + 6;
+  const int swz = pl.swz[j];
+  for (int64_t e = threadIdx.x; e < ws * P; e += kPullBlock) acc[e] = 0.0;
   __syncthreads();
   int64_t e0, e1;
   segment_bounds(off[t], tn[t], s, pl.S, e0, e1);
-  double* const mycol = acc + (int64_t)(4 * sub) * wt;
+  double* const mycol = acc + (int64_t)(4 * sub) * ws;
   // when L does not divide the block (L = 3: 85 groups of 3 lanes), the last lane has no
   // group: it takes no entry (its would be the next pass's first)
   int64_t eb = tid0 < B ? e0 + tid : e1;
@@ -494,12 +507,12 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
       if (more) fetch(ebn);
 #pragma unroll
       for (int m = 0; m < U; ++m) {
-        double* cell = mycol + pos[m];
+        double* cell = mycol + tile_cell(pos[m], swz);
         const uint32_t sflip = sg[m];
         const float xs[4] = {x[m].x, x[m].y, x[m].z, x[m].w};
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-          if (P % 4 == 0 || 4 * sub + q < P) atomicAdd(cell + q * wt, (double)apply_sign(xs[q], sflip));
+          if (P % 4 == 0 || 4 * sub + q < P) atomicAdd(cell + q * ws, (double)apply_sign(xs[q], sflip));
       }
       eb = ebn;
       if (!more) break;
@@ -515,23 +528,23 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
     for (int m = 0; m < U; ++m) x[m] = load_quad<P, FLAT>(vI, i[m], sub);
 #pragma unroll
     for (int m = 0; m < U; ++m) {
-      double* cell = mycol + pos[m];
+      double* cell = mycol + tile_cell(pos[m], swz);
       const uint32_t sflip = sg[m];
       const float xs[4] = {x[m].x, x[m].y, x[m].z, x[m].w};
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        if (P % 4 == 0 || 4 * sub + q < P) atomicAdd(cell + q * wt, (double)apply_sign(xs[q], sflip));
+        if (P % 4 == 0 || 4 * sub + q < P) atomicAdd(cell + q * ws, (double)apply_sign(xs[q], sflip));
     }
   }
   for (; eb < e1; eb += B) {
     uint32_t i, pos, sflip;
     decode_entry<PK>(list[eb], PK ? bases[eb / kListGroup] : (uint32_t)codes[eb], pl.off_bits, i, pos, sflip);
     const f4 x = load_quad<P, FLAT>(vI, i, sub);
-    double* cell = mycol + pos;
+    double* cell = mycol + tile_cell(pos, swz);
     const float xs[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      if (P % 4 == 0 || 4 * sub + q < P) atomicAdd(cell + q * wt, (double)apply_sign(xs[q], sflip));
+      if (P % 4 == 0 || 4 * sub + q < P) atomicAdd(cell + q * ws, (double)apply_sign(xs[q], sflip));
   }
   __syncthreads();
   // write out: tile position o holds column theta_inv_j * (kt W + o) mod c; along the
@@ -544,8 +557,9 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   if (pl.S == 1 && (merged || tables)) {
     for (int64_t o = threadIdx.x; o < wt; o += kPullBlock) {
       float x[P];
+      const uint32_t oc = tile_cell((uint32_t)o, swz);
 #pragma unroll
-      for (int q = 0; q < P; ++q) x[q] = (float)acc[q * wt + o];
+      for (int q = 0; q < P; ++q) x[q] = (float)acc[q * ws + oc];
       if (tables) {
 #pragma unroll
         for (int q = 0; q < P; ++q) tables[q * rc + row0 + col] = x[q];
@@ -557,8 +571,9 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
   }
   double* dst = partial + s * P * rc + row0;
   for (int64_t o = threadIdx.x; o < wt; o += kPullBlock) {
+    const uint32_t oc = tile_cell((uint32_t)o, swz);
 #pragma unroll
-    for (int q = 0; q < P; ++q) dst[q * rc + col] = acc[q * wt + o];
+    for (int q = 0; q < P; ++q) dst[q * rc + col] = acc[q * ws + oc];
     col = col + cstep >= c ? col + cstep - c : col + cstep;
   }
 }
@@ -667,7 +682,7 @@ template <int P, bool FLAT = false>
 void launch_pull_p(const gs_ctx* x, hipStream_t s, const float* rows, float* merged, float* tables) {
   const PullPlan& pl = x->plan;
   const dim3 grid((unsigned)((int64_t)pl.T * pl.S)), block(kPullBlock);
-  const size_t lds = (size_t)pl.W * pl.P * sizeof(double);
+  const size_t lds = (size_t)(((pl.W + 31) & ~31) + 6) * pl.P * sizeof(double);
   if (pl.packed)
     hipLaunchKernelGGL((k_pull<P, pull_unroll(P), true, FLAT>), grid, block, lds, s, x->hs, pl, x->list, x->codes,
                        x->bases, x->tile_off, x->tile_n, rows, x->partial, merged, tables);
@@ -720,6 +735,8 @@ uint64_t gcd_u64(uint64_t a, uint64_t b) {
 // (a fraction f = a / p of the steps). theta (coprime to c) minimises the expected step
 // (1 - f) |theta alpha|_c + f |theta (alpha - beta)|_c of the scaled position, |x|_c being the
 // distance of x mod c to 0. The search runs over theta < min(c, 2^22) with adds only.
+// (Minimising instead the chance that a step leaves a tile, (1 - f) min(1, d1 / W) +
+// f min(1, d2 / W), measured 10% slower at d = 66M x 16 and no faster at 25.6M x 8.)
 uint32_t column_scaling(uint32_t a, int64_t c) {
   if (c <= 2) return 1;
   const uint64_t cu = (uint64_t)c;
@@ -746,6 +763,25 @@ uint32_t column_scaling(uint32_t a, int64_t c) {
   return best_theta;
 }
 
+// The LDS swizzle of a row (tile_cell): the step between consecutive coordinates that most
+// of them take, (1 - f) of them theta alpha and f of them theta (alpha - beta), at distance d
+// from 0 mod c; when d is a multiple of 32, consecutive coordinates of a run land in one bank
+// (2^s cells apart, s = the trailing zero bits of d), and XOR-ing in bits s .. s + 4 spreads
+// them. (Steps of an odd multiple of 16 alternate between two banks; the swizzle measured
+// slower there.)
+int32_t cell_swizzle(uint32_t a, int64_t c, uint32_t theta) {
+  if (c <= 2) return 0;
+  const uint64_t cu = (uint64_t)c;
+  const uint64_t alpha = a % cu, beta = (uint64_t)kMersenne % cu;
+  const uint64_t step = a <= kMersenne / 2 ? alpha : (alpha + cu - beta) % cu;  // the common step
+  const uint64_t t = (uint64_t)theta % cu * step % cu;
+  const uint64_t dist = t < cu - t ? t : cu - t;
+  if (dist == 0) return 0;
+  int s = 0;
+  while (((dist >> s) & 1ull) == 0ull) ++s;
+  return s >= 5 ? (s > 26 ? 26 : s) : 0;
+}
+
 }  // namespace
 
 PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int64_t c, int num_cus) {
@@ -753,6 +789,7 @@ PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int6
   for (int j = 0; j < r; ++j) {
     pl.theta[j] = column_scaling(hs.row[j].a, c);
     pl.theta_inv[j] = inverse_mod(pl.theta[j] % (uint32_t)c, (uint32_t)c);
+    pl.swz[j] = cell_swizzle(hs.row[j].a, c, pl.theta[j]);
   }
   pl.P = P;
   pl.PP = (P + 3) & ~3;
@@ -760,7 +797,8 @@ PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int6
   // most 160 KiB / kTilesPerCu share a CU; W is then shrunk so that the tiles fill whole
   // rounds of resident workgroups (no ragged last round).
   const int64_t cu_lds = 160 * 1024;
-  const int64_t max_w = (cu_lds / kTilesPerCu) / (8 * (int64_t)P);
+  int64_t max_w = (cu_lds / kTilesPerCu) / (8 * (int64_t)P) - 6;
+  if (max_w >= 32) max_w &= ~31ll;  // a worker's column of cells is W rounded up to 32, plus 6
   int64_t W = max_w < 1 ? 1 : max_w;
   if (W > c) W = c;
   const int64_t slots = (int64_t)kTilesPerCu * num_cus;
@@ -816,7 +854,7 @@ PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int6
 }
 
 hipError_t prepare_pull_kernels(const gs_ctx* x) {
-  const size_t bytes = (size_t)x->plan.W * x->plan.P * sizeof(double);
+  const size_t bytes = (size_t)(((x->plan.W + 31) & ~31) + 6) * x->plan.P * sizeof(double);
   switch (x->P) {
 #define GS_ALLOW_CASE(PP) \
   case PP: return allow_pull_lds<PP>(bytes);
