@@ -95,8 +95,8 @@ __device__ __forceinline__ uint32_t column_at(const HashSet& hs, const PullPlan&
 // LDS cell of tile position t. A row whose common step between consecutive coordinates is a
 // multiple of 2^s would put a run's cells t, t + step, ... in 32 / 2^s of the 32 bank pairs
 // of fp64 cells; XOR-ing the low five bits with bits s .. s + 4 (which advance by an odd
-// amount each step) spreads them over all. Only the low five bits change, each by higher bits alone, so
-// the map is a bijection on every aligned block of 32 cells.
+// amount each step) spreads them over all. Only the low five bits change, bit i by bit i + s,
+// so the map is a bijection on every aligned block of 32 cells.
 __device__ __forceinline__ uint32_t tile_cell(uint32_t t, int swz) {
   return swz ? t ^ ((t >> swz) & 31u) : t;
 }
@@ -439,7 +439,7 @@ __global__ void __launch_bounds__(kPullBlock) k_pull(HashSet hs, PullPlan pl, co
                                                      const int64_t* __restrict__ off, const uint32_t* __restrict__ tn,
                                                      const float* __restrict__ vI, double* __restrict__ partial,
                                                      float* __restrict__ merged, float* __restrict__ tables) {
-  extern __shared__ double acc[];  // [P][W]: worker-major, so lanes adding for one worker hit spread banks
+  extern __shared__ double acc[];  // [P][ws] (below): worker-major, so lanes adding for one worker hit spread banks
   constexpr int PP = (P + 3) & ~3;
   constexpr int L = PP / 4;
   constexpr int64_t B = kPullBlock / L;  // entries per block pass
