@@ -639,8 +639,9 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
                                                    uint32_t* __restrict__ bitmap, const uint32_t* __restrict__ rnd,
                                                    uint32_t* __restrict__ hist_s) {
   // coordinates per lane per pass: independent hash chains in flight (two registers each per
-  // row, so fewer with many rows, where four would spill)
-  constexpr int U = R <= 8 ? 4 : R <= 12 ? 2 : 1;
+  // row, so fewer with many rows, where four would spill); six with the map in LDS and few
+  // rows (d = 25.6M x 8, r = 5: 71 -> 68.5 us; with the coarse map six measured no better)
+  constexpr int U = (MAP == kMapFine && R <= 6) ? 6 : R <= 8 ? 4 : R <= 12 ? 2 : 1;
   // map index j * hrow + col of a cell; below 2^32 whenever a map fits in LDS
   using Cell = typename std::conditional<MAP == kMapGlobal, uint64_t, uint32_t>::type;
   // LDS: [map words][buf_cap queue entries][2 counters], one static array, so a lookup's
