@@ -335,6 +335,31 @@ def test_edge_shapes(d, P, r, c, k):
     dv.close()
 
 
+@pytest.mark.parametrize("layout", ["worker_major", "interleaved"])
+def test_subnormal_values(layout):
+    # fp32 subnormals in the gradients and the state (a fifth of the entries, |x| < 2^-126),
+    # zeros and normal values mixed: the kernels keep subnormals (no flush to zero), so u and v
+    # stay bit-exact with the oracle, whose C arithmetic keeps them too, and small estimates
+    # still order correctly
+    d, P, r, c, k = 60_013, 4, 5, 1_500, 250
+    hp = synth.hash_params(synth.BASE_SEED + 29, r)
+    rng = np.random.default_rng(29)
+
+    def mix(shape, scale):
+        x = rng.laplace(0.0, scale, shape).astype(np.float32)
+        sub = rng.random(shape) < 0.2
+        x[sub] = (rng.uniform(-1.0, 1.0, int(sub.sum())) * 1e-39).astype(np.float32)
+        x[rng.random(shape) < 0.05] = 0.0
+        return x
+
+    dv = Dev(d, P, r, c, k, hp, 0.9, layout=layout)
+    u, v = mix((P, d), 1e-3), mix((P, d), 1e-3)
+    assert np.any((u != 0) & (np.abs(u) < np.finfo(np.float32).tiny)), "the state must hold subnormals"
+    for t in range(2):
+        u, v = chain_check(dv, mix((P, d), 1e-2), u, v, k, 0.9, label=f"subnormal {layout} t={t}")
+    dv.close()
+
+
 def test_all_zero_gradients_every_key_ties():
     d, P, r, c, k = 50_000, 4, 5, 1000, 333
     hp = synth.hash_params(synth.BASE_SEED + 5, r)
