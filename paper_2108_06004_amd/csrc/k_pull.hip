@@ -816,7 +816,7 @@ PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int6
   pl.PP = (P + 3) & ~3;
   // Tiles hold W columns x P workers of fp64 accumulators. Up to kTilesPerCu tiles of at
   // most 160 KiB / kTilesPerCu share a CU; W is then shrunk so that the tiles fill whole
-  // rounds of resident workgroups (no ragged last round).
+  // rounds of resident workgroups (no ragged last round), or one round as fully as it can.
   const int64_t cu_lds = 160 * 1024;
   int64_t max_w = (cu_lds / kTilesPerCu) / (8 * (int64_t)P) - 6;
   if (max_w >= 32) max_w &= ~31ll;  // a worker's column of cells is W rounded up to 32, plus 6
@@ -832,6 +832,27 @@ PullPlan make_pull_plan(const HashSet& hs, int64_t d, int32_t P, int32_t r, int6
       const int64_t w2 = (c + per_row - 1) / per_row;
       if (w2 >= 1 && w2 <= W) W = w2;
     }
+  } else {
+    // One round: tiles x list segments (below) take the workgroup slots. With few wide tiles
+    // (one or two workers: up to 20,448 columns) the segments alone leave CUs idle (65 tiles
+    // x 3 segments = 195 of 256 slots at d = 25.6M, P = 1), so narrower tiles are taken while
+    // they fill more slots, as long as a tile keeps at least one 16 Ki-entry segment's worth:
+    // the fewest tiles within 3% of a full round, else the fullest.
+    const int64_t tpr0 = (c + W - 1) / W;
+    int64_t best_tpr = tpr0, best_items = 0;
+    for (int64_t tpr = tpr0; tpr <= c && (int64_t)r * tpr <= slots; ++tpr) {
+      const int64_t T = (int64_t)r * tpr;
+      if (tpr > tpr0 && (int64_t)r * d / T < 16384) break;
+      int64_t S = slots / T;
+      if (S > (int64_t)r * d / T / 16384) S = (int64_t)r * d / T / 16384;
+      if (S < 1) S = 1;
+      if (T * S > best_items) {
+        best_items = T * S;
+        best_tpr = tpr;
+      }
+      if (T * S * 100 >= slots * 97) break;
+    }
+    W = (c + best_tpr - 1) / best_tpr;
   }
   pl.W = (int32_t)W;
   {
