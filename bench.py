@@ -39,6 +39,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MI355X_CUS = 256  # compute units (the library reads the device's own count)
 METRIC = "gradient coords/sec per full sketch+unsketch+top-k step; % of HBM peak"
 
 
@@ -131,11 +132,13 @@ def stage_kernels(w, layout: str = "interleaved", plan: dict = None) -> dict:
     else:
         acc = [f"k_vi_il<{w.P}, true>"]
     tail = ["k_digit2", "k_select2", "k_mark", "k_emit"]
+    # the full estimate's form: two coordinates per thread per pass up to 8 * 256 * (CUs)
+    unsketch = f"k_unsketch<{w.r}, {2 if w.d <= 8 * 256 * MI355X_CUS else 1}>"
     if w.d * w.r > 2_000_000:  # pruned selection (the library's choice above 2,000,000 cells of d*r)
         select = [f"k_sample<{w.r}, false>", "k_heavy", f"k_pruned<{w.r}, false, 0>", f"k_survivors<{w.r}, false>",
-                  f"k_unsketch<{w.r}>"] + tail
+                  unsketch] + tail
     else:  # every coordinate estimated
-        select = [f"k_unsketch<{w.r}>"] + tail
+        select = [unsketch] + tail
     segmented = plan["segments"] > 1 if plan is not None else w.d <= 1_000_000
     return {
         "accumulate": acc,

@@ -132,7 +132,15 @@ __device__ __forceinline__ bool fallback_needed(SelectCtl* ctl) {
   return fb;
 }
 
-template <int R>
+// k_unsketch's grid. Each block adds its LDS histogram into the global one with an atomic
+// per non-empty bin, and the atomics of many blocks on the few well-filled bins queue at one
+// address each. Up to kUnsketchSmall * kBlock * (CUs) coordinates that queue costs more than
+// the blocks' parallelism gains: at most one block per CU then, each thread taking two
+// coordinates per pass with all their cell loads in flight. Beyond it, four blocks per CU,
+// one coordinate per thread per pass.
+constexpr int kUnsketchSmall = 8;
+
+template <int R, int U>
 __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __restrict__ merged, int64_t d,
                                                      float* __restrict__ est, uint32_t* __restrict__ keys,
                                                      uint32_t* __restrict__ hist, uint32_t* __restrict__ bitmap,
@@ -154,22 +162,32 @@ __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __
     db[j] = mod_mersenne_affine(kr[j].a, 0u, (uint32_t)stride);
     dsg[j] = mod_mersenne_affine(kr[j].a2, 0u, (uint32_t)stride);
   }
-  for (int64_t i = i0; i < d; i += stride) {
-    float val[R];
+  // U coordinates (i, i + stride, ...) per pass with all their cell loads in flight; a cell
+  // column is valid for any hash value, so the loads past d need no guard
+  for (int64_t ib = i0; ib < d; ib += U * stride) {
+    float val[U][R];
 #pragma unroll
-    for (int j = 0; j < R; ++j) {
-      const uint32_t col = mod_c(hb[j], kr[j].c, kr[j].magic, kr[j].shift);
-      val[j] = apply_sign(merged[(int64_t)j * hs.c + col], sign_flip_of(hsg[j]));
-      hb[j] = add_mod_mersenne(hb[j], db[j]);
-      hsg[j] = add_mod_mersenne(hsg[j], dsg[j]);
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int j = 0; j < R; ++j) {
+        const uint32_t col = mod_c(hb[j], kr[j].c, kr[j].magic, kr[j].shift);
+        val[u][j] = apply_sign(merged[(int64_t)j * hs.c + col], sign_flip_of(hsg[j]));
+        hb[j] = add_mod_mersenne(hb[j], db[j]);
+        hsg[j] = add_mod_mersenne(hsg[j], dsg[j]);
+      }
     }
-    sort_net<R>(val);
-    const float e = median_sorted<R>(val);
-    if (est) est[i] = e;
-    const uint32_t key = abs_key(e);
-    keys[i] = key;
-    atomicAdd(&h[key >> kDigit1Shift], 1u);
-    if ((i & 31) == 0) bitmap[i >> 5] = 0u;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t i = ib + u * stride;
+      if (i >= d) break;
+      sort_net<R>(val[u]);
+      const float e = median_sorted<R>(val[u]);
+      if (est) est[i] = e;
+      const uint32_t key = abs_key(e);
+      keys[i] = key;
+      atomicAdd(&h[key >> kDigit1Shift], 1u);
+      if ((i & 31) == 0) bitmap[i >> 5] = 0u;
+    }
   }
   __syncthreads();
   for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) {
@@ -1132,8 +1150,12 @@ __global__ void k_hm_out(const SelectCtl* __restrict__ ctl, int64_t* __restrict_
 template <int R>
 void launch_unsketch_r(const HashSet& hs, int64_t d, int num_cus, const SelectBufs& b, hipStream_t s,
                        const float* merged, float* est, SelectCtl* gate) {
-  hipLaunchKernelGGL(k_unsketch<R>, dim3(grid_for(d, kBlock, 4 * num_cus)), dim3(kBlock), 0, s, hs, merged, d, est,
-                     b.cand_key, b.hist, b.bitmap, gate);
+  if (d <= (int64_t)kUnsketchSmall * kBlock * num_cus)
+    hipLaunchKernelGGL((k_unsketch<R, 2>), dim3(grid_for(d, 2 * kBlock, num_cus)), dim3(kBlock), 0, s, hs, merged, d,
+                       est, b.cand_key, b.hist, b.bitmap, gate);
+  else
+    hipLaunchKernelGGL((k_unsketch<R, 1>), dim3(grid_for(d, kBlock, 4 * num_cus)), dim3(kBlock), 0, s, hs, merged, d,
+                       est, b.cand_key, b.hist, b.bitmap, gate);
 }
 
 template <int R, bool HM>
