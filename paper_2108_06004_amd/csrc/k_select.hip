@@ -1199,9 +1199,11 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
 // unless it fell short of k) or the full estimate's dense ones.
 hipError_t launch_select_tail(int64_t d, int num_cus, const SelectBufs& b, hipStream_t s, int64_t k, int pruned,
                               int32_t* idx) {
-  // one block per CU for the pruned candidates (a few times k); the full estimate's dense
-  // ones (d) get up to eight per CU (a pruned pass's fallback keeps the smaller grid)
-  int g2 = num_cus;
+  // one block per two CUs for the pruned candidates (a few times k: fewer blocks each append
+  // their staged keys and histogram with fewer atomics that queue at the same addresses); the
+  // full estimate's dense ones (d) get up to eight per CU (a pruned pass's fallback keeps the
+  // smaller grid)
+  int g2 = std::max(1, num_cus / 2);
   if (!pruned) g2 = std::max(g2, grid_for(d, 8192, 8 * num_cus));
   hipLaunchKernelGGL(k_digit2, dim3(g2), dim3(kBlock), 0, s, b.cand_key, b.cand_idx, b.ctl, b.cand_cap, d, b.hist_c,
                      b.hist, pruned, (uint32_t)k, b.hist2, b.keys, b.stage_idx, b.bitmap);
