@@ -383,6 +383,31 @@ def test_all_zero_large_dense_survivors():
     dv.close()
 
 
+@pytest.mark.parametrize("mode", ["pruned", "full"])
+@pytest.mark.parametrize("d,c,k", [(60_000, 600, 150), (200_000, 40, 7000)])
+def test_tie_cut_inside_equal_keys(monkeypatch, d, c, k, mode):
+    # one sketch row: every coordinate of a cell has the same |estimate|, so the keys come in
+    # runs of about d / c equal values and the k-th falls inside one. About 100 equal keys
+    # (the ties ranked in LDS) and about 5,000 (the index-digit cut); the selection takes the
+    # lowest coordinates of the cut run
+    monkeypatch.setenv("GS_SELECT_PATH", mode)
+    P, r = 2, 1
+    hp = synth.hash_params(synth.BASE_SEED + 31 + c, r)
+    rng = np.random.default_rng(d + c)
+    dv = Dev(d, P, r, c, k, hp, 0.9)
+    g = rng.integers(-50, 51, (P, d)).astype(np.float32)
+    z = np.zeros_like(g)
+    # premise, from the oracle: the k-th key's run is cut, and it is short or long as intended
+    u1, v1 = z.copy(), z.copy()
+    oracle.accumulate(g, u1, v1, 0.9)
+    a = np.abs(oracle.unsketch(oracle.merge(oracle.sketch(v1, hp, c)), hp, d))
+    tau = np.sort(a)[::-1][k - 1]
+    n_eq, above = int(np.count_nonzero(a == tau)), int(np.count_nonzero(a > tau))
+    assert above < k < above + n_eq and (n_eq <= 1024) == (c == 600), (n_eq, above)
+    chain_check(dv, g, z, z.copy(), k, 0.9, label=f"tie cut d={d} c={c} k={k} {mode}")
+    dv.close()
+
+
 @pytest.mark.parametrize("d,P,r,c,k", [(10_007, 3, 5, 211, 300), (65_536, 8, 4, 4096, 655), (3001, 17, 5, 97, 60)])
 def test_atomic_sketch_path(monkeypatch, d, P, r, c, k):
     # the fp64-atomic sketch (used when the tile lists cannot be built) through every entry
