@@ -39,7 +39,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-MI355X_CUS = 256  # compute units (the library reads the device's own count)
+MI355X_CUS = 256  # compute units, when no device is visible to ask
 METRIC = "gradient coords/sec per full sketch+unsketch+top-k step; % of HBM peak"
 
 
@@ -120,6 +120,18 @@ def kernel_source_file(name: str):
     return None
 
 
+def num_cus() -> int:
+    """Compute units of device 0 (the library sizes its grids by the device's count)."""
+    try:
+        import torch
+
+        if torch.cuda.is_available():
+            return torch.cuda.get_device_properties(0).multi_processor_count
+    except Exception:
+        pass
+    return MI355X_CUS
+
+
 def stage_kernels(w, layout: str = "interleaved", plan: dict = None) -> dict:
     """The kernels each stage of the fused step launches (names as rocprofv3 reports them).
     `plan` is the context's gs_describe; without it the library's size rule is assumed (list
@@ -133,7 +145,7 @@ def stage_kernels(w, layout: str = "interleaved", plan: dict = None) -> dict:
         acc = [f"k_vi_il<{w.P}, true>"]
     tail = ["k_digit2", "k_select2", "k_mark", "k_emit"]
     # the full estimate's form: two coordinates per thread per pass up to 8 * 256 * (CUs)
-    unsketch = f"k_unsketch<{w.r}, {2 if w.d <= 8 * 256 * MI355X_CUS else 1}>"
+    unsketch = f"k_unsketch<{w.r}, {2 if w.d <= 8 * 256 * num_cus() else 1}>"
     if w.d * w.r > 2_000_000:  # pruned selection (the library's choice above 2,000,000 cells of d*r)
         select = [f"k_sample<{w.r}, false>", "k_heavy", f"k_pruned<{w.r}, false, 0>", f"k_survivors<{w.r}, false>",
                   unsketch] + tail
