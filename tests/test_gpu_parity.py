@@ -383,6 +383,26 @@ def test_all_zero_large_dense_survivors():
     dv.close()
 
 
+@pytest.mark.parametrize("extra", [0, 1])
+def test_full_estimate_forms_at_their_boundary(extra):
+    # the full estimate takes two coordinates per thread and pass on at most one workgroup per
+    # CU up to 8 * 256 * (CUs) coordinates, and one per thread on four workgroups per CU
+    # beyond: both forms at the boundary, estimates bit-exact, the top-k exact
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    d = 8 * 256 * cus + extra
+    r, c, k = 3, 5_003, 777
+    hp = synth.hash_params(synth.BASE_SEED + 41 + extra, r)
+    merged = np.random.default_rng(41 + extra).standard_normal((r, c)).astype(np.float32)
+    ctx = gs.GsContext(d, 1, r, c, k, hp)
+    est = torch.empty(d, dtype=torch.float32, device=DEV)
+    idx = torch.empty(k, dtype=torch.int32, device=DEV)
+    ctx.unsketch_topk(to_dev(merged), k, idx, est)
+    e = host(est)
+    assert np.array_equal(e, oracle.unsketch(merged, hp, d)), f"d={d}: estimates not exact"
+    assert np.array_equal(host(idx), oracle.topk(e, k)[0]), f"d={d}: top-k not exact"
+    ctx.close()
+
+
 @pytest.mark.parametrize("mode", ["pruned", "full"])
 @pytest.mark.parametrize("d,c,k", [(60_000, 600, 150), (200_000, 40, 7000)])
 def test_tie_cut_inside_equal_keys(monkeypatch, d, c, k, mode):
