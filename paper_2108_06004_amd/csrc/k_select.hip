@@ -821,10 +821,13 @@ __global__ void __launch_bounds__(kPruneBlock) k_pruned(HashSet hs, int64_t d, S
   }
 }
 
-constexpr int kSurvBuf = 2048;  // per-block LDS candidate buffer of k_survivors
+// k_survivors: two blocks of 512 threads per CU (25.6M x 8: 15.8-16.1 us; one block of 256, 512
+// or 1024 threads per CU: 18.8, 17.0, 18.8 us; four of 512: 17.9 us)
+constexpr int kSurvBlock = 512;
+constexpr int kSurvBuf = 2048;  // per-block LDS candidate buffer of k_survivors (at least 2 * kSurvBlock)
 
 template <int R, bool HM>
-__global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* __restrict__ merged,
+__global__ void __launch_bounds__(kSurvBlock) k_survivors(HashSet hs, const float* __restrict__ merged,
                                                       SelectCtl* __restrict__ ctl, const uint32_t* __restrict__ queue,
                                                       uint32_t* __restrict__ cand_key, int32_t* __restrict__ cand_idx,
                                                       int64_t cap, const uint32_t* __restrict__ rnd,
@@ -833,7 +836,7 @@ __global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* _
   __shared__ int32_t bidx[kSurvBuf];
   __shared__ uint32_t h[kDigit1Bins];
   __shared__ uint32_t bn, gbase, nheavy;
-  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) h[b] = 0u;
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kSurvBlock) h[b] = 0u;
   RowConst kr[R];
 #pragma unroll
   for (int j = 0; j < R; ++j) kr[j] = row_const(hs, j);
@@ -847,8 +850,8 @@ __global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* _
   }
   __syncthreads();
   uint32_t mine = 0;
-  const int64_t stride = (int64_t)gridDim.x * kBlock;
-  for (int64_t t0 = (int64_t)blockIdx.x * kBlock; t0 < n; t0 += stride) {  // block-uniform trip count
+  const int64_t stride = (int64_t)gridDim.x * kSurvBlock;
+  for (int64_t t0 = (int64_t)blockIdx.x * kSurvBlock; t0 < n; t0 += stride) {  // block-uniform trip count
     const int64_t t = t0 + threadIdx.x;
     bool cand = false;
     uint32_t key = 0u, i = 0u;
@@ -866,7 +869,7 @@ __global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* _
       }
     }
     hist_add(h, cand, key >> kDigit1Shift);
-    // block-local append (one LDS atomic per wave); at most kBlock per pass, so the buffer,
+    // block-local append (one LDS atomic per wave); at most kSurvBlock per pass, so the buffer,
     // flushed whenever it is half full, never overflows
     const uint64_t bal = __ballot(cand);
     uint32_t wbase = 0u;
@@ -883,7 +886,7 @@ __global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* _
       if (threadIdx.x == 0) gbase = atomicAdd(&ctl->n_cand, nb);
       __syncthreads();
       const int64_t g0 = gbase;
-      for (uint32_t u = threadIdx.x; u < nb; u += kBlock) {
+      for (uint32_t u = threadIdx.x; u < nb; u += kSurvBlock) {
         if (g0 + u < cap) {
           cand_key[g0 + u] = bkey[u];
           cand_idx[g0 + u] = bidx[u];
@@ -901,7 +904,7 @@ __global__ void __launch_bounds__(kBlock) k_survivors(HashSet hs, const float* _
   if constexpr (HM) {
     if (threadIdx.x == 0 && nheavy) atomicAdd(&ctl->n_heavy, (unsigned long long)nheavy);
   }
-  for (int b = threadIdx.x; b < kDigit1Bins; b += kBlock) {
+  for (int b = threadIdx.x; b < kDigit1Bins; b += kSurvBlock) {
     const uint32_t c = h[b];
     if (c) atomicAdd(&hist_c[b], c);
   }
@@ -1191,7 +1194,7 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
                        x->heavy, x->heavy, x->prune_map_words, x->heavy_row, 0, x->prune_buf_cap, x->keys,
                        x->bitmap, rnd, x->hist_s);
   }
-  hipLaunchKernelGGL((k_survivors<R, HM>), dim3(x->num_cus), dim3(kBlock), 0, s, x->hs, merged, x->ctl, x->keys,
+  hipLaunchKernelGGL((k_survivors<R, HM>), dim3(2 * x->num_cus), dim3(kSurvBlock), 0, s, x->hs, merged, x->ctl, x->keys,
                      x->cand_key, x->cand_idx, x->cand_cap, rnd, x->hist_c);
 }
 
