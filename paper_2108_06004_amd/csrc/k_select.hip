@@ -204,7 +204,8 @@ __global__ void __launch_bounds__(kBlock) k_unsketch(HashSet hs, const float* __
 
 constexpr int kSelUnroll = 8;    // candidate loads in flight per thread
 constexpr int kTieMax = 1024;    // ties at the k-th key resolved by ranking in LDS (else radix digits)
-constexpr int kStageBuf = 2048;  // per-block LDS buffer of k_digit2 (keys and coordinates)
+constexpr int kDigit2Block = 1024;              // threads per k_digit2 block
+constexpr int kStageBuf = 8 * kDigit2Block;  // per-block LDS buffer of k_digit2 (keys and coordinates)
 
 __device__ __forceinline__ bool dense_cands(const SelectCtl* ctl, int pruned) {
   return !pruned || ctl->fallback != 0u;
@@ -214,7 +215,7 @@ __device__ __forceinline__ bool dense_cands(const SelectCtl* ctl, int pruned) {
 // candidates' histogram (block 0 records it); then the digit-2 histogram of the bucket's
 // keys (LDS per block, added into hist2) and the bucket compacted, key and coordinate, into
 // stage_key / stage_idx (an LDS buffer per block, one global atomic per flush).
-__global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ cand_key,
+__global__ void __launch_bounds__(kDigit2Block) k_digit2(const uint32_t* __restrict__ cand_key,
                                                    const int32_t* __restrict__ cand_idx,
                                                    SelectCtl* __restrict__ ctl, int64_t cap, int64_t d,
                                                    const uint32_t* __restrict__ hist_c,
@@ -224,34 +225,34 @@ __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ 
   __shared__ uint32_t h[kDigitBins];
   __shared__ uint32_t bkey[kStageBuf];
   __shared__ int32_t bidx[kStageBuf];
-  __shared__ uint32_t shw[kBlock / 64];
+  __shared__ uint32_t shw[kDigit2Block / 64];
   __shared__ uint32_t res[2];
   __shared__ uint32_t bn, gbase;
   const bool dense = dense_cands(ctl, pruned);
   const int64_t n = dense ? d : (ctl->n_cand < (uint64_t)cap ? (int64_t)ctl->n_cand : cap);
-  find_bucket<kBlock, kDigit1Bins>(dense ? hist : hist_c, true, k, shw, res);
+  find_bucket<kDigit2Block, kDigit1Bins>(dense ? hist : hist_c, true, k, shw, res);
   const uint32_t b1 = res[0];
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     ctl->b1 = res[0];
     ctl->above1 = res[1];
   }
   const int lane = threadIdx.x & 63;
-  for (int b = threadIdx.x; b < kDigitBins; b += kBlock) h[b] = 0u;
+  for (int b = threadIdx.x; b < kDigitBins; b += kDigit2Block) h[b] = 0u;
   if (threadIdx.x == 0) bn = 0u;
   __syncthreads();
   const int64_t per = (n + gridDim.x - 1) / gridDim.x;
   const int64_t lo = (int64_t)blockIdx.x * per, hi = min(n, lo + per);
   constexpr int V = 4;
-  for (int64_t c0 = lo; c0 < hi; c0 += (int64_t)V * kBlock) {  // block-uniform
+  for (int64_t c0 = lo; c0 < hi; c0 += (int64_t)V * kDigit2Block) {  // block-uniform
     uint32_t key[V];
 #pragma unroll
     for (int m = 0; m < V; ++m) {
-      const int64_t t = c0 + (int64_t)m * kBlock + threadIdx.x;
+      const int64_t t = c0 + (int64_t)m * kDigit2Block + threadIdx.x;
       key[m] = t < hi ? cand_key[t] : 0u;
     }
 #pragma unroll
     for (int m = 0; m < V; ++m) {
-      const int64_t t = c0 + (int64_t)m * kBlock + threadIdx.x;
+      const int64_t t = c0 + (int64_t)m * kDigit2Block + threadIdx.x;
       const uint32_t d1 = key[m] >> kDigit1Shift;
       if (t < hi && d1 > b1) {  // above the k-th key's bucket: taken
         const uint32_t ix = dense ? (uint32_t)t : (uint32_t)cand_idx[t];
@@ -270,12 +271,12 @@ __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ 
       }
     }
     __syncthreads();
-    const uint32_t nb = bn;  // < kStageBuf / 2 + V * kBlock <= kStageBuf
-    if (nb >= (uint32_t)(kStageBuf / 2) || (c0 + (int64_t)V * kBlock >= hi && nb > 0)) {
+    const uint32_t nb = bn;  // < kStageBuf / 2 + V * kDigit2Block <= kStageBuf
+    if (nb >= (uint32_t)(kStageBuf / 2) || (c0 + (int64_t)V * kDigit2Block >= hi && nb > 0)) {
       if (threadIdx.x == 0) gbase = atomicAdd(&ctl->n_stage2, nb);
       __syncthreads();
       const uint32_t g0 = gbase;
-      for (uint32_t t = threadIdx.x; t < nb; t += kBlock) {
+      for (uint32_t t = threadIdx.x; t < nb; t += kDigit2Block) {
         stage_key[g0 + t] = bkey[t];
         stage_idx[g0 + t] = bidx[t];
       }
@@ -284,7 +285,7 @@ __global__ void __launch_bounds__(kBlock) k_digit2(const uint32_t* __restrict__ 
     }
     __syncthreads();
   }
-  for (int b = threadIdx.x; b < kDigitBins; b += kBlock) {
+  for (int b = threadIdx.x; b < kDigitBins; b += kDigit2Block) {
     const uint32_t c = h[b];
     if (c) atomicAdd(&hist2[b], c);
   }
@@ -1202,13 +1203,13 @@ void launch_prune_r(gs_ctx* x, hipStream_t s, const float* merged, int64_t k, co
 // unless it fell short of k) or the full estimate's dense ones.
 hipError_t launch_select_tail(int64_t d, int num_cus, const SelectBufs& b, hipStream_t s, int64_t k, int pruned,
                               int32_t* idx) {
-  // one block per two CUs for the pruned candidates (a few times k: fewer blocks each append
-  // their staged keys and histogram with fewer atomics that queue at the same addresses); the
-  // full estimate's dense ones (d) get up to eight per CU (a pruned pass's fallback keeps the
-  // smaller grid)
-  int g2 = std::max(1, num_cus / 2);
+  // one block (of 1,024 threads) per four CUs for the pruned candidates (a few times k: fewer
+  // blocks each append their staged keys and histogram with fewer atomics that queue at the
+  // same addresses); the full estimate's dense ones (d) get up to 8 * (CUs) blocks (a pruned
+  // pass's fallback keeps the smaller grid)
+  int g2 = std::max(1, num_cus / 4);
   if (!pruned) g2 = std::max(g2, grid_for(d, 8192, 8 * num_cus));
-  hipLaunchKernelGGL(k_digit2, dim3(g2), dim3(kBlock), 0, s, b.cand_key, b.cand_idx, b.ctl, b.cand_cap, d, b.hist_c,
+  hipLaunchKernelGGL(k_digit2, dim3(g2), dim3(kDigit2Block), 0, s, b.cand_key, b.cand_idx, b.ctl, b.cand_cap, d, b.hist_c,
                      b.hist, pruned, (uint32_t)k, b.hist2, b.keys, b.stage_idx, b.bitmap);
   hipLaunchKernelGGL(k_select2, dim3(1), dim3(kSelBlock), 0, s, b.ctl, b.hist2, b.keys, b.stage_idx, b.hist_c, b.hist,
                      pruned, (uint32_t)k, b.emit_flags, b.emit_blocks);
